@@ -1,0 +1,566 @@
+/*
+ * NITI CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, exact restatement of what the integer-training method of
+ * "Training Integer Neural Networks Using Integer-only Arithmetic" (NITI)
+ * computes on its hot path.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or helper with the HIP library; the two meet only through
+ * the seeded input generator, which holds none of the method's arithmetic.
+ *
+ * Conventions
+ *   - Every contraction is summed exactly in int64, then reduced to the
+ *     int32 accumulator the method stores (two's complement, mod 2^32).
+ *     A sum whose magnitude reaches 2^31 raises ORC_FLAG_ACC_BOUND.
+ *   - Tensors are NCHW (activations, errors) and KCRS (weights), the
+ *     convention the method's layer equations are usually written in.
+ *   - No blocking, fusion or reordering beyond the definitions.  The outer
+ *     loops over independent output elements are split across OpenMP
+ *     threads; each element's sum is formed in its natural index order.
+ *
+ * Readings of points the method leaves open (all listed in the design notes):
+ *   R1 effective bitwidth counts magnitude bits only: B(v) = bitlen(max|v|).
+ *   R2 a rounded magnitude that would reach 128 is held at 127.
+ *   R3 |INT32_MIN| is the magnitude 2^31 (uint32), so B = 32.
+ *   R4 the integer weight update saturates to [-127, 127].
+ *   R5 ReLU in the forward pass acts on the int32 accumulator before the
+ *      block exponent is found; the backward ReLU mask acts on the rounded
+ *      int8 error (it does not change that error's exponent).
+ *   R6 the loss offset p is max(xhat) - 10.
+ *   R7 the loss constant is 47274 (the decimal value printed; the hex
+ *      spelling next to it is 47272).
+ *   R8 xhat is an arithmetic (flooring) shift by 15 - s_a.
+ *   R9 the Taylor branch of the loss is formed exactly in int64 at the
+ *      smallest scale that makes every term an integer, 2^(1-2 s_a); below
+ *      s_a = -22 that no longer fits, and s_a is held at -22 with a flag.
+ */
+#include <stdint.h>
+#include <string.h>
+#include <stdlib.h>
+
+#define ORC_FLAG_ACC_BOUND 1   /* an exact sum left the int32 range      */
+#define ORC_FLAG_EXP_RANGE 2   /* an int8 block exponent left [-128,127] */
+#define ORC_FLAG_LOSS_SA   4   /* loss s_a below the int64 Taylor range  */
+
+typedef struct orc_stats {
+    uint64_t max_abs; /* max magnitude over the whole tensor            */
+    int32_t b;        /* effective bitwidth of that maximum             */
+    int32_t bp;       /* binary point (shift) applied                    */
+    int32_t flags;    /* ORC_FLAG_* bits                                 */
+    int32_t s_out;    /* output block exponent (when one is formed)     */
+} orc_stats;
+
+/* ------------------------------------------------------------------ */
+/* Section 3.2: effective bitwidth B(V) -- bits needed for the maximum. */
+int orc_bitlen(uint64_t m)
+{
+    int b = 0;
+    while (m) {
+        b++;
+        m >>= 1;
+    }
+    return b;
+}
+
+static uint64_t mag64(int64_t v)
+{
+    /* |v| as an unsigned value; exact for INT64_MIN as well. */
+    return v < 0 ? (uint64_t)0 - (uint64_t)v : (uint64_t)v;
+}
+
+/* ------------------------------------------------------------------ */
+/* Algorithm 3 (Section 3.4): pseudo stochastic rounding of a fixed point
+ * value <q.f> with bp fraction bits.  q is the integer part of |v|, f the
+ * fraction.  For odd bp the lowest fraction bit is dropped; then the upper
+ * half of f is compared with the lower half, which serves as the random
+ * draw, and q is bumped when the upper half is strictly larger.  The sign
+ * of v is applied last.  Reading R2: a magnitude of 128 is held at 127;
+ * the same hold applies when a caller-given bp leaves more than 7 bits. */
+int64_t orc_psr(int64_t v, int bp)
+{
+    uint64_t x = mag64(v);
+    uint64_t q, f, thi, rlo;
+    int nb, h;
+    if (bp <= 0) {
+        q = x;
+    } else {
+        q = x >> bp;
+        f = x & ((bp >= 64) ? ~(uint64_t)0 : (((uint64_t)1 << bp) - 1));
+        nb = bp;
+        if (nb & 1) {
+            f >>= 1;
+            nb -= 1;
+        }
+        h = nb / 2;
+        thi = f >> h;
+        rlo = f & (((uint64_t)1 << h) - 1);
+        if (thi > rlo)
+            q += 1;
+    }
+    if (q > 127)
+        q = 127;
+    return v < 0 ? -(int64_t)q : (int64_t)q;
+}
+
+/* Round to nearest, ties away from zero on the magnitude: the rounding the
+ * experiments used for activations and errors (Section 4.3). */
+int64_t orc_rtn(int64_t v, int bp)
+{
+    uint64_t x = mag64(v);
+    uint64_t q;
+    if (bp <= 0) {
+        q = x;
+    } else {
+        q = x >> bp;
+        if ((x >> (bp - 1)) & 1)
+            q += 1;
+    }
+    if (q > 127)
+        q = 127;
+    return v < 0 ? -(int64_t)q : (int64_t)q;
+}
+
+static int64_t round_one(int64_t v, int bp, int mode)
+{
+    return mode == 1 ? orc_rtn(v, bp) : orc_psr(v, bp);
+}
+
+/* ------------------------------------------------------------------ */
+/* Accumulator reduction: the exact sum kept as the int32 the method
+ * accumulates in (Section 3.2), two's complement. */
+static int32_t wrap32(int64_t s, int32_t *flags)
+{
+    if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
+        *flags |= ORC_FLAG_ACC_BOUND;
+    return (int32_t)(uint32_t)(uint64_t)s;
+}
+
+/* Algorithms 1 and 2: block exponent of a whole tensor and shift-and-round.
+ * max |v| (uint64 magnitude) -> b = B(max) -> bp = max(0, b - target) ->
+ * every element rounded with that one bp.  Returns bp. */
+int orc_shift_round_i64(const int64_t *v, int64_t n, int target, int mode,
+                        int8_t *out, orc_stats *st)
+{
+    uint64_t mx = 0;
+    int64_t i;
+    int b, bp;
+    for (i = 0; i < n; i++) {
+        uint64_t m = mag64(v[i]);
+        if (m > mx)
+            mx = m;
+    }
+    b = orc_bitlen(mx);
+    bp = b - target;
+    if (bp < 0)
+        bp = 0;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < n; i++)
+        out[i] = (int8_t)round_one(v[i], bp, mode);
+    if (st) {
+        st->max_abs = mx;
+        st->b = b;
+        st->bp = bp;
+    }
+    return bp;
+}
+
+/* Same on an int32 tensor (accumulators, gradients). */
+int orc_shift_round_i32(const int32_t *v, int64_t n, int target, int mode,
+                        int8_t *out, orc_stats *st)
+{
+    uint64_t mx = 0;
+    int64_t i;
+    int b, bp;
+    for (i = 0; i < n; i++) {
+        uint64_t m = mag64((int64_t)v[i]);
+        if (m > mx)
+            mx = m;
+    }
+    b = orc_bitlen(mx);
+    bp = b - target;
+    if (bp < 0)
+        bp = 0;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < n; i++)
+        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode);
+    if (st) {
+        st->max_abs = mx;
+        st->b = b;
+        st->bp = bp;
+    }
+    return bp;
+}
+
+/* Round with a caller-given binary point (no block exponent search). */
+void orc_round_fixed_i32(const int32_t *v, int64_t n, int bp, int mode, int8_t *out)
+{
+    int64_t i;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < n; i++)
+        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode);
+}
+
+/* Algorithm 2, exponent line: s_q = s_q32 + bp, with s_q32 = s_a + s_w
+ * (Section 3.1: the product's exponent is the sum of the operands').  The
+ * result is an int8; leaving its range raises ORC_FLAG_EXP_RANGE and the
+ * value is held at the nearest end. */
+int orc_out_exponent(int s_a, int s_w, int bp, int32_t *flags)
+{
+    int s = s_a + s_w + bp;
+    if (s > 127) {
+        *flags |= ORC_FLAG_EXP_RANGE;
+        s = 127;
+    }
+    if (s < -128) {
+        *flags |= ORC_FLAG_EXP_RANGE;
+        s = -128;
+    }
+    return s;
+}
+
+/* ------------------------------------------------------------------ */
+/* Int8MatrixMultiply (Algorithm 1) in its plain matrix form:
+ * S[m][n] = sum_k A[m][k] * B[n][k]  (A is M x K, B is N x K, row-major). */
+void orc_gemm_nt_raw(const int8_t *A, const int8_t *B, int64_t M, int64_t N,
+                     int64_t K, int64_t *S)
+{
+    int64_t m;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (m = 0; m < M; m++) {
+        const int8_t *a = A + m * K;
+        int64_t n, k;
+        for (n = 0; n < N; n++) {
+            const int8_t *b = B + n * K;
+            int64_t s = 0;
+            for (k = 0; k < K; k++)
+                s += (int64_t)a[k] * (int64_t)b[k];
+            S[m * N + n] = s;
+        }
+    }
+}
+
+/* Same sums for a chosen set of output elements only: (rows[i], cols[i]). */
+void orc_gemm_nt_pick(const int8_t *A, const int8_t *B, int64_t K,
+                      const int64_t *rows, const int64_t *cols, int64_t cnt,
+                      int64_t *S)
+{
+    int64_t i;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < cnt; i++) {
+        const int8_t *a = A + rows[i] * K;
+        const int8_t *b = B + cols[i] * K;
+        int64_t s = 0, k;
+        for (k = 0; k < K; k++)
+            s += (int64_t)a[k] * (int64_t)b[k];
+        S[i] = s;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Convolution, Section 3.2 (reduced to matrix products by implicit GEMM in
+ * the method; here written directly from its definition).
+ *   x  [N][C][H][W], w [K][C][R][S], y [N][K][P][Q]
+ *   P = (H + 2 ph - R) / sh + 1,  Q = (W + 2 pw - S) / sw + 1
+ *   y[n][k][p][q] = sum_{c,r,s} w[k][c][r][s] * x[n][c][p sh - ph + r][q sw - pw + s]
+ * with x outside the image taken as zero. */
+typedef struct orc_conv {
+    int64_t n, c, h, w, k, r, s;
+    int64_t sh, sw, ph, pw;
+} orc_conv;
+
+static int64_t out_dim(int64_t in, int64_t pad, int64_t ker, int64_t st)
+{
+    return (in + 2 * pad - ker) / st + 1;
+}
+
+void orc_conv_fwd_raw(const orc_conv *d, const int8_t *x, const int8_t *w, int64_t *y)
+{
+    const int64_t P = out_dim(d->h, d->ph, d->r, d->sh);
+    const int64_t Q = out_dim(d->w, d->pw, d->s, d->sw);
+    int64_t nk;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (nk = 0; nk < d->n * d->k; nk++) {
+        const int64_t n = nk / d->k, k = nk % d->k;
+        int64_t p, q, c, r, s;
+        for (p = 0; p < P; p++)
+            for (q = 0; q < Q; q++) {
+                int64_t acc = 0;
+                for (c = 0; c < d->c; c++)
+                    for (r = 0; r < d->r; r++)
+                        for (s = 0; s < d->s; s++) {
+                            const int64_t hh = p * d->sh - d->ph + r;
+                            const int64_t ww = q * d->sw - d->pw + s;
+                            if (hh < 0 || hh >= d->h || ww < 0 || ww >= d->w)
+                                continue;
+                            acc += (int64_t)w[((k * d->c + c) * d->r + r) * d->s + s] *
+                                   (int64_t)x[((n * d->c + c) * d->h + hh) * d->w + ww];
+                        }
+                y[((n * d->k + k) * P + p) * Q + q] = acc;
+            }
+    }
+}
+
+/* Error back-propagation, e(l-1) = w(l) (x) e(l) (Algorithm 1): the exact
+ * adjoint of the forward convolution with respect to x.
+ *   dx[n][c][h][w] = sum over (k, r, s) with h + ph - r = p sh, w + pw - s = q sw,
+ *                    0 <= p < P, 0 <= q < Q, of w[k][c][r][s] * dy[n][k][p][q] */
+void orc_conv_bwd_data_raw(const orc_conv *d, const int8_t *dy, const int8_t *w, int64_t *dx)
+{
+    const int64_t P = out_dim(d->h, d->ph, d->r, d->sh);
+    const int64_t Q = out_dim(d->w, d->pw, d->s, d->sw);
+    int64_t nc;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (nc = 0; nc < d->n * d->c; nc++) {
+        const int64_t n = nc / d->c, c = nc % d->c;
+        int64_t hh, ww, k, r, s;
+        for (hh = 0; hh < d->h; hh++)
+            for (ww = 0; ww < d->w; ww++) {
+                int64_t acc = 0;
+                for (k = 0; k < d->k; k++)
+                    for (r = 0; r < d->r; r++)
+                        for (s = 0; s < d->s; s++) {
+                            const int64_t ph = hh + d->ph - r, pw = ww + d->pw - s;
+                            int64_t p, q;
+                            if (ph < 0 || pw < 0 || ph % d->sh || pw % d->sw)
+                                continue;
+                            p = ph / d->sh;
+                            q = pw / d->sw;
+                            if (p >= P || q >= Q)
+                                continue;
+                            acc += (int64_t)w[((k * d->c + c) * d->r + r) * d->s + s] *
+                                   (int64_t)dy[((n * d->k + k) * P + p) * Q + q];
+                        }
+                dx[((n * d->c + c) * d->h + hh) * d->w + ww] = acc;
+            }
+    }
+}
+
+/* Weight gradient g(l) = a(l-1) (x) e(l) (Algorithm 1; Section 3.3): the
+ * exact adjoint of the forward convolution with respect to w.
+ *   g[k][c][r][s] = sum_{n,p,q} dy[n][k][p][q] * x[n][c][p sh - ph + r][q sw - pw + s] */
+void orc_conv_bwd_weight_raw(const orc_conv *d, const int8_t *x, const int8_t *dy, int64_t *g)
+{
+    const int64_t P = out_dim(d->h, d->ph, d->r, d->sh);
+    const int64_t Q = out_dim(d->w, d->pw, d->s, d->sw);
+    int64_t kc;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (kc = 0; kc < d->k * d->c; kc++) {
+        const int64_t k = kc / d->c, c = kc % d->c;
+        int64_t r, s, n, p, q;
+        for (r = 0; r < d->r; r++)
+            for (s = 0; s < d->s; s++) {
+                int64_t acc = 0;
+                for (n = 0; n < d->n; n++)
+                    for (p = 0; p < P; p++)
+                        for (q = 0; q < Q; q++) {
+                            const int64_t hh = p * d->sh - d->ph + r;
+                            const int64_t ww = q * d->sw - d->pw + s;
+                            if (hh < 0 || hh >= d->h || ww < 0 || ww >= d->w)
+                                continue;
+                            acc += (int64_t)dy[((n * d->k + k) * P + p) * Q + q] *
+                                   (int64_t)x[((n * d->c + c) * d->h + hh) * d->w + ww];
+                        }
+                g[((k * d->c + c) * d->r + r) * d->s + s] = acc;
+            }
+    }
+}
+
+/* One forward output element, for sampled checks of large layers. */
+int64_t orc_conv_fwd_one(const orc_conv *d, const int8_t *x, const int8_t *w,
+                         int64_t n, int64_t k, int64_t p, int64_t q)
+{
+    int64_t acc = 0, c, r, s;
+    for (c = 0; c < d->c; c++)
+        for (r = 0; r < d->r; r++)
+            for (s = 0; s < d->s; s++) {
+                const int64_t hh = p * d->sh - d->ph + r;
+                const int64_t ww = q * d->sw - d->pw + s;
+                if (hh < 0 || hh >= d->h || ww < 0 || ww >= d->w)
+                    continue;
+                acc += (int64_t)w[((k * d->c + c) * d->r + r) * d->s + s] *
+                       (int64_t)x[((n * d->c + c) * d->h + hh) * d->w + ww];
+            }
+    return acc;
+}
+
+/* ------------------------------------------------------------------ */
+/* Composite steps, each the method's sequence for one layer.           */
+
+/* Exact sums -> int32 accumulators (flagging the bound) -> optional ReLU
+ * (reading R5) -> block exponent -> rounding with target bits.  `acc32`
+ * receives the int32 accumulators (after ReLU) when non-NULL. */
+void orc_finish_i64(const int64_t *S, int64_t n, int relu, int target, int mode,
+                    int8_t *out, int32_t *acc32, orc_stats *st)
+{
+    int32_t flags = 0;
+    int32_t *a = acc32 ? acc32 : (int32_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    int64_t i;
+    for (i = 0; i < n; i++) {
+        int32_t v = wrap32(S[i], &flags);
+        if (relu && v < 0)
+            v = 0;
+        a[i] = v;
+    }
+    orc_shift_round_i32(a, n, target, mode, out, st);
+    if (st)
+        st->flags |= flags;
+    if (!acc32)
+        free(a);
+}
+
+/* Section 3.3 / Algorithm 1: the discrete update.  b = B(g32),
+ * g = round(g32, max(0, b - mu)), w <- w - g held to [-127, 127] (R4). */
+void orc_sgd_update(int8_t *w, const int32_t *g32, int64_t n, int mu, int mode,
+                    orc_stats *st)
+{
+    int8_t *g = (int8_t *)malloc((size_t)(n > 0 ? n : 1));
+    int64_t i;
+    orc_shift_round_i32(g32, n, mu, mode, g, st);
+    for (i = 0; i < n; i++) {
+        int v = (int)w[i] - (int)g[i];
+        if (v > 127)
+            v = 127;
+        if (v < -127)
+            v = -127;
+        w[i] = (int8_t)v;
+    }
+    free(g);
+}
+
+/* ------------------------------------------------------------------ */
+/* Section 3.5: integer cross-entropy loss gradient for one batch.
+ *   logits a [B][N] (int8) sharing exponent s_a; labels y [B].
+ *   Per sample the unnormalised exponentials t_i are formed, C = sum t_i,
+ *   e32_i = t_i - [i == y] C (the 1/C factor and 2^p are dropped, as the
+ *   method does), then the whole [B][N] tensor gets one block exponent and
+ *   is rounded to int8 with target 7.
+ *   s_a <= -7 (Taylor): t_i = 2^(1-2s_a) + a_i 2^(1-s_a) + a_i^2, i.e.
+ *     (1 + a 2^s_a + a^2 2^(2 s_a) / 2) scaled by 2^(1-2 s_a) (reading R9).
+ *   s_a >  -7 (base 2): xhat_i = floor(47274 a_i 2^(s_a - 15)) (R7, R8),
+ *     p = max xhat - 10 (R6), xtilde = max(0, xhat - p), t_i = 1 << xtilde.
+ *   `e32` receives the pre-rounding values when non-NULL. */
+int orc_loss_t_case(int s_a) { return s_a <= -7 ? 1 : 2; }
+
+static int64_t loss_xhat(int64_t a, int s_a)
+{
+    int64_t prod = 47274 * a;
+    int sh = 15 - s_a;
+    if (sh >= 0)
+        return prod >= 0 ? (prod >> sh) : -((-prod + ((int64_t)1 << sh) - 1) >> sh);
+    /* left shift: s_a > 15.  Any shift of at least 1 already separates
+     * distinct logits by more than 10, so the shift is capped there (exact
+     * for the t_i that result). */
+    return prod * 2;
+}
+
+void orc_int_ce_loss_grad(const int8_t *logits, int s_a, const int32_t *labels,
+                          int64_t B, int64_t N, int mode, int8_t *err,
+                          int64_t *e32, orc_stats *st)
+{
+    int64_t *e = e32 ? e32 : (int64_t *)malloc((size_t)(B * N > 0 ? B * N : 1) * sizeof(int64_t));
+    int32_t flags = 0;
+    int64_t bi, i;
+    if (s_a <= -7 && s_a < -22) {
+        flags |= ORC_FLAG_LOSS_SA;
+        s_a = -22;
+    }
+    for (bi = 0; bi < B; bi++) {
+        const int8_t *a = logits + bi * N;
+        int64_t *ev = e + bi * N;
+        int64_t C = 0;
+        if (s_a <= -7) {
+            const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
+            for (i = 0; i < N; i++) {
+                const int64_t ai = a[i];
+                ev[i] = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
+            }
+        } else {
+            int64_t mx = 0, p;
+            for (i = 0; i < N; i++) {
+                const int64_t xh = loss_xhat(a[i], s_a);
+                if (i == 0 || xh > mx)
+                    mx = xh;
+            }
+            p = mx - 10;
+            for (i = 0; i < N; i++) {
+                int64_t xt = loss_xhat(a[i], s_a) - p;
+                if (xt < 0)
+                    xt = 0;
+                ev[i] = (int64_t)1 << xt;
+            }
+        }
+        for (i = 0; i < N; i++)
+            C += ev[i];
+        ev[labels[bi]] -= C;
+    }
+    orc_shift_round_i64(e, B * N, 7, mode, err, st);
+    if (st)
+        st->flags |= flags;
+    if (!e32)
+        free(e);
+}
+
+/* ------------------------------------------------------------------ */
+/* Layer glue the networks of the experiments need (not contractions).  */
+
+/* Backward ReLU (reading R5): zero the int8 error where the stored int8
+ * activation is not positive. */
+void orc_relu_mask(int8_t *e, const int8_t *a, int64_t n)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        if (a[i] <= 0)
+            e[i] = 0;
+}
+
+/* 2x2 stride-2 max pooling, NCHW, H and W even.  idx receives the position
+ * (0..3, row-major in the window) of the first maximum. */
+void orc_maxpool2_fwd(const int8_t *x, int64_t n, int64_t c, int64_t h, int64_t w,
+                      int8_t *y, uint8_t *idx)
+{
+    const int64_t H2 = h / 2, W2 = w / 2;
+    int64_t nc, i, j;
+    for (nc = 0; nc < n * c; nc++)
+        for (i = 0; i < H2; i++)
+            for (j = 0; j < W2; j++) {
+                const int8_t *base = x + (nc * h + 2 * i) * w + 2 * j;
+                int8_t v[4];
+                int best = 0, t;
+                v[0] = base[0];
+                v[1] = base[1];
+                v[2] = base[w];
+                v[3] = base[w + 1];
+                for (t = 1; t < 4; t++)
+                    if (v[t] > v[best])
+                        best = t;
+                y[(nc * H2 + i) * W2 + j] = v[best];
+                if (idx)
+                    idx[(nc * H2 + i) * W2 + j] = (uint8_t)best;
+            }
+}
+
+/* Backward of the pooling: each pooled error goes to the first maximum of
+ * its window, the other three positions get zero. */
+void orc_maxpool2_bwd(const int8_t *dy, const uint8_t *idx, int64_t n, int64_t c,
+                      int64_t h, int64_t w, int8_t *dx)
+{
+    const int64_t H2 = h / 2, W2 = w / 2;
+    int64_t nc, i, j;
+    memset(dx, 0, (size_t)(n * c * h * w));
+    for (nc = 0; nc < n * c; nc++)
+        for (i = 0; i < H2; i++)
+            for (j = 0; j < W2; j++) {
+                const int64_t o = (nc * H2 + i) * W2 + j;
+                const int t = idx[o];
+                dx[(nc * h + 2 * i + t / 2) * w + 2 * j + t % 2] = dy[o];
+            }
+}
+
+/* Section 3: the one quantisation step, applied to the input images:
+ * an 8-bit pixel p in [0, 255] becomes p >> 1 in [0, 127] with s = -7. */
+void orc_quantize_u8(const uint8_t *px, int64_t n, int8_t *q)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        q[i] = (int8_t)(px[i] >> 1);
+}
