@@ -1,0 +1,221 @@
+/*
+ * niti.h -- C ABI of the MI355X (gfx950) NITI hot-path library, libniti.so.
+ *
+ * NITI ("Training Integer Neural Networks Using Integer-only Arithmetic",
+ * arXiv 2009.13108) trains with int8 tensors that each carry one shared
+ * int8 exponent (a block exponent, Section 3.1).  Every layer multiplies
+ * int8 operands into int32 accumulators (Section 3.2), finds the effective
+ * bitwidth of the largest accumulator over the whole tensor, and shifts the
+ * tensor back to int8 with pseudo stochastic rounding (Algorithms 1-3).
+ * Weight gradients are shifted to m_u bits and subtracted from the int8
+ * weights (Section 3.3).  The loss gradient is formed in integers
+ * (Section 3.5).
+ *
+ * Conventions shared by every entry point
+ *   Memory      Every tensor pointer is a DEVICE pointer owned by the caller.
+ *               The library never allocates or frees device memory.  Calls
+ *               that need temporary device memory take a caller-provided
+ *               workspace (ws, ws_bytes); niti_workspace_bytes() sizes it.
+ *   Layout      Activations and errors are NHWC int8 (channels fastest),
+ *               convolution weights are KRSC int8 (output channel, filter
+ *               row, filter column, input channel), matrices are row-major.
+ *               Exponents are int8 scalars in device memory, so a training
+ *               step never waits on the host.
+ *   Streams     Every call only enqueues work on `stream` (a hipStream_t,
+ *               passed as void*; NULL is the default stream) and returns.
+ *   Errors      Arguments are checked on the host before anything is
+ *               enqueued; on error a negative niti_status is returned and
+ *               no work is launched.  A failed launch returns NITI_ERR_HIP.
+ *               Data-dependent conditions never fail a call: they set bits
+ *               in niti_stats.flags.
+ *   Stats       Calls that form a block exponent need a niti_stats block in
+ *               device memory, zero-filled by the caller before its first
+ *               use and kept per tensor (per layer and pass) afterwards.  It
+ *               holds the result of the call and the library's working
+ *               state; two calls in flight at once must not share one.
+ *   Rounding    mode NITI_ROUND_PSR is Algorithm 3; NITI_ROUND_RTN rounds
+ *               to nearest with ties away from zero (Section 4.3 uses it for
+ *               activations and errors).  A rounded magnitude that would
+ *               reach 128 is held at 127, so outputs lie in [-127, 127].
+ *   Speculation The library first rounds with the binary point that the
+ *               same stats block reported last time (bp_hint), checks it
+ *               against the true block maximum, and recomputes the output
+ *               when they differ.  Results are identical either way; a
+ *               miss only costs time and sets NITI_FLAG_HINT_MISS.
+ */
+#ifndef NITI_H
+#define NITI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum niti_status {
+    NITI_OK = 0,
+    NITI_ERR_NULL = -1,        /* a required pointer is NULL               */
+    NITI_ERR_SHAPE = -2,       /* a size is negative, zero where it must not be, or inconsistent */
+    NITI_ERR_UNSUPPORTED = -3, /* valid but outside what the kernels cover */
+    NITI_ERR_WORKSPACE = -4,   /* workspace missing or smaller than needed */
+    NITI_ERR_HIP = -5,         /* the HIP runtime reported an error        */
+    NITI_ERR_ARG = -6          /* an enum or scalar argument is out of range */
+} niti_status;
+
+typedef enum niti_round_mode {
+    NITI_ROUND_PSR = 0, /* pseudo stochastic rounding, Algorithm 3 */
+    NITI_ROUND_RTN = 1  /* round to nearest, ties away from zero   */
+} niti_round_mode;
+
+/* niti_stats.flags bits */
+#define NITI_FLAG_ACC_BOUND 1u  /* reduction long enough that int32 sums may wrap (K*127*127 >= 2^31); sums are kept mod 2^32 */
+#define NITI_FLAG_EXP_RANGE 2u  /* an output exponent left [-128, 127] and was held at the end */
+#define NITI_FLAG_LOSS_SA   4u  /* loss exponent below -22: the Taylor branch used s_a = -22 */
+#define NITI_FLAG_HINT_MISS 8u  /* the speculated binary point was wrong; the output was recomputed */
+
+/* Per-tensor statistics and working state, 64 bytes of device memory. */
+typedef struct niti_stats {
+    uint64_t acc_max;  /* working: running block maximum (zero between calls) */
+    uint32_t ticket;   /* working: completion counter (zero between calls)    */
+    uint32_t wflags;   /* working: flags raised by kernels (zero between calls) */
+    uint64_t max_abs;  /* out: largest magnitude over the whole result         */
+    int32_t b;         /* out: effective bitwidth of max_abs (Section 3.2)     */
+    int32_t bp;        /* out: binary point used, max(0, b - target)           */
+    int32_t flags;     /* out: NITI_FLAG_* of this call                        */
+    int32_t s_out;     /* out: output exponent formed by this call, if any     */
+    int32_t bp_hint;   /* in/out: binary point tried first by the next call    */
+    uint32_t calls;    /* out: calls made with this block                      */
+    uint32_t misses;   /* out: calls whose first try was wrong                 */
+    uint32_t reserved[3];
+} niti_stats;
+
+/* Convolution geometry.  Input x is NHWC [n][h][w][c]; filter is KRSC
+ * [k][r][s][c]; output is NHWC [n][p][q][k] with
+ * p = (h + 2 pad_h - r) / stride_h + 1 and q = (w + 2 pad_w - s) / stride_w + 1. */
+typedef struct niti_conv_desc {
+    int64_t n, h, w, c;
+    int64_t k, r, s;
+    int32_t stride_h, stride_w;
+    int32_t pad_h, pad_w;
+} niti_conv_desc;
+
+/* Operation ids for niti_workspace_bytes. */
+#define NITI_OP_GEMM_FWD        0
+#define NITI_OP_CONV_FWD        1
+#define NITI_OP_CONV_BWD_DATA   2
+#define NITI_OP_CONV_BWD_WEIGHT 3
+#define NITI_OP_INT_CE_LOSS     4
+
+/* Fully-connected / plain forward layer (Algorithm 1, forward loop;
+ * Section 3.2).  C = round(A B^T) with A [M][K], B [N][K] and C [M][N],
+ * all int8 row-major; the int32 products are optionally passed through ReLU,
+ * then the block exponent is found over all of C and the tensor is shifted
+ * by max(0, b - target_bits) and rounded.  *s_c = *s_a + *s_b + bp when all
+ * three exponent pointers are given (all NULL otherwise).  M, N >= 1,
+ * K >= 0 (A and B may be NULL when K == 0: C is then all zero),
+ * target_bits in 1..31.  No workspace. */
+niti_status niti_gemm_fwd(const int8_t *A, const int8_t *B, int8_t *C,
+                          int64_t M, int64_t N, int64_t K,
+                          const int8_t *s_a, const int8_t *s_b, int8_t *s_c,
+                          int target_bits, int relu, niti_round_mode mode,
+                          niti_stats *stats, void *stream);
+
+/* Convolution forward (Algorithm 1, forward loop; Section 3.2 reduces it to
+ * an implicit GEMM).  y = round(conv(x, w)), exponents as niti_gemm_fwd
+ * with target 7.  Needs c % 4 == 0 (pad image channels with zeros).  No
+ * workspace. */
+niti_status niti_conv_fwd(const niti_conv_desc *d, const int8_t *x, const int8_t *w,
+                          int8_t *y, const int8_t *s_x, const int8_t *s_w, int8_t *s_y,
+                          int relu, niti_round_mode mode, niti_stats *stats,
+                          void *stream);
+
+/* Error back-propagation through a convolution (Algorithm 1,
+ * e(l-1) = w(l) (x) e(l); Section 3.2): dx = round(adjoint of conv in x,
+ * applied to dy) with target 7.  dy is NHWC [n][p][q][k], dx NHWC
+ * [n][h][w][c].  The error exponent is not formed (Section 3.1: it cancels
+ * out of the learning rule).  If relu_src (NHWC like dx, the int8 forward
+ * activation of that layer) is given, dx is zeroed where relu_src <= 0
+ * after rounding; the block exponent is taken before that mask.  Workspace:
+ * niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, ...). */
+niti_status niti_conv_bwd_data(const niti_conv_desc *d, const int8_t *dy, const int8_t *w,
+                               int8_t *dx, const int8_t *relu_src, niti_round_mode mode,
+                               niti_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
+/* Weight gradient and discrete update (Algorithm 1, g(l) = a(l-1) (x) e(l)
+ * then w <- w - g; Section 3.3).  g32 = sum over n, p, q of dy x x, exact
+ * mod 2^32; b = B(g32); g = round(g32, max(0, b - mu)); w <- w - g held to
+ * [-127, 127], in place.  mu in 1..8.  If g32_out is given it receives the
+ * int32 gradient (KRSC).  Workspace:
+ * niti_workspace_bytes(NITI_OP_CONV_BWD_WEIGHT, d, ...).  A fully-connected
+ * layer is the case h = w = r = s = 1. */
+niti_status niti_conv_bwd_weight(const niti_conv_desc *d, const int8_t *x, const int8_t *dy,
+                                 int8_t *w, int32_t *g32_out, int mu, niti_round_mode mode,
+                                 niti_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
+/* Shift and round an int32 tensor (Algorithm 2 with Algorithm 3).  bp >= 0
+ * rounds with that binary point (stats may be NULL; magnitudes are held at
+ * 127); bp < 0 finds the block exponent first, bp = max(0, B(x) -
+ * target_bits), which needs stats.  *s_out = *s_in + bp when both are
+ * given.  n >= 0. */
+niti_status niti_round_psr(const int32_t *x, int8_t *y, int64_t n, int bp, int target_bits,
+                           niti_round_mode mode, const int8_t *s_in, int8_t *s_out,
+                           niti_stats *stats, void *stream);
+
+/* Integer cross-entropy gradient (Section 3.5).  logits [batch][classes]
+ * int8 with exponent *s_logits; labels int32 in [0, classes).  Per sample:
+ * s_a <= -7 uses t_i = 2^(1-2 s_a) + a_i 2^(1-s_a) + a_i^2 (second-order
+ * Taylor series, scaled to integers; s_a below -22 is taken as -22 and
+ * flagged); s_a > -7 uses t_i = 1 << max(0, xhat_i - p) with
+ * xhat_i = floor(47274 a_i 2^(s_a-15)) and p = max(xhat) - 10.  Then
+ * e32_i = t_i - [i == label] sum(t), and err = round(e32) with target 7 over
+ * the whole batch.  classes in 1..65536.  Workspace:
+ * niti_workspace_bytes(NITI_OP_INT_CE_LOSS, NULL, batch, classes, 0). */
+niti_status niti_int_ce_loss_grad(const int8_t *logits, const int8_t *s_logits,
+                                  const int32_t *labels, int8_t *err, int64_t batch,
+                                  int64_t classes, niti_round_mode mode, niti_stats *stats,
+                                  void *ws, size_t ws_bytes, void *stream);
+
+/* Discrete weight update from an int32 gradient (Section 3.3): b = B(g32),
+ * g = round(g32, max(0, b - mu)), w <- w - g held to [-127, 127], in place.
+ * mu in 1..8, n >= 0. */
+niti_status niti_sgd_update(int8_t *w, const int32_t *g32, int64_t n, int mu,
+                            niti_round_mode mode, niti_stats *stats, void *stream);
+
+/* Bytes of workspace an operation needs (0 when none).  d is used by the
+ * convolution ops, (M, N) = (batch, classes) by the loss. */
+size_t niti_workspace_bytes(int op, const niti_conv_desc *d, int64_t M, int64_t N, int64_t K);
+
+/* Human-readable name of a status code (static storage). */
+const char *niti_status_str(niti_status s);
+
+/* ---- Layer glue used by the experiments' networks (not contractions) ---- */
+
+/* Input quantisation (Section 3): 8-bit pixels px, NCHW [n][c][h][w], become
+ * int8 p >> 1 (exponent -7 for the caller to attach) in NHWC
+ * [n][h][w][c_pad]; channels c..c_pad-1 are zero.  c_pad >= c. */
+niti_status niti_quantize_u8(const uint8_t *px, int8_t *x, int64_t n, int64_t c, int64_t h,
+                             int64_t w, int64_t c_pad, void *stream);
+
+/* 2x2 stride-2 max pooling, NHWC, h and w even.  idx (one byte per output)
+ * records the window position (0..3, row-major) of the first maximum.  The
+ * exponent is unchanged. */
+niti_status niti_maxpool2_fwd(const int8_t *x, int8_t *y, uint8_t *idx, int64_t n, int64_t h,
+                              int64_t w, int64_t c, void *stream);
+
+/* Backward of niti_maxpool2_fwd: dx (NHWC [n][h][w][c]) receives each dy at
+ * its window's recorded position and zero elsewhere. */
+niti_status niti_maxpool2_bwd(const int8_t *dy, const uint8_t *idx, int8_t *dx, int64_t n,
+                              int64_t h, int64_t w, int64_t c, void *stream);
+
+/* Backward ReLU on an int8 error: e[i] = 0 where a[i] <= 0, in place. */
+niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
+
+/* Size of niti_stats, for bindings. */
+size_t niti_stats_bytes(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NITI_H */

@@ -1,0 +1,347 @@
+// Bandwidth-bound passes of the NITI step: the tensor-wide maximum, the
+// shift-and-round of an int32 tensor (Algorithms 2 and 3), the discrete
+// weight update (Section 3.3), the integer cross-entropy gradient (Section
+// 3.5), the back-propagation filter repack and the layer glue (input
+// quantisation, 2x2 max pooling, backward ReLU).
+#include "niti_internal.h"
+
+namespace niti {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+inline int grid_for(int64_t n, int per_thread = 4, int cap = 2048) {
+    int64_t g = (n + (int64_t)kThreads * per_thread - 1) / ((int64_t)kThreads * per_thread);
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (int)g;
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * 4;
+    for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n; i += stride) {
+        if (i + 4 <= n && (((uintptr_t)(p + i)) & 15) == 0) {
+            *(int4*)(p + i) = make_int4(v, v, v, v);
+        } else {
+            for (int64_t j = i; j < i + 4 && j < n; j++) p[j] = v;
+        }
+    }
+}
+
+__global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) {
+    uint64_t m = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const uint64_t a = mag32(x[i]);
+        m = a > m ? a : m;
+    }
+    block_publish_max(st, m);
+}
+
+// bp_fixed >= 0: that binary point.  bp_fixed < 0: the block binary point
+// from st->acc_max, then the statistics are finalized by the last group.
+__global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_fixed, int target,
+                                 int mode, niti_stats* st, ExpArgs ex) {
+    const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(load_acc_max(st), target);
+    const RoundK rk = make_round(bp, mode);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        y[i] = round_i32(x[i], rk);
+    if (bp_fixed >= 0) {
+        // Algorithm 2: s_q = s_q32 + bp, held to the int8 range.
+        if (ex.s_out && blockIdx.x == 0 && threadIdx.x == 0) {
+            int s = (int)*ex.s_a + bp;
+            *ex.s_out = (int8_t)(s > 127 ? 127 : (s < -128 ? -128 : s));
+        }
+        return;
+    }
+    if (!st) return;
+    __syncthreads();
+    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
+        finalize_stats(st, target, ex, 0u, 0, 0);
+}
+
+// Discrete update: g = round(g32, max(0, B(g32) - mu)); w <- clamp(w - g).
+__global__ void update_kernel(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu,
+                              int mode, niti_stats* st, uint32_t static_flags) {
+    const int bp = block_bp(load_acc_max(st), mu);
+    const RoundK rk = make_round(bp, mode);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const int32_t g = g32[i];
+        if (g32_copy) g32_copy[i] = g;
+        int v = (int)w[i] - (int)round_i32(g, rk);
+        v = v > 127 ? 127 : (v < -127 ? -127 : v);
+        w[i] = (int8_t)v;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
+        finalize_stats(st, mu, ExpArgs{nullptr, nullptr, nullptr}, static_flags, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// Integer cross-entropy gradient, one wave per sample (Section 3.5).
+constexpr int kLossMinSa = -22;
+
+__device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
+    const int64_t prod = 47274 * a;
+    const int sh = 15 - s_a;
+    if (sh >= 0) return prod >> sh;  // arithmetic shift: floor
+    // s_a > 15: any left shift already separates distinct logits by more
+    // than the 10-bit window, so one doubling gives the same t values.
+    return prod * 2;
+}
+
+__global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
+                            int64_t* e64, int64_t batch, int64_t classes, niti_stats* st) {
+    const int lane = threadIdx.x & 63;
+    const int64_t sample = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
+    int s_a = (int)*s_logits;
+    bool flag_sa = false;
+    if (s_a < kLossMinSa) {
+        flag_sa = true;
+        s_a = kLossMinSa;
+    }
+    uint64_t m = 0;
+    if (sample < batch) {
+        const int8_t* a = logits + sample * classes;
+        int64_t* e = e64 + sample * classes;
+        int64_t C = 0;
+        if (s_a <= -7) {
+            const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
+            for (int64_t i = lane; i < classes; i += 64) {
+                const int64_t ai = a[i];
+                const int64_t t = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
+                e[i] = t;
+                C += t;
+            }
+        } else {
+            int64_t mx = INT64_MIN;
+            for (int64_t i = lane; i < classes; i += 64) {
+                const int64_t xh = loss_xhat(a[i], s_a);
+                mx = xh > mx ? xh : mx;
+            }
+            mx = wave_max_i64(mx);
+            const int64_t p = mx - 10;
+            for (int64_t i = lane; i < classes; i += 64) {
+                int64_t xt = loss_xhat(a[i], s_a) - p;
+                xt = xt < 0 ? 0 : xt;
+                const int64_t t = (int64_t)1 << xt;
+                e[i] = t;
+                C += t;
+            }
+        }
+        C = wave_sum_i64(C);
+        const int32_t y = labels[sample];
+        // Lane i owns entries i, i+64, ...; the owner of the label's entry
+        // subtracts C (a label outside [0, classes) contributes no term).
+        if (y >= 0 && y < classes && (y & 63) == lane) e[y] -= C;
+        for (int64_t i = lane; i < classes; i += 64) {
+            const int64_t v = e[i];
+            const uint64_t mg = v < 0 ? 0ull - (uint64_t)v : (uint64_t)v;
+            m = mg > m ? mg : m;
+        }
+    }
+    if (flag_sa && threadIdx.x == 0 && blockIdx.x == 0)
+        atomicOr(&st->wflags, NITI_FLAG_LOSS_SA);
+    block_publish_max(st, m);
+}
+
+__global__ void loss_round_kernel(const int64_t* e64, int8_t* err, int64_t n, int mode, niti_stats* st) {
+    const int bp = block_bp(load_acc_max(st), 7);
+    const RoundK rk = make_round(bp, mode);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        err[i] = round_i64(e64[i], rk);
+    __syncthreads();
+    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
+        finalize_stats(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// Back-propagation filters.  Class (a, b) of a stride (sh, sw) layer uses
+// filter rows r = r0 + sh*(T-1-t) and columns s = s0 + sw*(U-1-u), so that
+// the class is a stride-1 correlation over dy:
+//   wc[c][t][u][k] = w[k][r0 + sh (T-1-t)][s0 + sw (U-1-u)][c].
+struct DgradClasses {
+    DgradClass c[kMaxProblems];
+    int n;
+};
+
+__global__ void repack_dgrad_kernel(const int8_t* w, int8_t* out, DgradClasses cl, int K, int R, int S,
+                                    int C, int sh, int sw, int64_t total) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += stride) {
+        int ci = 0;
+        for (int i = 1; i < cl.n; i++)
+            if (idx >= cl.c[i].offset) ci = i;
+        const DgradClass& d = cl.c[ci];
+        int64_t o = idx - d.offset;  // within class: [c][t][u][k]
+        const int k = (int)(o % K);
+        o /= K;
+        const int u = (int)(o % d.U);
+        o /= d.U;
+        const int t = (int)(o % d.T);
+        const int c = (int)(o / d.T);
+        const int r = d.r0 + sh * (d.T - 1 - t);
+        const int s = d.s0 + sw * (d.U - 1 - u);
+        out[idx] = w[(((int64_t)k * R + r) * S + s) * C + c];
+    }
+}
+
+// ---------------------------------------------------------------------------
+__global__ void quantize_kernel(const uint8_t* px, int8_t* x, int64_t n, int64_t c, int64_t h,
+                                int64_t w, int64_t cp) {
+    const int64_t total = n * h * w * cp;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t ch = i % cp;
+        int64_t pix = i / cp;
+        const int64_t col = pix % w;
+        pix /= w;
+        const int64_t row = pix % h;
+        const int64_t img = pix / h;
+        int8_t v = 0;
+        if (ch < c) v = (int8_t)(px[((img * c + ch) * h + row) * w + col] >> 1);
+        x[i] = v;
+    }
+}
+
+__global__ void maxpool_fwd_kernel(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, int64_t h,
+                                   int64_t w, int64_t c) {
+    const int64_t H2 = h / 2, W2 = w / 2, total = n * H2 * W2 * c;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t ch = i % c;
+        int64_t t = i / c;
+        const int64_t j = t % W2;
+        t /= W2;
+        const int64_t r = t % H2;
+        const int64_t img = t / H2;
+        const int8_t* b = x + ((img * h + 2 * r) * w + 2 * j) * c + ch;
+        int8_t v[4] = {b[0], b[c], b[w * c], b[w * c + c]};
+        int best = 0;
+        for (int q = 1; q < 4; q++)
+            if (v[q] > v[best]) best = q;
+        y[i] = v[best];
+        idx[i] = (uint8_t)best;
+    }
+}
+
+__global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n,
+                                   int64_t h, int64_t w, int64_t c) {
+    // One thread per input element: it takes dy where its window picked it.
+    const int64_t total = n * h * w * c;
+    const int64_t W2 = w / 2, H2 = h / 2;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t ch = i % c;
+        int64_t t = i / c;
+        const int64_t col = t % w;
+        t /= w;
+        const int64_t row = t % h;
+        const int64_t img = t / h;
+        const int64_t o = ((img * H2 + row / 2) * W2 + col / 2) * c + ch;
+        const int pos = (int)((row & 1) * 2 + (col & 1));
+        dx[i] = idx[o] == pos ? dy[o] : (int8_t)0;
+    }
+}
+
+__global__ void relu_mask_kernel(int8_t* e, const int8_t* a, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        if (a[i] <= 0) e[i] = 0;
+}
+
+}  // namespace
+
+hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(n, 16)), dim3(kThreads), 0, s, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t max_abs_i32(const int32_t* x, int64_t n, niti_stats* st, hipStream_t s) {
+    hipLaunchKernelGGL(max_abs_i32_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, x, n, st);
+    return hipGetLastError();
+}
+
+hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int target, int mode,
+                         niti_stats* st, ExpArgs ex, hipStream_t s) {
+    hipLaunchKernelGGL(round_i32_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, x, y, n, bp,
+                       target, mode, st, ex);
+    return hipGetLastError();
+}
+
+hipError_t update_run(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu, int mode,
+                      niti_stats* st, uint32_t static_flags, hipStream_t s) {
+    hipLaunchKernelGGL(update_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, w, g32, g32_copy, n,
+                       mu, mode, st, static_flags);
+    return hipGetLastError();
+}
+
+hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t* labels, int8_t* err,
+                    int64_t* e64, int64_t batch, int64_t classes, int mode, niti_stats* st,
+                    hipStream_t s) {
+    const int per_block = kThreads / 64;
+    const int64_t blocks = (batch + per_block - 1) / per_block;
+    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(kThreads), 0, s,
+                       logits, s_logits, labels, e64, batch, classes, st);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = batch * classes;
+    hipLaunchKernelGGL(loss_round_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, e64, err, n, mode,
+                       st);
+    return hipGetLastError();
+}
+
+hipError_t repack_dgrad_run(const int8_t* w, int8_t* out, const DgradClass* cls, int ncls, int K, int R,
+                            int S, int C, int sh, int sw, hipStream_t s) {
+    DgradClasses cl;
+    cl.n = ncls;
+    int64_t total = 0;
+    for (int i = 0; i < ncls; i++) {
+        cl.c[i] = cls[i];
+        total = cls[i].offset + (int64_t)C * cls[i].T * cls[i].U * K;
+    }
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(repack_dgrad_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, w, out, cl, K,
+                       R, S, C, sh, sw, total);
+    return hipGetLastError();
+}
+
+hipError_t quantize_run(const uint8_t* px, int8_t* x, int64_t n, int64_t c, int64_t h, int64_t w,
+                        int64_t cp, hipStream_t s) {
+    const int64_t total = n * h * w * cp;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, px, x, n, c, h, w,
+                       cp);
+    return hipGetLastError();
+}
+
+hipError_t maxpool_fwd_run(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, int64_t h, int64_t w,
+                           int64_t c, hipStream_t s) {
+    const int64_t total = n * (h / 2) * (w / 2) * c;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, x, y, idx, n, h,
+                       w, c);
+    return hipGetLastError();
+}
+
+hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
+                           int64_t w, int64_t c, hipStream_t s) {
+    const int64_t total = n * h * w * c;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, dy, idx, dx, n,
+                       h, w, c);
+    return hipGetLastError();
+}
+
+hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(relu_mask_kernel, dim3(grid_for(n, 4)), dim3(kThreads), 0, s, e, a, n);
+    return hipGetLastError();
+}
+
+}  // namespace niti

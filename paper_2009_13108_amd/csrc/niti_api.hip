@@ -1,0 +1,376 @@
+// C ABI of libniti.so (declared in include/niti.h): argument checks on the
+// host, problem set-up, and kernel launches.  Nothing here allocates device
+// memory or waits on the device.
+#include <limits.h>
+
+#include "niti_internal.h"
+
+using namespace niti;
+
+namespace {
+
+constexpr int64_t kMaxBytes = (int64_t)1 << 31;  // 32-bit offsets inside kernels
+constexpr int64_t kAccLimit = (int64_t)1 << 31;
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+inline bool too_big(int64_t a) { return a < 0 || a >= kMaxBytes; }
+
+inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
+
+inline niti_status hip_status(hipError_t e) { return e == hipSuccess ? NITI_OK : NITI_ERR_HIP; }
+
+inline uint32_t acc_flags(int64_t red_len) {
+    return (red_len * 127 * 127 >= kAccLimit) ? NITI_FLAG_ACC_BOUND : 0u;
+}
+
+bool valid_mode(niti_round_mode m) { return m == NITI_ROUND_PSR || m == NITI_ROUND_RTN; }
+
+// Geometry checks shared by the three convolution passes.
+niti_status check_conv(const niti_conv_desc* d, int64_t* P, int64_t* Q) {
+    if (!d) return NITI_ERR_NULL;
+    if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1)
+        return NITI_ERR_SHAPE;
+    if (d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0) return NITI_ERR_SHAPE;
+    const int64_t p = (d->h + 2 * (int64_t)d->pad_h - d->r);
+    const int64_t q = (d->w + 2 * (int64_t)d->pad_w - d->s);
+    if (p < 0 || q < 0) return NITI_ERR_SHAPE;
+    *P = p / d->stride_h + 1;
+    *Q = q / d->stride_w + 1;
+    if (d->c % 4 != 0) return NITI_ERR_UNSUPPORTED;
+    if (d->stride_h != d->stride_w || d->stride_h > 2) return NITI_ERR_UNSUPPORTED;
+    if (too_big(d->n * d->h * d->w * d->c) || too_big(d->n * *P * *Q * d->k) ||
+        too_big(d->k * d->r * d->s * d->c) || too_big(d->k * d->r * d->s * d->c * 4))
+        return NITI_ERR_UNSUPPORTED;
+    return NITI_OK;
+}
+
+void set_out_grid(IgemmProblem& p, int64_t n, int64_t ohc, int64_t owc) {
+    p.OHc = (int32_t)ohc;
+    p.OWc = (int32_t)owc;
+    p.M = (int32_t)(n * ohc * owc);
+    p.div_ohw = make_fastdiv((uint32_t)(ohc * owc));
+    p.div_ow = make_fastdiv((uint32_t)owc);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t niti_stats_bytes(void) { return sizeof(niti_stats); }
+
+const char* niti_status_str(niti_status s) {
+    switch (s) {
+        case NITI_OK: return "ok";
+        case NITI_ERR_NULL: return "required pointer is NULL";
+        case NITI_ERR_SHAPE: return "invalid or inconsistent sizes";
+        case NITI_ERR_UNSUPPORTED: return "shape or layout not supported by the kernels";
+        case NITI_ERR_WORKSPACE: return "workspace missing or too small";
+        case NITI_ERR_HIP: return "HIP runtime error";
+        case NITI_ERR_ARG: return "argument out of range";
+    }
+    return "unknown status";
+}
+
+size_t niti_workspace_bytes(int op, const niti_conv_desc* d, int64_t M, int64_t N, int64_t K) {
+    (void)K;
+    switch (op) {
+        case NITI_OP_CONV_BWD_DATA:
+            return d ? (size_t)round_up(d->k * d->r * d->s * d->c, 256) : 0;
+        case NITI_OP_CONV_BWD_WEIGHT:
+            return d ? (size_t)round_up(d->k * d->r * d->s * d->c * 4, 256) : 0;
+        case NITI_OP_INT_CE_LOSS:
+            return (M > 0 && N > 0) ? (size_t)round_up(M * N * 8, 256) : 0;
+        default:
+            return 0;
+    }
+}
+
+niti_status niti_gemm_fwd(const int8_t* A, const int8_t* B, int8_t* C, int64_t M, int64_t N, int64_t K,
+                          const int8_t* s_a, const int8_t* s_b, int8_t* s_c, int target_bits, int relu,
+                          niti_round_mode mode, niti_stats* stats, void* stream) {
+    if (!C || !stats) return NITI_ERR_NULL;
+    if (M < 1 || N < 1 || K < 0) return NITI_ERR_SHAPE;
+    if ((!A || !B) && K > 0) return NITI_ERR_NULL;
+    if (target_bits < 1 || target_bits > 31 || !valid_mode(mode)) return NITI_ERR_ARG;
+    const int nexp = (s_a != nullptr) + (s_b != nullptr) + (s_c != nullptr);
+    if (nexp != 0 && nexp != 3) return NITI_ERR_NULL;
+    if (too_big(M * K) || too_big(N * K) || too_big(M * N) || too_big(round_up(K, 16)))
+        return NITI_ERR_UNSUPPORTED;
+    IgemmBatch b{};
+    b.nprob = 1;
+    IgemmProblem& p = b.p[0];
+    p.act = A;
+    p.wgt = B;
+    p.out = C;
+    p.mask = nullptr;
+    p.Nout = (int32_t)N;
+    p.R = 1;
+    p.L = (int32_t)K;
+    p.Lpad = (int32_t)round_up(K, 16);
+    p.Ktot = p.Lpad;
+    p.H = 1;
+    p.W = 1;
+    p.C = (int32_t)K;
+    p.st = 1;
+    p.off_h = 0;
+    p.off_w = 0;
+    set_out_grid(p, M, 1, 1);
+    p.OH = 1;
+    p.OW = 1;
+    p.ldo = (int32_t)N;
+    p.os = 1;
+    p.oa = 0;
+    p.ob = 0;
+    IgemmCtl ctl{};
+    ctl.stats = stats;
+    ctl.ex = ExpArgs{s_a, s_b, s_c};
+    ctl.target = target_bits;
+    ctl.relu = relu ? 1 : 0;
+    ctl.mode = mode;
+    ctl.static_flags = acc_flags(K);
+    return hip_status(igemm_run(b, ctl, as_stream(stream)));
+}
+
+niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t* w, int8_t* y,
+                          const int8_t* s_x, const int8_t* s_w, int8_t* s_y, int relu, niti_round_mode mode,
+                          niti_stats* stats, void* stream) {
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!x || !w || !y || !stats) return NITI_ERR_NULL;
+    const int nexp = (s_x != nullptr) + (s_w != nullptr) + (s_y != nullptr);
+    if (nexp != 0 && nexp != 3) return NITI_ERR_NULL;
+    if (!valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    IgemmBatch b{};
+    b.nprob = 1;
+    IgemmProblem& p = b.p[0];
+    p.act = x;
+    p.wgt = w;
+    p.out = y;
+    p.mask = nullptr;
+    p.Nout = (int32_t)d->k;
+    p.R = (int32_t)d->r;
+    p.L = (int32_t)(d->s * d->c);
+    p.Lpad = (int32_t)round_up(p.L, 16);
+    p.Ktot = p.R * p.Lpad;
+    p.H = (int32_t)d->h;
+    p.W = (int32_t)d->w;
+    p.C = (int32_t)d->c;
+    p.st = d->stride_h;
+    p.off_h = -d->pad_h;
+    p.off_w = -d->pad_w;
+    set_out_grid(p, d->n, P, Q);
+    p.OH = (int32_t)P;
+    p.OW = (int32_t)Q;
+    p.ldo = (int32_t)d->k;
+    p.os = 1;
+    p.oa = 0;
+    p.ob = 0;
+    IgemmCtl ctl{};
+    ctl.stats = stats;
+    ctl.ex = ExpArgs{s_x, s_w, s_y};
+    ctl.target = 7;
+    ctl.relu = relu ? 1 : 0;
+    ctl.mode = mode;
+    ctl.static_flags = acc_flags(d->r * d->s * d->c);
+    return hip_status(igemm_run(b, ctl, as_stream(stream)));
+}
+
+niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const int8_t* w, int8_t* dx,
+                               const int8_t* relu_src, niti_round_mode mode, niti_stats* stats, void* ws,
+                               size_t ws_bytes, void* stream) {
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!dy || !w || !dx || !stats) return NITI_ERR_NULL;
+    if (!valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    const size_t need = niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0);
+    if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
+    const int st = d->stride_h;
+    const int K = (int)d->k, R = (int)d->r, S = (int)d->s, C = (int)d->c;
+    DgradClass cls[kMaxProblems];
+    IgemmBatch b{};
+    int ncls = 0;
+    int64_t off = 0;
+    for (int a = 0; a < st; a++) {
+        for (int bb = 0; bb < st; bb++) {
+            DgradClass& c = cls[ncls];
+            c.r0 = (a + d->pad_h) % st;
+            c.s0 = (bb + d->pad_w) % st;
+            c.T = c.r0 < R ? (R - c.r0 + st - 1) / st : 0;
+            c.U = c.s0 < S ? (S - c.s0 + st - 1) / st : 0;
+            c.offset = off;
+            off += (int64_t)C * c.T * c.U * K;
+            const int64_t hc = a < d->h ? (d->h - a + st - 1) / st : 0;
+            const int64_t wc = bb < d->w ? (d->w - bb + st - 1) / st : 0;
+            ncls++;
+            if (hc == 0 || wc == 0) continue;
+            IgemmProblem& p = b.p[b.nprob++];
+            const int da = (a + d->pad_h - c.r0) / st;
+            const int db = (bb + d->pad_w - c.s0) / st;
+            p.act = dy;
+            p.wgt = (const int8_t*)ws + c.offset;
+            p.out = dx;
+            p.mask = relu_src;
+            p.Nout = C;
+            p.R = c.T;
+            p.L = c.U * K;
+            p.Lpad = (int32_t)round_up(p.L, 16);
+            p.Ktot = p.R * p.Lpad;
+            p.H = (int32_t)P;
+            p.W = (int32_t)Q;
+            p.C = K;
+            p.st = 1;
+            p.off_h = da - c.T + 1;
+            p.off_w = db - c.U + 1;
+            set_out_grid(p, d->n, hc, wc);
+            p.OH = (int32_t)d->h;
+            p.OW = (int32_t)d->w;
+            p.ldo = C;
+            p.os = st;
+            p.oa = a;
+            p.ob = bb;
+        }
+    }
+    hipError_t e = repack_dgrad_run(w, (int8_t*)ws, cls, ncls, K, R, S, C, st, st, as_stream(stream));
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    IgemmCtl ctl{};
+    ctl.stats = stats;
+    ctl.ex = ExpArgs{nullptr, nullptr, nullptr};
+    ctl.target = 7;
+    ctl.relu = 0;
+    ctl.mode = mode;
+    ctl.static_flags = acc_flags((int64_t)K * R * S);
+    return hip_status(igemm_run(b, ctl, as_stream(stream)));
+}
+
+niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const int8_t* dy, int8_t* w,
+                                 int32_t* g32_out, int mu, niti_round_mode mode, niti_stats* stats, void* ws,
+                                 size_t ws_bytes, void* stream) {
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!x || !dy || !w || !stats) return NITI_ERR_NULL;
+    if (mu < 1 || mu > 8 || !valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    const int64_t nw = d->k * d->r * d->s * d->c;
+    int32_t* g32 = g32_out;
+    if (!g32) {
+        if (!ws || ws_bytes < (size_t)(nw * 4)) return NITI_ERR_WORKSPACE;
+        g32 = (int32_t*)ws;
+    }
+    const int64_t npix = d->n * P * Q;
+    if (too_big(npix)) return NITI_ERR_UNSUPPORTED;
+    hipStream_t strm = as_stream(stream);
+    hipError_t e = fill_i32(g32, nw, 0, strm);
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    WgradProblem p{};
+    p.x = x;
+    p.dy = dy;
+    p.g32 = g32;
+    p.H = (int32_t)d->h;
+    p.W = (int32_t)d->w;
+    p.C = (int32_t)d->c;
+    p.K = (int32_t)d->k;
+    p.R = (int32_t)d->r;
+    p.S = (int32_t)d->s;
+    p.P = (int32_t)P;
+    p.Q = (int32_t)Q;
+    p.sh = d->stride_h;
+    p.sw = d->stride_w;
+    p.ph = d->pad_h;
+    p.pw = d->pad_w;
+    p.L = p.S * p.C;
+    p.ncol = p.R * p.L;
+    p.npix = (int32_t)npix;
+    p.div_pq = make_fastdiv((uint32_t)(P * Q));
+    p.div_q = make_fastdiv((uint32_t)Q);
+    p.div_l = make_fastdiv((uint32_t)p.L);
+    p.div_c = make_fastdiv((uint32_t)p.C);
+    e = wgrad_run(p, strm);
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    e = max_abs_i32(g32, nw, stats, strm);
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    return hip_status(update_run(w, g32, nullptr, nw, mu, mode, stats, acc_flags(npix), strm));
+}
+
+niti_status niti_round_psr(const int32_t* x, int8_t* y, int64_t n, int bp, int target_bits,
+                           niti_round_mode mode, const int8_t* s_in, int8_t* s_out, niti_stats* stats,
+                           void* stream) {
+    if (n < 0) return NITI_ERR_SHAPE;
+    if ((!x || !y) && n > 0) return NITI_ERR_NULL;
+    if (!valid_mode(mode) || bp > 31) return NITI_ERR_ARG;
+    if ((s_in == nullptr) != (s_out == nullptr)) return NITI_ERR_NULL;
+    if (bp < 0) {
+        if (!stats) return NITI_ERR_NULL;
+        if (target_bits < 1 || target_bits > 31) return NITI_ERR_ARG;
+    }
+    hipStream_t strm = as_stream(stream);
+    if (bp < 0) {
+        hipError_t e = max_abs_i32(x, n, stats, strm);
+        if (e != hipSuccess) return NITI_ERR_HIP;
+    }
+    return hip_status(round_i32_run(x, y, n, bp, target_bits, mode, bp < 0 ? stats : nullptr,
+                                    ExpArgs{s_in, nullptr, s_out}, strm));
+}
+
+niti_status niti_int_ce_loss_grad(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
+                                  int8_t* err, int64_t batch, int64_t classes, niti_round_mode mode,
+                                  niti_stats* stats, void* ws, size_t ws_bytes, void* stream) {
+    if (!logits || !s_logits || !labels || !err || !stats) return NITI_ERR_NULL;
+    if (batch < 1 || classes < 1) return NITI_ERR_SHAPE;
+    if (classes > 65536 || !valid_mode(mode)) return NITI_ERR_ARG;
+    if (too_big(batch * classes * 8)) return NITI_ERR_UNSUPPORTED;
+    const size_t need = niti_workspace_bytes(NITI_OP_INT_CE_LOSS, nullptr, batch, classes, 0);
+    if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
+    return hip_status(loss_run(logits, s_logits, labels, err, (int64_t*)ws, batch, classes, mode, stats,
+                               as_stream(stream)));
+}
+
+niti_status niti_sgd_update(int8_t* w, const int32_t* g32, int64_t n, int mu, niti_round_mode mode,
+                            niti_stats* stats, void* stream) {
+    if (n < 0) return NITI_ERR_SHAPE;
+    if (((!w || !g32) && n > 0) || !stats) return NITI_ERR_NULL;
+    if (mu < 1 || mu > 8 || !valid_mode(mode)) return NITI_ERR_ARG;
+    if (too_big(n * 4)) return NITI_ERR_UNSUPPORTED;
+    hipStream_t strm = as_stream(stream);
+    hipError_t e = max_abs_i32(g32, n, stats, strm);
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    return hip_status(update_run(w, g32, nullptr, n, mu, mode, stats, 0u, strm));
+}
+
+niti_status niti_quantize_u8(const uint8_t* px, int8_t* x, int64_t n, int64_t c, int64_t h, int64_t w,
+                             int64_t c_pad, void* stream) {
+    if (!px || !x) return NITI_ERR_NULL;
+    if (n < 1 || c < 1 || h < 1 || w < 1 || c_pad < c) return NITI_ERR_SHAPE;
+    if (too_big(n * h * w * c_pad)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(quantize_run(px, x, n, c, h, w, c_pad, as_stream(stream)));
+}
+
+niti_status niti_maxpool2_fwd(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, int64_t h, int64_t w,
+                              int64_t c, void* stream) {
+    if (!x || !y || !idx) return NITI_ERR_NULL;
+    if (n < 1 || h < 2 || w < 2 || c < 1 || (h & 1) || (w & 1)) return NITI_ERR_SHAPE;
+    if (too_big(n * h * w * c)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(maxpool_fwd_run(x, y, idx, n, h, w, c, as_stream(stream)));
+}
+
+niti_status niti_maxpool2_bwd(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
+                              int64_t w, int64_t c, void* stream) {
+    if (!dy || !idx || !dx) return NITI_ERR_NULL;
+    if (n < 1 || h < 2 || w < 2 || c < 1 || (h & 1) || (w & 1)) return NITI_ERR_SHAPE;
+    if (too_big(n * h * w * c)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(maxpool_bwd_run(dy, idx, dx, n, h, w, c, as_stream(stream)));
+}
+
+niti_status niti_relu_mask(int8_t* e, const int8_t* a, int64_t n, void* stream) {
+    if (n < 0) return NITI_ERR_SHAPE;
+    if ((!e || !a) && n > 0) return NITI_ERR_NULL;
+    if (too_big(n)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(relu_mask_run(e, a, n, as_stream(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,227 @@
+// Device-side building blocks shared by the NITI kernels: magnitude
+// rounding (Algorithm 3 and round-to-nearest), the effective bitwidth of a
+// block maximum (Section 3.2), fast unsigned division for index decoding,
+// wave reductions and the per-call statistics epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "niti.h"
+
+namespace niti {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Effective bitwidth B(v) of a magnitude: bits needed to write it (Section 3.2).
+__host__ __device__ inline int bitlen64(uint64_t m) {
+#ifdef __HIP_DEVICE_COMPILE__
+    return m ? 64 - __clzll((long long)m) : 0;
+#else
+    return m ? 64 - __builtin_clzll(m) : 0;
+#endif
+}
+
+// Binary point for a block: shift just enough that the maximum keeps
+// `target` magnitude bits (Algorithm 1: max(0, b - 7); Section 3.3: b - m_u).
+__host__ __device__ inline int block_bp(uint64_t mx, int target) {
+    int bp = bitlen64(mx) - target;
+    return bp < 0 ? 0 : bp;
+}
+
+// Constants of one rounding shift, uniform over a whole tensor.
+struct RoundK {
+    uint32_t bp;     // binary point (0..31 for int32 data, 0..63 for int64)
+    uint32_t odd;    // 1 when bp is odd: the lowest fraction bit is dropped
+    uint32_t h;      // half width of the (even) fraction
+    uint64_t fmask;  // bp low bits
+    uint64_t hmask;  // h low bits
+    int rtn;         // 1: round to nearest instead
+};
+
+__host__ __device__ inline RoundK make_round(int bp, int mode) {
+    RoundK k;
+    k.bp = (uint32_t)bp;
+    k.odd = (uint32_t)bp & 1u;
+    k.h = ((uint32_t)bp - k.odd) >> 1;
+    k.fmask = bp >= 64 ? ~0ull : ((1ull << bp) - 1ull);
+    k.hmask = (1ull << k.h) - 1ull;
+    k.rtn = mode == NITI_ROUND_RTN;
+    return k;
+}
+
+// Pseudo stochastic rounding of an unsigned 32-bit magnitude (Algorithm 3):
+// integer part q = x >> bp, fraction f = low bp bits (odd bp: its lowest
+// bit dropped); q is bumped when the upper half of f exceeds the lower half,
+// the lower half standing in for a random draw.  Held at 127.
+__device__ __forceinline__ uint32_t round_mag32(uint32_t x, const RoundK& k) {
+    uint32_t q = x >> k.bp;
+    if (k.rtn) {
+        q += k.bp ? ((x >> (k.bp - 1)) & 1u) : 0u;
+    } else {
+        uint32_t f = (x & (uint32_t)k.fmask) >> k.odd;
+        uint32_t thi = f >> k.h;
+        uint32_t rlo = f & (uint32_t)k.hmask;
+        q += thi > rlo ? 1u : 0u;
+    }
+    return q < 127u ? q : 127u;
+}
+
+__device__ __forceinline__ uint64_t round_mag64(uint64_t x, const RoundK& k) {
+    uint64_t q = k.bp >= 64 ? 0 : (x >> k.bp);
+    if (k.rtn) {
+        q += k.bp ? ((x >> (k.bp - 1)) & 1ull) : 0ull;
+    } else {
+        uint64_t f = (x & k.fmask) >> k.odd;
+        uint64_t thi = f >> k.h;
+        uint64_t rlo = f & k.hmask;
+        q += thi > rlo ? 1ull : 0ull;
+    }
+    return q < 127ull ? q : 127ull;
+}
+
+__device__ __forceinline__ uint32_t mag32(int32_t v) {
+    return v < 0 ? 0u - (uint32_t)v : (uint32_t)v;
+}
+
+__device__ __forceinline__ int8_t round_i32(int32_t v, const RoundK& k) {
+    int32_t q = (int32_t)round_mag32(mag32(v), k);
+    return (int8_t)(v < 0 ? -q : q);
+}
+
+__device__ __forceinline__ int8_t round_i64(int64_t v, const RoundK& k) {
+    uint64_t m = v < 0 ? 0ull - (uint64_t)v : (uint64_t)v;
+    int32_t q = (int32_t)round_mag64(m, k);
+    return (int8_t)(v < 0 ? -q : q);
+}
+
+// ---------------------------------------------------------------------------
+// Unsigned division by a runtime-constant divisor d >= 1 for n < 2^31
+// (multiply-high with a precomputed magic number, as in Granlund and
+// Montgomery, "Division by invariant integers using multiplication", 1994).
+struct FastDiv {
+    uint32_t d;
+    uint32_t mul;
+    uint32_t shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f;
+    f.d = d ? d : 1;
+    uint32_t l = 0;
+    while ((1ull << l) < f.d) l++;
+    // mul = floor(2^32 (2^l - d) / d) + 1, quotient = (mulhi(n, mul) + n) >> l
+    f.mul = (uint32_t)((((1ull << l) - f.d) << 32) / f.d + 1);
+    f.shift = l;
+    return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+    uint32_t t = __umulhi(n, f.mul);
+    return (uint32_t)(((uint64_t)t + n) >> f.shift);
+}
+
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        uint64_t u = __shfl_xor(v, o, kWave);
+        v = u > v ? u : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ __forceinline__ int64_t wave_max_i64(int64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        int64_t u = __shfl_xor(v, o, kWave);
+        v = u > v ? u : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t load_acc_max(niti_stats* st) {
+    return __hip_atomic_load(&st->acc_max, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Fold a block's maximum into the tensor maximum.  The tensor maximum only
+// grows, so a value not above one already observed can be skipped.
+__device__ __forceinline__ void publish_max(niti_stats* st, uint64_t m) {
+    if (m > load_acc_max(st)) atomicMax((unsigned long long*)&st->acc_max, (unsigned long long)m);
+}
+
+// Workgroup-wide maximum, folded into the tensor maximum by one thread.
+// Every thread of the block must call it.
+__device__ __forceinline__ void block_publish_max(niti_stats* st, uint64_t m) {
+    __shared__ uint64_t red[16];
+    m = wave_max_u64(m);
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    if (lane == 0) red[wv] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int nw = (blockDim.x + kWave - 1) / kWave;
+        uint64_t r = 0;
+        for (int i = 0; i < nw; i++) r = red[i] > r ? red[i] : r;
+        if (r) publish_max(st, r);
+    }
+}
+
+// Exponent operands of a call that forms an output exponent.
+struct ExpArgs {
+    const int8_t* s_a;  // first operand exponent (or NULL)
+    const int8_t* s_b;  // second operand exponent (or NULL)
+    int8_t* s_out;      // output exponent (or NULL: not formed)
+};
+
+// Last step of a call: derive b and bp from the tensor maximum, form the
+// output exponent (Algorithm 2: s_q = s_q32 + bp), record the statistics,
+// make bp the next call's first guess, and leave the working fields zero.
+__device__ inline void finalize_stats(niti_stats* st, int target, ExpArgs ex, uint32_t static_flags,
+                                      int hinted, int hint) {
+    const uint64_t mx = __hip_atomic_load(&st->acc_max, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t wf = __hip_atomic_load(&st->wflags, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    const int b = bitlen64(mx);
+    const int bp = block_bp(mx, target);
+    uint32_t fl = wf | static_flags;
+    if (hinted && bp != hint) {
+        fl |= NITI_FLAG_HINT_MISS;
+        st->misses += 1;
+    }
+    int s = 0;
+    if (ex.s_out) {
+        s = (ex.s_a ? (int)*ex.s_a : 0) + (ex.s_b ? (int)*ex.s_b : 0) + bp;
+        if (s > 127) { s = 127; fl |= NITI_FLAG_EXP_RANGE; }
+        if (s < -128) { s = -128; fl |= NITI_FLAG_EXP_RANGE; }
+        *ex.s_out = (int8_t)s;
+    }
+    st->max_abs = mx;
+    st->b = b;
+    st->bp = bp;
+    st->flags = (int32_t)fl;
+    st->s_out = s;
+    st->bp_hint = bp;
+    st->calls += 1;
+    __hip_atomic_store(&st->acc_max, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&st->wflags, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&st->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called once per workgroup by thread 0 after the group's work is issued;
+// returns true in exactly one workgroup, the last to arrive.
+__device__ __forceinline__ bool last_block_arrived(niti_stats* st, uint32_t nblocks) {
+    __threadfence();
+    const uint32_t t = __hip_atomic_fetch_add(&st->ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    return t == nblocks - 1;
+}
+
+}  // namespace niti

@@ -1,0 +1,93 @@
+// Internal launch interfaces between the C ABI (niti_api.hip) and the
+// kernels.  Nothing here is exported.
+#pragma once
+
+#include "niti_device.h"
+
+namespace niti {
+
+constexpr int kMaxProblems = 4;   // sub-pixel classes of a stride-2 back-propagation
+constexpr int kPhaseFirst = 0;
+constexpr int kPhaseFixup = 1;
+constexpr int kFixupGrid = 1024;  // workgroups of the fix-up launch
+
+// One implicit-GEMM problem (see igemm.hip for the index form).
+struct IgemmProblem {
+    const int8_t* act;   // NHWC activation operand [img][H][W][C]
+    const int8_t* wgt;   // weight operand [Nout][R][L]
+    int8_t* out;         // NHWC output tensor base
+    const int8_t* mask;  // backward ReLU source, addressed like out (or NULL)
+    int32_t M;           // output pixels of this problem: img * OHc * OWc
+    int32_t Nout;        // output channels
+    int32_t R, L, Lpad, Ktot;
+    int32_t H, W, C;     // activation geometry
+    int32_t OHc, OWc;    // this problem's output grid
+    int32_t st, off_h, off_w;  // input row = out row * st + off (+ tap)
+    int32_t OH, OW, ldo;       // output tensor rows, columns, channel stride
+    int32_t os, oa, ob;        // out row = grid row * os + oa (cols: ob)
+    int32_t tiles_m, tiles_n, tile_base;
+    FastDiv div_ohw, div_ow;
+};
+
+struct IgemmBatch {
+    IgemmProblem p[kMaxProblems];
+    int32_t nprob;
+    int32_t total_tiles;
+};
+
+struct IgemmCtl {
+    niti_stats* stats;
+    ExpArgs ex;
+    int32_t target;
+    int32_t relu;
+    int32_t mode;
+    int32_t phase;
+    uint32_t static_flags;
+};
+
+hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
+
+// Weight-gradient contraction, split over the pixel reduction, accumulated
+// into g32 [K][R][S*C] with 32-bit atomic adds (exact mod 2^32).
+struct WgradProblem {
+    const int8_t* x;   // NHWC [img][H][W][C]
+    const int8_t* dy;  // NHWC [img][P][Q][K]
+    int32_t* g32;      // [K][R*S*C], zero on entry
+    int32_t H, W, C, K, R, S, P, Q;
+    int32_t sh, sw, ph, pw;
+    int32_t L, ncol;   // L = S*C, ncol = R*L
+    int32_t npix;      // img*P*Q
+    int32_t chunk;     // pixels per split (multiple of 64)
+    FastDiv div_pq, div_q, div_l, div_c;
+};
+
+hipError_t wgrad_run(WgradProblem& p, hipStream_t stream);
+
+// Elementwise / reduction passes.
+hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t max_abs_i32(const int32_t* x, int64_t n, niti_stats* st, hipStream_t s);
+// Round with a fixed bp (stats may be NULL) or with the block bp derived
+// from stats->acc_max (bp < 0), finalizing stats in the latter case.
+hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int target, int mode,
+                         niti_stats* st, ExpArgs ex, hipStream_t s);
+hipError_t update_run(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu,
+                      int mode, niti_stats* st, uint32_t static_flags, hipStream_t s);
+hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
+                    int8_t* err, int64_t* e64, int64_t batch, int64_t classes, int mode,
+                    niti_stats* st, hipStream_t s);
+// Back-propagation filters: wc[class][c][t][u][k] = w[k][r(t)][s(u)][c].
+struct DgradClass {
+    int32_t r0, s0, T, U;  // first tap and tap counts of the class
+    int64_t offset;        // byte offset of this class's filter in the packed buffer
+};
+hipError_t repack_dgrad_run(const int8_t* w, int8_t* out, const DgradClass* cls, int ncls,
+                            int K, int R, int S, int C, int sh, int sw, hipStream_t s);
+hipError_t quantize_run(const uint8_t* px, int8_t* x, int64_t n, int64_t c, int64_t h, int64_t w,
+                        int64_t cp, hipStream_t s);
+hipError_t maxpool_fwd_run(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, int64_t h,
+                           int64_t w, int64_t c, hipStream_t s);
+hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
+                           int64_t w, int64_t c, hipStream_t s);
+hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s);
+
+}  // namespace niti

@@ -1,0 +1,244 @@
+// Weight-gradient contraction g32 = a(l-1) (x) e(l) (Algorithm 1; Section
+// 3.3) on int8 MFMA.
+//
+//   g32[k][r][s*C + c] = sum over pixels (n, p, q) of
+//                        dy[n][p][q][k] * x[n][p*sh - ph + r][q*sw - pw + s][c]
+//
+// The reduction runs over the N*P*Q output pixels, far longer than the
+// output, so the pixel range is split across workgroups and each group adds
+// its partial tile into g32 with 32-bit atomic adds.  Integer addition is
+// associative mod 2^32, so the result does not depend on the split or the
+// order of arrival.
+//
+// Both operands arrive pixel-major from NHWC memory (channels contiguous)
+// while the MFMA wants each lane's 16 bytes along the reduction (pixels).
+// Each thread therefore loads four pixels' dwords, transposes the 4x4 byte
+// block in registers (v_perm_b32) and writes pixel-contiguous dwords into
+// LDS; the MFMA fragments are then plain 16-byte LDS reads.
+#include "niti_internal.h"
+
+namespace niti {
+
+namespace {
+
+constexpr int BKP = 64;     // pixels per main-loop step
+constexpr int PITCH = 80;   // LDS row pitch in bytes (64 + 16 pad)
+constexpr int NTHREADS = 256;
+
+// 4x4 byte transpose: in[i] holds bytes (row i, col 0..3); out[b] holds
+// bytes (row 0..3, col b).
+__device__ __forceinline__ void transpose4x4(const uint32_t in[4], uint32_t out[4]) {
+    const uint32_t t0 = __builtin_amdgcn_perm(in[1], in[0], 0x05010400u);
+    const uint32_t t1 = __builtin_amdgcn_perm(in[1], in[0], 0x07030602u);
+    const uint32_t t2 = __builtin_amdgcn_perm(in[3], in[2], 0x05010400u);
+    const uint32_t t3 = __builtin_amdgcn_perm(in[3], in[2], 0x07030602u);
+    out[0] = __builtin_amdgcn_perm(t2, t0, 0x05040100u);
+    out[1] = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
+    out[2] = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
+    out[3] = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+}
+
+struct PixPos {
+    int n, p, q;
+};
+
+__device__ __forceinline__ PixPos decode_pix(const WgradProblem& P, int pix) {
+    PixPos r;
+    r.n = (int)fdiv((uint32_t)pix, P.div_pq);
+    const int rem = pix - r.n * P.P * P.Q;
+    r.p = (int)fdiv((uint32_t)rem, P.div_q);
+    r.q = rem - r.p * P.Q;
+    return r;
+}
+
+__device__ __forceinline__ void next_pix(const WgradProblem& P, PixPos& x) {
+    if (++x.q == P.Q) {
+        x.q = 0;
+        if (++x.p == P.P) {
+            x.p = 0;
+            ++x.n;
+        }
+    }
+}
+
+template <int TBK, int TBC>
+__global__ __launch_bounds__(NTHREADS) void wgrad_kernel(WgradProblem P) {
+    constexpr int WTK = TBK / 2, WTC = TBC / 2;
+    constexpr int FK = WTK / 32, FC = WTC / 32;
+    constexpr int XCD = TBC / 4;                 // column dwords per pixel row of the x tile
+    constexpr int XGP = NTHREADS / XCD;          // 4-pixel groups per pass (x)
+    constexpr int XPASS = (BKP / 4) / XGP;       // passes over the 16 pixel groups
+    constexpr int DKD = TBK / 4;
+    constexpr int DGP = NTHREADS / DKD;
+    constexpr int DPASS = (BKP / 4) / DGP;
+
+    __shared__ int8_t xs[2][TBC * PITCH];
+    __shared__ int8_t ds[2][TBK * PITCH];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wk = wave & 1, wc = wave >> 1;
+    const int c0 = blockIdx.x * TBC;
+    const int k0 = blockIdx.y * TBK;
+    const int pbeg = blockIdx.z * P.chunk;
+    const int pend = min(P.npix, pbeg + P.chunk);
+    if (pbeg >= pend) return;
+
+    // This thread's x column dword (fixed over the whole reduction).
+    const int xcd = threadIdx.x % XCD, xg = threadIdx.x / XCD;
+    const int col = c0 + 4 * xcd;
+    const bool col_ok = col < P.ncol;
+    int cr = 0, cs = 0, cc = 0;
+    if (col_ok) {
+        cr = (int)fdiv((uint32_t)col, P.div_l);
+        const int j = col - cr * P.L;
+        cs = (int)fdiv((uint32_t)j, P.div_c);
+        cc = j - cs * P.C;
+    }
+    // This thread's dy channel dword.
+    const int dkd = threadIdx.x % DKD, dg = threadIdx.x / DKD;
+    const int kch = k0 + 4 * dkd;
+    const bool k_ok = kch < P.K;  // K % 4 == 0 is not required: tail handled bytewise
+
+    uint32_t xr[XPASS][4], dr[DPASS][4];
+
+    auto gload = [&](int pix0) {
+#pragma unroll
+        for (int ps = 0; ps < XPASS; ps++) {
+            const int pb = pix0 + 4 * (xg + ps * XGP);
+            PixPos pp = decode_pix(P, pb < P.npix ? pb : 0);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                uint32_t v = 0;
+                const int pix = pb + i;
+                if (col_ok && pix < pend) {
+                    const int h = pp.p * P.sh - P.ph + cr;
+                    const int w = pp.q * P.sw - P.pw + cs;
+                    if ((unsigned)h < (unsigned)P.H && (unsigned)w < (unsigned)P.W)
+                        v = *(const uint32_t*)(P.x + (((int64_t)pp.n * P.H + h) * P.W + w) * P.C + cc);
+                }
+                xr[ps][i] = v;
+                next_pix(P, pp);
+            }
+        }
+#pragma unroll
+        for (int ps = 0; ps < DPASS; ps++) {
+            const int pb = pix0 + 4 * (dg + ps * DGP);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                uint32_t v = 0;
+                const int pix = pb + i;
+                if (k_ok && pix < pend) {
+                    const int8_t* src = P.dy + (int64_t)pix * P.K + kch;
+                    if (kch + 4 <= P.K && (((uintptr_t)src) & 3) == 0) {
+                        v = *(const uint32_t*)src;
+                    } else {
+                        for (int b = 0; b < 4 && kch + b < P.K; b++)
+                            v |= (uint32_t)(uint8_t)src[b] << (8 * b);
+                    }
+                }
+                dr[ps][i] = v;
+            }
+        }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int ps = 0; ps < XPASS; ps++) {
+            uint32_t t[4];
+            transpose4x4(xr[ps], t);
+            const int pg = xg + ps * XGP;
+#pragma unroll
+            for (int b = 0; b < 4; b++) *(uint32_t*)&xs[buf][(4 * xcd + b) * PITCH + 4 * pg] = t[b];
+        }
+#pragma unroll
+        for (int ps = 0; ps < DPASS; ps++) {
+            uint32_t t[4];
+            transpose4x4(dr[ps], t);
+            const int pg = dg + ps * DGP;
+#pragma unroll
+            for (int b = 0; b < 4; b++) *(uint32_t*)&ds[buf][(4 * dkd + b) * PITCH + 4 * pg] = t[b];
+        }
+    };
+
+    v16i acc[FC][FK];
+#pragma unroll
+    for (int a = 0; a < FC; a++)
+#pragma unroll
+        for (int b = 0; b < FK; b++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[a][b][e] = 0;
+
+    const int nsteps = (pend - pbeg + BKP - 1) / BKP;
+    gload(pbeg);
+    sstore(0);
+    __syncthreads();
+    for (int it = 0; it < nsteps; it++) {
+        const int buf = it & 1;
+        if (it + 1 < nsteps) gload(pbeg + (it + 1) * BKP);
+#pragma unroll
+        for (int ks = 0; ks < 2; ks++) {
+            const int koff = ks * 32 + (lane >> 5) * 16;
+            v4i fa[FC], fb[FK];
+#pragma unroll
+            for (int a = 0; a < FC; a++)
+                fa[a] = *(const v4i*)&xs[buf][(wc * WTC + a * 32 + (lane & 31)) * PITCH + koff];
+#pragma unroll
+            for (int b = 0; b < FK; b++)
+                fb[b] = *(const v4i*)&ds[buf][(wk * WTK + b * 32 + (lane & 31)) * PITCH + koff];
+#pragma unroll
+            for (int a = 0; a < FC; a++)
+#pragma unroll
+                for (int b = 0; b < FK; b++)
+                    acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+        }
+        if (it + 1 < nsteps) sstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    // acc[a][b] element 4*jj + i: column c0 + wc*WTC + a*32 + 8*jj + 4*(lane/32) + i,
+    // channel k0 + wk*WTK + b*32 + lane%32.
+#pragma unroll
+    for (int b = 0; b < FK; b++) {
+        const int k = k0 + wk * WTK + b * 32 + (lane & 31);
+        if (k >= P.K) continue;
+        int32_t* grow = P.g32 + (int64_t)k * P.ncol;
+#pragma unroll
+        for (int a = 0; a < FC; a++)
+#pragma unroll
+            for (int jj = 0; jj < 4; jj++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int cidx = c0 + wc * WTC + a * 32 + 8 * jj + 4 * (lane >> 5) + i;
+                    const int32_t v = acc[a][b][4 * jj + i];
+                    if (cidx < P.ncol && v != 0)
+                        __hip_atomic_fetch_add(grow + cidx, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+    }
+}
+
+template <int TBK, int TBC>
+hipError_t launch_wgrad(WgradProblem& p, hipStream_t stream) {
+    const int tc = (p.ncol + TBC - 1) / TBC;
+    const int tk = (p.K + TBK - 1) / TBK;
+    const int tiles = tc * tk;
+    const int steps = (p.npix + BKP - 1) / BKP;
+    // Enough workgroups to fill the chip, but at least 8 steps per group so
+    // the atomic epilogue stays small next to the main loop.
+    int splits = (2048 + tiles - 1) / tiles;
+    int max_splits = (steps + 7) / 8;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    int chunk_steps = (steps + splits - 1) / splits;
+    p.chunk = chunk_steps * BKP;
+    splits = (steps + chunk_steps - 1) / chunk_steps;
+    hipLaunchKernelGGL((wgrad_kernel<TBK, TBC>), dim3(tc, tk, splits), dim3(NTHREADS), 0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t wgrad_run(WgradProblem& p, hipStream_t stream) {
+    if (p.K <= 64) return launch_wgrad<64, 128>(p, stream);
+    return launch_wgrad<128, 128>(p, stream);
+}
+
+}  // namespace niti

@@ -1,0 +1,99 @@
+"""The C ABI library loads without a GPU, exports every symbol its header
+declares, and rejects bad arguments on the host before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2009_13108_amd import niti
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "niti.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(niti_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_seven_hot_path_calls():
+    names = declared_functions()
+    for n in ["niti_gemm_fwd", "niti_conv_fwd", "niti_conv_bwd_data", "niti_conv_bwd_weight",
+              "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = niti.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    assert set(declared_functions()) == set(niti.EXPORTS)
+
+
+def test_stats_layout_matches_header():
+    assert niti.lib().niti_stats_bytes() == 64 == niti.STATS_DTYPE.itemsize
+
+
+def test_status_strings():
+    for s in range(0, -7, -1):
+        assert isinstance(niti.status_str(s), str) and niti.status_str(s)
+
+
+def test_workspace_sizes():
+    d = niti.ConvDesc.make(2, 8, 8, 64, 128, 3, 3, 1, 1)
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d) >= 128 * 9 * 64
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, d) >= 128 * 9 * 64 * 4
+    assert niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, 128, 1000) >= 128 * 1000 * 8
+    assert niti.workspace_bytes(niti.OP_CONV_FWD, d) == 0
+
+
+FAKE = ctypes.c_void_p(0x100000)   # never dereferenced: every call below fails validation
+
+
+def test_gemm_rejects_on_host():
+    L = niti.lib()
+    S = FAKE
+    assert L.niti_gemm_fwd(None, FAKE, FAKE, 4, 4, 4, None, None, None, 7, 0, 0, S, None) == -1
+    assert L.niti_gemm_fwd(FAKE, FAKE, None, 4, 4, 0, None, None, None, 7, 0, 0, S, None) == -1
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 0, 4, 4, None, None, None, 7, 0, 0, S, None) == -2
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, -1, None, None, None, 7, 0, 0, S, None) == -2
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, None, None, None, 0, 0, 0, S, None) == -6
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, None, None, None, 7, 0, 5, S, None) == -6
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, FAKE, None, None, 7, 0, 0, S, None) == -1
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, None, None, None, 7, 0, 0, None, None) == -1
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 1 << 20, 1 << 20, 4, None, None, None, 7, 0, 0, S, None) == -3
+
+
+def test_conv_rejects_on_host():
+    L = niti.lib()
+    d = niti.ConvDesc.make(2, 8, 8, 3, 16, 3, 3, 1, 1)           # c % 4 != 0
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -3
+    d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 3, 1)           # stride 3
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -3
+    d = niti.ConvDesc.make(2, 2, 2, 4, 16, 5, 5, 1, 0)           # filter larger than padded input
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -2
+    d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 1, 1)
+    assert L.niti_conv_fwd(None, FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -1
+    assert L.niti_conv_bwd_data(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, None, 0, None) == -4
+    assert L.niti_conv_bwd_data(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, 16, None) == -4
+    assert L.niti_conv_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, 5, 0, FAKE, None, 0, None) == -4
+    assert L.niti_conv_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, 0, FAKE, FAKE, 1 << 20, None) == -6
+    assert L.niti_conv_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, 9, 0, FAKE, FAKE, 1 << 20, None) == -6
+
+
+def test_other_calls_reject_on_host():
+    L = niti.lib()
+    assert L.niti_round_psr(FAKE, FAKE, -1, 3, 7, 0, None, None, None, None) == -2
+    assert L.niti_round_psr(FAKE, FAKE, 10, -1, 7, 0, None, None, None, None) == -1   # derive needs stats
+    assert L.niti_round_psr(FAKE, FAKE, 10, 32, 7, 0, None, None, None, None) == -6
+    assert L.niti_round_psr(FAKE, FAKE, 10, 3, 7, 0, FAKE, None, None, None) == -1
+    assert L.niti_int_ce_loss_grad(FAKE, FAKE, FAKE, FAKE, 4, 10, 0, FAKE, None, 0, None) == -4
+    assert L.niti_int_ce_loss_grad(FAKE, FAKE, FAKE, FAKE, 4, 100000, 0, FAKE, FAKE, 1 << 30, None) == -6
+    assert L.niti_int_ce_loss_grad(FAKE, None, FAKE, FAKE, 4, 10, 0, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.niti_sgd_update(FAKE, FAKE, 10, 0, 0, FAKE, None) == -6
+    assert L.niti_sgd_update(FAKE, FAKE, 10, 5, 0, None, None) == -1
+    assert L.niti_maxpool2_fwd(FAKE, FAKE, FAKE, 1, 3, 4, 4, None) == -2
+    assert L.niti_quantize_u8(FAKE, FAKE, 1, 3, 4, 4, 2, None) == -2
+    assert L.niti_relu_mask(FAKE, FAKE, -4, None) == -2

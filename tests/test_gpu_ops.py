@@ -1,0 +1,305 @@
+"""GPU parity of every C-ABI entry point against the CPU oracle.
+
+Each case draws seeded inputs, runs the HIP library through its C ABI and
+the oracle on the same bytes, and requires byte-identical int8 outputs,
+identical int32 gradients and identical block statistics (max, b, bp) and
+exponents.  Sizes span several tiles with ragged edges; each case is also
+run twice so the second call exercises the speculated-shift path.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2009_13108_amd import inputs as I
+from paper_2009_13108_amd import niti
+from helpers import dev, host, kcrs, krsc, nchw, nhwc, say, same_stats
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    niti.lib()
+
+
+def _i8(v):
+    import torch
+    return torch.tensor([v], dtype=torch.int8, device="cuda")
+
+
+GEMM_CASES = [
+    # M, N, K, relu, mode, distribution of B
+    (1, 1, 1, False, oracle.PSR, "w"),
+    (7, 5, 3, False, oracle.PSR, "w"),
+    (33, 17, 65, True, oracle.PSR, "w"),
+    (32, 128, 784, False, oracle.PSR, "e5"),
+    (300, 200, 784, True, oracle.PSR, "w"),
+    (257, 129, 1000, False, oracle.RTN, "w"),
+    (64, 10, 128, False, oracle.PSR, "w"),
+    (129, 300, 0, False, oracle.PSR, "w"),
+    (513, 257, 333, True, oracle.PSR, "e5"),
+]
+
+
+@pytest.mark.parametrize("case", GEMM_CASES)
+def test_gemm_fwd_parity(case):
+    import torch
+    M, N, K, relu, mode, dist = case
+    say("gemm_fwd", case)
+    A = I.activations(1000 + M, (M, K))
+    B = (I.weights if dist == "w" else I.errors5)(2000 + N, (N, K))
+    exp_out, _, st = oracle.gemm_fwd(A, B, relu=relu, mode=mode)
+    s_exp, _ = oracle.out_exponent(-7, -9, st["bp"])
+    dA, dB = dev(A), dev(B)
+    C = torch.empty((M, N), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    sa, sb, sc = _i8(-7), _i8(-9), _i8(0)
+    for rep in range(2):
+        C.fill_(99)
+        niti.gemm_fwd(dA, dB, C, stats, sa, sb, sc, 7, relu, mode)
+        torch.cuda.synchronize()
+        g = niti.read_stats(stats)[0]
+        assert (host(C) == exp_out).all(), "rep %d" % rep
+        assert same_stats(g, st), (g, st)
+        assert int(host(sc)[0]) == s_exp
+        assert g["calls"] == rep + 1
+    assert g["misses"] <= 1 and g["flags"] & niti.FLAG_HINT_MISS == 0
+
+
+def test_gemm_fwd_hint_miss_recomputes():
+    import torch
+    say("gemm_fwd hint miss")
+    # One stats block reused across tensors with different block exponents:
+    # every call's first guess is wrong and the output must be recomputed.
+    A1 = I.activations(1, (64, 256)); B1 = I.weights(2, (96, 256))
+    A2 = I.errors5(3, (64, 256)); B2 = I.errors5(4, (96, 256))
+    stats = niti.new_stats()
+    for (A, B) in [(A1, B1), (A2, B2), (A1, B1)]:
+        exp_out, _, st = oracle.gemm_fwd(A, B)
+        C = torch.empty((64, 96), dtype=torch.int8, device="cuda")
+        niti.gemm_fwd(dev(A), dev(B), C, stats)
+        torch.cuda.synchronize()
+        g = niti.read_stats(stats)[0]
+        assert (host(C) == exp_out).all() and same_stats(g, st)
+        assert g["flags"] & niti.FLAG_HINT_MISS
+
+
+CONV_CASES = [
+    # n, c, h, w, k, r, s, stride, pad, relu
+    (1, 4, 5, 5, 4, 3, 3, 1, 1, False),
+    (2, 4, 7, 6, 8, 3, 3, 1, 1, True),
+    (2, 8, 9, 9, 12, 3, 3, 2, 1, False),
+    (1, 4, 11, 11, 8, 7, 7, 2, 3, True),
+    (2, 4, 8, 8, 20, 1, 1, 2, 0, False),
+    (1, 8, 6, 7, 12, 1, 1, 1, 0, True),
+    (3, 4, 5, 5, 4, 3, 3, 1, 0, False),
+    (1, 4, 6, 6, 8, 2, 3, 2, 2, False),
+    (2, 64, 14, 14, 64, 3, 3, 1, 1, True),
+    (2, 64, 15, 15, 128, 3, 3, 2, 1, False),
+    (2, 32, 16, 16, 96, 1, 1, 2, 0, True),
+    (1, 4, 32, 32, 64, 7, 7, 2, 3, True),
+    (4, 128, 7, 7, 130, 3, 3, 1, 1, False),
+]
+
+
+def _conv_inputs(case, seed):
+    n, c, h, w, k, r, s, st, pd, relu = case
+    d = oracle.conv_desc(n, c, h, w, k, r, s, st, pd)
+    P, Q = oracle.conv_out_hw(d)
+    x = I.activations(seed + 1, (n, c, h, w))
+    wt = I.weights(seed + 2, (k, c, r, s))
+    dy = I.errors8(seed + 3, (n, k, P, Q))
+    gd = niti.ConvDesc.make(n, h, w, c, k, r, s, st, pd)
+    return d, gd, x, wt, dy
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_fwd_parity(case):
+    import torch
+    say("conv_fwd", case)
+    d, gd, x, wt, dy = _conv_inputs(case, 10 * case[1] + case[4])
+    relu = case[-1]
+    exp_out, _, st = oracle.conv_fwd(d, x, wt, relu=relu)
+    s_exp, _ = oracle.out_exponent(-3, -8, st["bp"])
+    y = torch.empty(gd.y_shape(), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    sx, sw, sy = _i8(-3), _i8(-8), _i8(0)
+    dx_, dw_ = dev(nhwc(x)), dev(krsc(wt))
+    for rep in range(2):
+        y.fill_(77)
+        niti.conv_fwd(gd, dx_, dw_, y, stats, sx, sw, sy, relu=relu)
+        torch.cuda.synchronize()
+        g = niti.read_stats(stats)[0]
+        assert (nchw(host(y)) == exp_out).all(), "rep %d" % rep
+        assert same_stats(g, st) and int(host(sy)[0]) == s_exp
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_bwd_data_parity(case):
+    import torch
+    say("conv_bwd_data", case)
+    d, gd, x, wt, dy = _conv_inputs(case, 7 * case[2] + case[4])
+    use_mask = case[-1]
+    relu_src = I.weights(55, (d.n, d.c, d.h, d.w)) if use_mask else None
+    exp_out, _, st = oracle.conv_bwd_data(d, dy, wt, relu_src=relu_src)
+    dx = torch.empty(gd.x_shape(), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    ws = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, gd))
+    mask = dev(nhwc(relu_src)) if use_mask else None
+    for rep in range(2):
+        dx.fill_(55)
+        niti.conv_bwd_data(gd, dev(nhwc(dy)), dev(krsc(wt)), dx, stats, ws, relu_src=mask)
+        torch.cuda.synchronize()
+        g = niti.read_stats(stats)[0]
+        assert (nchw(host(dx)) == exp_out).all(), "rep %d" % rep
+        assert same_stats(g, st)
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+@pytest.mark.parametrize("mu", [5, 3])
+def test_conv_bwd_weight_parity(case, mu):
+    import torch
+    say("conv_bwd_weight", case, mu)
+    d, gd, x, wt, dy = _conv_inputs(case, 3 * case[3] + case[1])
+    exp_w, exp_g32, st = oracle.conv_bwd_weight(d, x, dy, wt, mu=mu)
+    w_dev = dev(krsc(wt))
+    g32 = torch.empty(gd.w_shape(), dtype=torch.int32, device="cuda")
+    stats = niti.new_stats()
+    niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w_dev, stats, None, g32_out=g32, mu=mu)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)[0]
+    assert (kcrs(host(g32)) == exp_g32).all()
+    assert (kcrs(host(w_dev)) == exp_w).all()
+    assert same_stats(g, st)
+    # same again through the workspace (no g32_out), from the original weights
+    w2 = dev(krsc(wt))
+    ws = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gd))
+    niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w2, stats, ws, mu=mu)
+    torch.cuda.synchronize()
+    assert (kcrs(host(w2)) == exp_w).all()
+
+
+@pytest.mark.parametrize("n", [0, 1, 5, 1000, 65537])
+def test_round_psr_parity(n):
+    import torch
+    say("round_psr", n)
+    x = I.uniform_int(90 + n, (n,), -(1 << 30), (1 << 30), dtype=np.int32)
+    if n > 3:
+        x[3] = -(2 ** 31)
+    exp, st = oracle.shift_round(x, 7)
+    y = torch.empty(n, dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    s_in, s_out = _i8(-5), _i8(0)
+    niti.round_psr(dev(x), y, -1, 7, stats, s_in, s_out)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)[0]
+    assert (host(y) == exp).all() and same_stats(g, st)
+    assert int(host(s_out)[0]) == max(-128, min(127, -5 + st["bp"]))
+    for bp in (0, 1, 4, 9, 31):
+        niti.round_psr(dev(x), y, bp, 7, None, s_in, s_out)
+        torch.cuda.synchronize()
+        assert (host(y) == oracle.round_fixed(x, bp)).all()
+        assert int(host(s_out)[0]) == -5 + bp
+        niti.round_psr(dev(x), y, bp, 7, None, mode=niti.RTN)
+        torch.cuda.synchronize()
+        assert (host(y) == oracle.round_fixed(x, bp, oracle.RTN)).all()
+
+
+def test_round_psr_worked_examples():
+    import json, os, torch
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "psr_examples.json")))
+    for c in g["cases"]:
+        x = dev(np.array([c["x"]], np.int32))
+        y = torch.empty(1, dtype=torch.int8, device="cuda")
+        niti.round_psr(x, y, c["bp"], 7)
+        torch.cuda.synchronize()
+        assert int(host(y)[0]) == c["out"], c
+    for c in g["blocks"]:
+        x = dev(np.array(c["acc"], np.int32))
+        y = torch.empty(len(c["acc"]), dtype=torch.int8, device="cuda")
+        stats = niti.new_stats()
+        niti.round_psr(x, y, -1, c["target"], stats)
+        torch.cuda.synchronize()
+        assert host(y).tolist() == c["out"] and niti.read_stats(stats)[0]["bp"] == c["bp"]
+
+
+@pytest.mark.parametrize("s_a", [-40, -22, -13, -9, -7, -6, -3, 0, 5, 15, 16, 100])
+@pytest.mark.parametrize("shape", [(256, 10), (128, 1000), (3, 65)])
+def test_int_ce_loss_grad_parity(s_a, shape):
+    import torch
+    say("loss", s_a, shape)
+    B, N = shape
+    logits = I.weights(500 + B + s_a, (B, N))
+    labels = I.labels(600 + N, B, N)
+    exp, e32, st = oracle.int_ce_loss_grad(logits, s_a, labels)
+    err = torch.empty((B, N), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    ws = niti.new_workspace(niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, B, N))
+    niti.int_ce_loss_grad(dev(logits), _i8(s_a), dev(labels), err, stats, ws)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)[0]
+    assert (host(err) == exp).all()
+    assert same_stats(g, st, ("max_abs", "b", "bp", "flags"))
+
+
+def test_int_ce_loss_worked_examples():
+    import json, os, torch
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "loss_examples.json")))
+    for c in g["cases"]:
+        lg = np.array(c["logits"], np.int8)
+        B, N = lg.shape
+        err = torch.empty((B, N), dtype=torch.int8, device="cuda")
+        stats = niti.new_stats()
+        ws = niti.new_workspace(niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, B, N))
+        niti.int_ce_loss_grad(dev(lg), _i8(c["s_a"]), dev(np.array(c["labels"], np.int32)), err, stats, ws)
+        torch.cuda.synchronize()
+        assert host(err).tolist() == c["err"], c["why"]
+
+
+@pytest.mark.parametrize("n,mu", [(1, 5), (1000, 5), (36864, 3), (2359296, 1), (7, 8)])
+def test_sgd_update_parity(n, mu):
+    import torch
+    say("sgd_update", n, mu)
+    w = I.weights(700 + n, (n,))
+    g32 = I.uniform_int(800 + n, (n,), -(1 << 26), 1 << 26, dtype=np.int32)
+    exp_w, st = oracle.sgd_update(w, g32, mu)
+    wd = dev(w)
+    stats = niti.new_stats()
+    niti.sgd_update(wd, dev(g32), stats, mu)
+    torch.cuda.synchronize()
+    assert (host(wd) == exp_w).all() and same_stats(niti.read_stats(stats)[0], st)
+
+
+def test_glue_parity():
+    import torch
+    say("glue")
+    px = I.pixels(5, (3, 3, 10, 12))
+    q = oracle.quantize_u8(px)
+    x = torch.empty((3, 10, 12, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(dev(px), x)
+    torch.cuda.synchronize()
+    got = nchw(host(x))
+    assert (got[:, :3] == q).all() and (got[:, 3] == 0).all()
+
+    a = I.weights(6, (2, 16, 8, 12))
+    y_exp, idx_exp = oracle.maxpool2_fwd(a)
+    y = torch.empty((2, 4, 6, 16), dtype=torch.int8, device="cuda")
+    idx = torch.empty((2, 4, 6, 16), dtype=torch.uint8, device="cuda")
+    niti.maxpool2_fwd(dev(nhwc(a)), y, idx)
+    torch.cuda.synchronize()
+    assert (nchw(host(y)) == y_exp).all() and (nchw(host(idx)) == idx_exp).all()
+    dy = I.weights(7, y_exp.shape)
+    dx_exp = oracle.maxpool2_bwd(dy, idx_exp, a.shape)
+    dx = torch.empty((2, 8, 12, 16), dtype=torch.int8, device="cuda")
+    niti.maxpool2_bwd(dev(nhwc(dy)), idx, dx)
+    torch.cuda.synchronize()
+    assert (nchw(host(dx)) == dx_exp).all()
+
+    e = I.weights(8, (1000,)); act = I.weights(9, (1000,))
+    e_exp = oracle.relu_mask(e.copy(), act)
+    ed = dev(e)
+    niti.relu_mask(ed, dev(act))
+    torch.cuda.synchronize()
+    assert (host(ed) == e_exp).all()
