@@ -1,0 +1,186 @@
+"""Integer networks trained with the NITI step (Algorithm 1), run through the
+C ABI.  Every arithmetic step is a libniti call on the current HIP stream;
+this module only owns device buffers and call order.
+
+A network is a list of layer specs:
+  ("fc",   n_in, n_out, relu)
+  ("conv", c_in, c_out, ksize, stride, pad, relu)
+  ("pool",)                                  2x2 stride-2 max pooling
+Activations are NHWC int8 with one int8 exponent per tensor; a fully-
+connected layer after convolutions reads the NHWC tensor flattened in
+(h, w, c) order.  One training step (Algorithm 1):
+  forward: y = round(layer(x)) with s_y = s_x + s_w + bp, ReLU on the int32
+           accumulators where the spec asks;
+  loss:    integer cross-entropy gradient of the logits (Section 3.5);
+  backward, last layer first: the error of the layer input is computed with
+           the weights before their update (the backward ReLU mask of the
+           layer below is fused into that call), then the weight gradient is
+           formed, shifted to mu bits and subtracted from the weights
+           (Section 3.3).  The first layer's input error is not needed.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import niti
+
+
+def _i8(v):
+    import torch
+    return torch.tensor([int(v)], dtype=torch.int8, device="cuda")
+
+
+class IntNet:
+    def __init__(self, specs, in_shape, batch, weights, w_exps, mu=5, mode=niti.PSR):
+        """in_shape = (h, w, c) of the NHWC input (c a multiple of 4 for convs);
+        weights: list of int8 numpy arrays (KRSC for conv, [out][in] for fc),
+        one per weighted layer; w_exps: their static exponents."""
+        import torch
+        self.specs = list(specs)
+        self.batch = batch
+        self.mu = mu
+        self.mode = mode
+        self.layers = []
+        h, w, c = in_shape
+        wi = 0
+        nstats = 0
+        for sp in self.specs:
+            L = {"spec": sp, "in_shape": (h, w, c)}
+            if sp[0] == "conv":
+                _, cin, cout, k, st, pd, relu = sp
+                assert cin == c, (sp, c)
+                d = niti.ConvDesc.make(batch, h, w, c, cout, k, k, st, pd)
+                L.update(kind="conv", desc=d, relu=relu)
+                h, w, c = d.p, d.q, cout
+            elif sp[0] == "fc":
+                _, nin, nout, relu = sp
+                assert nin == h * w * c, (sp, (h, w, c))
+                d = niti.ConvDesc.make(batch, 1, 1, nin, nout, 1, 1, 1, 0)
+                L.update(kind="fc", desc=d, relu=relu, nin=nin, nout=nout)
+                h, w, c = 1, 1, nout
+            elif sp[0] == "pool":
+                L.update(kind="pool")
+                h, w = h // 2, w // 2
+            else:
+                raise ValueError(sp)
+            L["out_shape"] = (h, w, c)
+            if L["kind"] in ("conv", "fc"):
+                arr = np.ascontiguousarray(weights[wi])
+                L["w"] = torch.from_numpy(arr).cuda()
+                L["s_w"] = _i8(w_exps[wi])
+                L["stats"] = nstats       # fwd, bwd_data, bwd_weight
+                nstats += 3
+                wi += 1
+            self.layers.append(L)
+        assert wi == len(weights)
+        self.stats = niti.new_stats(nstats + 1)
+        self.loss_stats = nstats
+        # buffers
+        for L in self.layers:
+            oh, ow, oc = L["out_shape"]
+            L["y"] = torch.empty((batch, oh, ow, oc), dtype=torch.int8, device="cuda")
+            L["s_y"] = _i8(0)
+            L["e_in"] = torch.empty((batch,) + tuple(L["in_shape"]), dtype=torch.int8, device="cuda")
+            if L["kind"] == "pool":
+                L["idx"] = torch.empty_like(L["y"], dtype=torch.uint8)
+        ws = 0
+        for L in self.layers:
+            if L["kind"] in ("conv", "fc"):
+                ws = max(ws, niti.workspace_bytes(niti.OP_CONV_BWD_DATA, L["desc"]),
+                         niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, L["desc"]))
+        n_cls = self.layers[-1]["out_shape"][2]
+        ws = max(ws, niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, batch, n_cls))
+        self.ws = niti.new_workspace(ws)
+        self.err = torch.empty((batch, n_cls), dtype=torch.int8, device="cuda")
+
+    # -------------------------------------------------------------- forward
+    def forward(self, x, s_x):
+        a, s_a = x, s_x
+        for L in self.layers:
+            k = L["kind"]
+            if k == "conv":
+                niti.conv_fwd(L["desc"], a, L["w"], L["y"], self.stats, s_a, L["s_w"], L["s_y"],
+                              relu=L["relu"], mode=self.mode, stats_index=L["stats"])
+            elif k == "fc":
+                niti.gemm_fwd(a.view(self.batch, L["nin"]), L["w"], L["y"].view(self.batch, L["nout"]),
+                              self.stats, s_a, L["s_w"], L["s_y"], 7, L["relu"], self.mode,
+                              stats_index=L["stats"])
+            else:
+                niti.maxpool2_fwd(a, L["y"], L["idx"])
+                L["s_y"] = s_a
+            L["x"] = a
+            a, s_a = L["y"], L["s_y"]
+        return a, s_a
+
+    # -------------------------------------------------------------- backward
+    def backward(self, err):
+        e = err.view(self.layers[-1]["y"].shape)
+        for i in range(len(self.layers) - 1, -1, -1):
+            L = self.layers[i]
+            k = L["kind"]
+            below = self.layers[i - 1] if i > 0 else None
+            need_e_in = i > 0
+            # ReLU mask of the layer whose output is this layer's input
+            mask = None
+            if below is not None and below["kind"] in ("conv", "fc") and below["relu"]:
+                mask = L["x"]
+            if k == "pool":
+                niti.maxpool2_bwd(e, L["idx"], L["e_in"])
+                if below is not None and below["kind"] in ("conv", "fc") and below["relu"]:
+                    niti.relu_mask(L["e_in"], below["y"])
+                e = L["e_in"]
+                continue
+            d = L["desc"]
+            if k == "conv":
+                x_v, e_v, ein_v, m_v = L["x"], e, L["e_in"], mask
+            else:
+                B = self.batch
+                x_v = L["x"].reshape(B, 1, 1, L["nin"])
+                e_v = e.reshape(B, 1, 1, L["nout"])
+                ein_v = L["e_in"].view(B, 1, 1, L["nin"])
+                m_v = mask.reshape(B, 1, 1, L["nin"]) if mask is not None else None
+            w_v = L["w"] if k == "conv" else L["w"].view(L["nout"], 1, 1, L["nin"])
+            if need_e_in:
+                niti.conv_bwd_data(d, e_v, w_v, ein_v, self.stats, self.ws, relu_src=m_v, mode=self.mode,
+                                   stats_index=L["stats"] + 1)
+            niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws, mu=self.mu, mode=self.mode,
+                                 stats_index=L["stats"] + 2)
+            e = L["e_in"]
+
+    def step(self, x, s_x, labels):
+        """One training step; returns (logits, s_logits) of the forward pass."""
+        logits, s_l = self.forward(x, s_x)
+        n_cls = logits.shape[-1]
+        niti.int_ce_loss_grad(logits.view(self.batch, n_cls), s_l, labels, self.err, self.stats, self.ws,
+                              mode=self.mode, stats_index=self.loss_stats)
+        self.backward(self.err)
+        return logits, s_l
+
+    def weights(self):
+        return [L["w"] for L in self.layers if L["kind"] in ("conv", "fc")]
+
+
+# ------------------------------------------------------------------ workloads
+MLP_784 = [("fc", 784, 256, True), ("fc", 256, 128, True), ("fc", 128, 10, False)]
+
+VGG_32 = [("conv", 4, 64, 3, 1, 1, True), ("conv", 64, 64, 3, 1, 1, True), ("pool",),
+          ("conv", 64, 128, 3, 1, 1, True), ("conv", 128, 128, 3, 1, 1, True), ("pool",),
+          ("conv", 128, 256, 3, 1, 1, True), ("conv", 256, 256, 3, 1, 1, True), ("pool",),
+          ("fc", 4096, 10, False)]
+
+# ResNet-18 at 224x224: each distinct layer shape with its multiplicity in
+# the network (name, c_in, c_out, ksize, stride, pad, input size, count).
+RESNET18_LAYERS = [
+    ("stem7x7s2", 4, 64, 7, 2, 3, 224, 1),
+    ("l1_3x3", 64, 64, 3, 1, 1, 56, 4),
+    ("l2_3x3s2", 64, 128, 3, 2, 1, 56, 1),
+    ("l2_1x1s2", 64, 128, 1, 2, 0, 56, 1),
+    ("l2_3x3", 128, 128, 3, 1, 1, 28, 3),
+    ("l3_3x3s2", 128, 256, 3, 2, 1, 28, 1),
+    ("l3_1x1s2", 128, 256, 1, 2, 0, 28, 1),
+    ("l3_3x3", 256, 256, 3, 1, 1, 14, 3),
+    ("l4_3x3s2", 256, 512, 3, 2, 1, 14, 1),
+    ("l4_1x1s2", 256, 512, 1, 2, 0, 14, 1),
+    ("l4_3x3", 512, 512, 3, 1, 1, 7, 3),
+]
+RESNET18_FC = (512, 1000)
