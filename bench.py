@@ -1,0 +1,342 @@
+#!/usr/bin/env python3
+"""Throughput of the NITI integer-training hot path on one MI355X.
+
+Default workload: the ResNet-18-shaped int8 layer set at 224x224, batch 128
+(7x7/2 stem, 3x3 stages at 56/28/14/7 with 64..512 channels, the 1x1/2
+downsample convolutions, the 512->1000 head).  One step runs, for every
+layer of the network (20 convolutions and the head, each with its own
+weights): the forward contraction with fused ReLU / block exponent / pseudo
+stochastic rounding, the error back-propagation with fused rounding and
+backward ReLU mask (not for the stem, whose input error is not needed), and
+the weight gradient with the discrete mu=5 update; the head also runs the
+integer cross-entropy gradient.  Inputs are seeded synthetic int8 tensors
+resident in device memory before timing starts.
+
+Printed: one JSON line.  value = algorithmic int8 tera-operations per second
+of the whole step (2 ops per multiply-accumulate of each contraction,
+counted on the unpadded channel count); roofline = the dominant kernel
+family timed live with HIP events on its stream; cpu_baseline = the CPU
+oracle on a bounded sample of the same layer set.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "int8 TOPS of fused NITI conv/GEMM+round (fwd/bwd/wgrad), % of int8 MFMA peak"
+PEAK_INT8_TOPS = 5000.0       # MI355X dense int8 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def conv_macs(n, c, h, w, k, r, s, st, pd):
+    p = (h + 2 * pd - r) // st + 1
+    q = (w + 2 * pd - s) // st + 1
+    return n * p * q * k * c * r * s
+
+
+# ----------------------------------------------------------------------------
+class ResNetStep:
+    """Buffers and call sequence of one training step over the layer set."""
+
+    def __init__(self, batch=128, seed_cfg=4, mu=5):
+        import torch
+        from paper_2009_13108_amd import inputs as I
+        from paper_2009_13108_amd import model as M
+        from paper_2009_13108_amd import niti
+
+        self.niti = niti
+        self.batch = batch
+        self.mu = mu
+        dev = "cuda"
+        self.layers = []
+        nst = 0
+        ws = 0
+        for li, (name, cin, cout, k, st, pd, hw, count) in enumerate(M.RESNET18_LAYERS):
+            d = niti.ConvDesc.make(batch, hw, hw, cin, cout, k, k, st, pd)
+            x = I.activations(I.base_seed(seed_cfg, 100 + li), (batch, hw, hw, cin), device=dev)
+            c_real = cin
+            if name.startswith("stem"):
+                x[..., 3:] = 0          # 3 image channels, zero-padded to 4
+                c_real = 3
+            dy = I.errors8(I.base_seed(seed_cfg, 200 + li), d.y_shape(), device=dev)
+            ws_ = []
+            for cpy in range(count):
+                w = I.weights(I.base_seed(seed_cfg, 1000 + 10 * li + cpy), d.w_shape(), device=dev)
+                if name.startswith("stem"):
+                    w[..., 3:] = 0
+                ws_.append(w)
+            L = {"name": name, "desc": d, "x": x, "dy": dy, "w": ws_, "count": count,
+                 "y": torch.empty(d.y_shape(), dtype=torch.int8, device=dev),
+                 "dx": torch.empty(d.x_shape(), dtype=torch.int8, device=dev),
+                 "stats": nst, "bwd_data": not name.startswith("stem"),
+                 "macs": conv_macs(batch, c_real, hw, hw, cout, k, k, st, pd)}
+            nst += 3 * count
+            ws = max(ws, niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d),
+                     niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, d))
+            self.layers.append(L)
+        fin, fout = M.RESNET18_FC
+        self.fc_desc = niti.ConvDesc.make(batch, 1, 1, fin, fout, 1, 1, 1, 0)
+        self.feat = I.activations(I.base_seed(seed_cfg, 300), (batch, fin), device=dev)
+        self.wfc = I.weights(I.base_seed(seed_cfg, 301), (fout, fin), device=dev)
+        self.labels = I.labels(I.base_seed(seed_cfg, 302), batch, fout, device=dev)
+        self.logits = torch.empty((batch, fout), dtype=torch.int8, device=dev)
+        self.err = torch.empty((batch, fout), dtype=torch.int8, device=dev)
+        self.dfeat = torch.empty((batch, fin), dtype=torch.int8, device=dev)
+        self.s_feat = torch.tensor([-9], dtype=torch.int8, device=dev)
+        self.s_wfc = torch.tensor([-11], dtype=torch.int8, device=dev)
+        self.s_logits = torch.zeros(1, dtype=torch.int8, device=dev)
+        self.fc_stats = nst
+        nst += 4
+        self.fc_macs = batch * fin * fout
+        ws = max(ws, niti.workspace_bytes(niti.OP_CONV_BWD_DATA, self.fc_desc),
+                 niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, self.fc_desc),
+                 niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, batch, fout))
+        self.ws = niti.new_workspace(ws)
+        self.stats = niti.new_stats(nst)
+        self.fam_ops = {"igemm": 0, "wgrad": 0}
+        for L in self.layers:
+            self.fam_ops["igemm"] += 2 * L["macs"] * L["count"] * (2 if L["bwd_data"] else 1)
+            self.fam_ops["wgrad"] += 2 * L["macs"] * L["count"]
+        self.fam_ops["igemm"] += 2 * 2 * self.fc_macs
+        self.fam_ops["wgrad"] += 2 * self.fc_macs
+        self.ops_per_step = self.fam_ops["igemm"] + self.fam_ops["wgrad"]
+        self.fam_calls = {"igemm": 0, "wgrad": 0}
+        for L in self.layers:
+            self.fam_calls["igemm"] += L["count"] * (2 if L["bwd_data"] else 1)
+            self.fam_calls["wgrad"] += L["count"]
+        self.fam_calls["igemm"] += 2
+        self.fam_calls["wgrad"] += 1
+
+    def step(self, timer=None):
+        niti = self.niti
+        t = timer or (lambda fam, fn: fn())
+        for L in self.layers:
+            d = L["desc"]
+            for c in range(L["count"]):
+                w = L["w"][c]
+                s0 = L["stats"] + 3 * c
+                t("igemm", lambda: niti.conv_fwd(d, L["x"], w, L["y"], self.stats, relu=True, stats_index=s0))
+                if L["bwd_data"]:
+                    t("igemm", lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
+                                                          relu_src=L["x"], stats_index=s0 + 1))
+                t("wgrad", lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws,
+                                                        mu=self.mu, stats_index=s0 + 2))
+        B = self.batch
+        fin, fout = self.fc_desc.c, self.fc_desc.k
+        s = self.fc_stats
+        t("igemm", lambda: niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc,
+                                         self.s_logits, 7, False, stats_index=s))
+        niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats, self.ws,
+                              stats_index=s + 1)
+        fd = self.fc_desc
+        t("igemm", lambda: niti.conv_bwd_data(fd, self.err.view(B, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
+                                              self.dfeat.view(B, 1, 1, fin), self.stats, self.ws,
+                                              relu_src=self.feat.view(B, 1, 1, fin), stats_index=s + 2))
+        t("wgrad", lambda: niti.conv_bwd_weight(fd, self.feat.view(B, 1, 1, fin), self.err.view(B, 1, 1, fout),
+                                                self.wfc.view(fout, 1, 1, fin), self.stats, self.ws,
+                                                mu=self.mu, stats_index=s + 3))
+
+    def misses(self):
+        st = self.niti.read_stats(self.stats)
+        return sum(x["misses"] for x in st), sum(x["calls"] for x in st)
+
+
+class EventTimer:
+    """HIP events around each call of a kernel family, on the stream the
+    library launches on (torch's current stream)."""
+
+    def __init__(self):
+        self.pairs = {"igemm": [], "wgrad": []}
+
+    def __call__(self, fam, fn):
+        import torch
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        self.pairs[fam].append((a, b))
+
+    def totals_ms(self):
+        return {f: sum(a.elapsed_time(b) for a, b in p) for f, p in self.pairs.items()}
+
+
+# ----------------------------------------------------------------------------
+def cpu_baseline(batch=2):
+    """The oracle on the same layer set at a small batch: one step of
+    forward, error back-propagation and weight gradient + update per distinct
+    layer shape (each once), plus the head and the loss."""
+    import numpy as np
+
+    import oracle
+    from paper_2009_13108_amd import inputs as I
+    from paper_2009_13108_amd import model as M
+
+    ops = 0
+    t0 = time.time()
+    for li, (name, cin, cout, k, st, pd, hw, count) in enumerate(M.RESNET18_LAYERS):
+        c = 3 if name.startswith("stem") else cin
+        d = oracle.conv_desc(batch, c, hw, hw, cout, k, k, st, pd)
+        P, Q = oracle.conv_out_hw(d)
+        x = I.activations(I.base_seed(4, 100 + li), (batch, c, hw, hw))
+        dy = I.errors8(I.base_seed(4, 200 + li), (batch, cout, P, Q))
+        w = I.weights(I.base_seed(4, 1000 + 10 * li), (cout, c, k, k))
+        macs = conv_macs(batch, c, hw, hw, cout, k, k, st, pd)
+        oracle.conv_fwd(d, x, w, relu=True)
+        ops += 2 * macs
+        if not name.startswith("stem"):
+            oracle.conv_bwd_data(d, dy, w, relu_src=x)
+            ops += 2 * macs
+        oracle.conv_bwd_weight(d, x, dy, w, mu=5)
+        ops += 2 * macs
+    fin, fout = M.RESNET18_FC
+    feat = I.activations(I.base_seed(4, 300), (batch, fin))
+    wfc = I.weights(I.base_seed(4, 301), (fout, fin))
+    lab = I.labels(I.base_seed(4, 302), batch, fout)
+    logits, _, _ = oracle.gemm_fwd(feat, wfc)
+    err, _, _ = oracle.int_ce_loss_grad(logits, -9, lab)
+    fd = oracle.conv_desc(batch, fin, 1, 1, fout, 1, 1, 1, 0)
+    oracle.conv_bwd_data(fd, err.reshape(batch, fout, 1, 1), wfc.reshape(fout, fin, 1, 1))
+    oracle.conv_bwd_weight(fd, feat.reshape(batch, fin, 1, 1), err.reshape(batch, fout, 1, 1),
+                           wfc.reshape(fout, fin, 1, 1))
+    ops += 3 * 2 * batch * fin * fout
+    dt = time.time() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": cores, "kind": "oracle",
+            "sample": "ResNet-18 layer set at 224x224, batch %d, each distinct layer shape once "
+                      "(fwd+bwd_data+bwd_weight/update) plus the 512->1000 head and loss; %.2f GOP in %.1f s"
+                      % (batch, ops / 1e9, dt)}
+
+
+# ----------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--batch", type=int, default=128)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-batch", type=int, default=8)
+    ap.add_argument("--layers", action="store_true", help="per-layer timing table on stderr")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the sharding notes in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    print("[bench] building inputs", file=sys.stderr, flush=True)
+    job = ResNetStep(batch=args.batch)
+    torch.cuda.synchronize()
+    print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        job.step()
+    torch.cuda.synchronize()
+    m0, c0 = job.misses()
+
+    # headline: K whole steps between two events
+    print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        job.step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    m1, c1 = job.misses()
+
+    # roofline: the same steps again with events around every contraction call
+    timer = EventTimer()
+    for _ in range(args.steps):
+        job.step(timer)
+    torch.cuda.synchronize()
+    tot = timer.totals_ms()
+    fam = max(tot, key=lambda f: tot[f])
+    per_call_ms = tot[fam] / (args.steps * job.fam_calls[fam])
+    ops_per_call = job.fam_ops[fam] / job.fam_calls[fam]
+    achieved = ops_per_call / (per_call_ms * 1e-3) / 1e12
+    value = job.ops_per_step / (ms * 1e-3) / 1e12
+
+    if args.layers:
+        report_layers(job)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle, batch %d)" % args.cpu_batch, file=sys.stderr, flush=True)
+        cpu = cpu_baseline(args.cpu_batch)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "resnet18_layers_224_b%d: 20 conv layers (7x7/2 stem, 3x3 at 56/28/14/7, "
+                               "1x1/2 downsample) + 512->1000 head; fwd+bwd_data+bwd_weight/update per layer, "
+                               "integer CE loss" % args.batch,
+                   "batch": args.batch, "image": 224, "mu": 5, "rounding": "pseudo-stochastic",
+                   "parallelism": "single GPU"},
+        "pct_of_int8_mfma_peak": round(100.0 * value / PEAK_INT8_TOPS, 2),
+        "ops_per_step": job.ops_per_step,
+        "hint": {"misses_timed": m1 - m0, "calls_timed": c1 - c0},
+        "roofline": {"bound": "mfma", "kernel": fam, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
+                     "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": None,
+                     "per_call_ms": round(per_call_ms, 5), "calls_per_step": job.fam_calls[fam],
+                     "family_ms_per_step": {f: round(v / args.steps, 4) for f, v in tot.items()}},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def report_layers(job, reps=5):
+    """Per-layer pass times (stderr), for the design notes."""
+    import torch
+    niti = job.niti
+    print("%-12s %10s %10s %10s %8s %8s %8s" % ("layer", "fwd_us", "dgrad_us", "wgrad_us", "fwdTOPS",
+                                                 "dgTOPS", "wgTOPS"), file=sys.stderr)
+    for L in job.layers:
+        d, w, s0 = L["desc"], L["w"][0], L["stats"]
+        calls = [lambda: niti.conv_fwd(d, L["x"], w, L["y"], job.stats, relu=True, stats_index=s0),
+                 (lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], job.stats, job.ws, relu_src=L["x"],
+                                             stats_index=s0 + 1)) if L["bwd_data"] else None,
+                 lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, job.stats, job.ws, mu=job.mu,
+                                              stats_index=s0 + 2)]
+        us = []
+        for fn in calls:
+            if fn is None:
+                us.append(float("nan"))
+                continue
+            fn()
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            us.append(a.elapsed_time(b) * 1e3 / reps)
+        tops = [2 * L["macs"] / (u * 1e-6) / 1e12 if u == u else float("nan") for u in us]
+        print("%-12s %10.1f %10.1f %10.1f %8.1f %8.1f %8.1f" % ((L["name"],) + tuple(us) + tuple(tops)),
+              file=sys.stderr, flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -74,20 +74,26 @@ typedef enum niti_round_mode {
 #define NITI_FLAG_LOSS_SA   4u  /* loss exponent below -22: the Taylor branch used s_a = -22 */
 #define NITI_FLAG_HINT_MISS 8u  /* the speculated binary point was wrong; the output was recomputed */
 
-/* Per-tensor statistics and working state, 64 bytes of device memory. */
+/* Per-tensor statistics and working state, 128 bytes of device memory.
+ * The "out" fields hold the result of the last call made with the block. */
 typedef struct niti_stats {
-    uint64_t acc_max;  /* working: running block maximum (zero between calls) */
-    uint32_t ticket;   /* working: completion counter (zero between calls)    */
-    uint32_t wflags;   /* working: flags raised by kernels (zero between calls) */
-    uint64_t max_abs;  /* out: largest magnitude over the whole result         */
-    int32_t b;         /* out: effective bitwidth of max_abs (Section 3.2)     */
-    int32_t bp;        /* out: binary point used, max(0, b - target)           */
-    int32_t flags;     /* out: NITI_FLAG_* of this call                        */
-    int32_t s_out;     /* out: output exponent formed by this call, if any     */
-    int32_t bp_hint;   /* in/out: binary point tried first by the next call    */
-    uint32_t calls;    /* out: calls made with this block                      */
-    uint32_t misses;   /* out: calls whose first try was wrong                 */
-    uint32_t reserved[3];
+    uint64_t max_abs;    /* out: largest magnitude over the whole result       */
+    int32_t b;           /* out: effective bitwidth of max_abs (Section 3.2)   */
+    int32_t bp;          /* out: binary point used, max(0, b - target)         */
+    int32_t flags;       /* out: NITI_FLAG_* of this call                      */
+    int32_t s_out;       /* out: output exponent formed by this call, if any   */
+    int32_t bp_hint;     /* in/out: binary point tried first by the next call  */
+    uint32_t calls;      /* out: calls made with this block                    */
+    uint32_t misses;     /* out: calls whose first try was wrong               */
+    uint32_t reserved0;
+    /* Library working state.  A call accumulates its block maximum and
+     * flags in slot (calls & 1) and clears the other slot for the next
+     * call, so no completion counter or extra launch is needed. */
+    uint64_t acc_max[2];
+    uint32_t wflags[2];
+    int32_t cur;         /* slot of the call in progress  */
+    int32_t hint_used;   /* guess the call in progress tried */
+    uint32_t reserved[14];
 } niti_stats;
 
 /* Convolution geometry.  Input x is NHWC [n][h][w][c]; filter is KRSC
@@ -211,7 +217,7 @@ niti_status niti_maxpool2_bwd(const int8_t *dy, const uint8_t *idx, int8_t *dx, 
 /* Backward ReLU on an int8 error: e[i] = 0 where a[i] <= 0, in place. */
 niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
 
-/* Size of niti_stats, for bindings. */
+/* Size of niti_stats (128), for bindings. */
 size_t niti_stats_bytes(void);
 
 #ifdef __cplusplus

@@ -29,55 +29,70 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     }
 }
 
+// Accumulating launch of a call: the tensor maximum of x.
 __global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) {
+    const int slot = call_slot(st);
+    begin_call(st, slot, -1);
     uint64_t m = 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         const uint64_t a = mag32(x[i]);
         m = a > m ? a : m;
     }
-    block_publish_max(st, m);
+    block_publish_max(st, slot, m);
 }
 
-// bp_fixed >= 0: that binary point.  bp_fixed < 0: the block binary point
-// from st->acc_max, then the statistics are finalized by the last group.
+// Sum of the per-split partial weight gradients (exact mod 2^32) into g32,
+// and the tensor maximum of the sum.  With one split the partial already is
+// g32 and only the maximum is taken.
+__global__ void reduce_max_kernel(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st) {
+    const int slot = call_slot(st);
+    begin_call(st, slot, -1);
+    uint64_t m = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        uint32_t v = (uint32_t)part[i];
+        for (int z = 1; z < splits; z++) v += (uint32_t)part[(int64_t)z * n + i];
+        if (splits > 1) g32[i] = (int32_t)v;
+        const uint64_t a = mag32((int32_t)v);
+        m = a > m ? a : m;
+    }
+    block_publish_max(st, slot, m);
+}
+
+// bp_fixed >= 0: that binary point.  bp_fixed < 0: the block binary point of
+// the call in progress; this is its finishing launch.
 __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_fixed, int target,
                                  int mode, niti_stats* st, ExpArgs ex) {
-    const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(load_acc_max(st), target);
+    const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(load_acc(st, st->cur & 1), target);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         y[i] = round_i32(x[i], rk);
     if (bp_fixed >= 0) {
         // Algorithm 2: s_q = s_q32 + bp, held to the int8 range.
-        if (ex.s_out && blockIdx.x == 0 && threadIdx.x == 0) {
+        if (ex.s_out && is_finisher()) {
             int s = (int)*ex.s_a + bp;
             *ex.s_out = (int8_t)(s > 127 ? 127 : (s < -128 ? -128 : s));
         }
         return;
     }
-    if (!st) return;
-    __syncthreads();
-    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
-        finalize_stats(st, target, ex, 0u, 0, 0);
+    if (is_finisher()) finish_call(st, target, ex, 0u, 0);
 }
 
-// Discrete update: g = round(g32, max(0, B(g32) - mu)); w <- clamp(w - g).
-__global__ void update_kernel(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu,
-                              int mode, niti_stats* st, uint32_t static_flags) {
-    const int bp = block_bp(load_acc_max(st), mu);
+// Discrete update, the finishing launch of its call:
+// g = round(g32, max(0, B(g32) - mu)); w <- clamp(w - g).
+__global__ void update_kernel(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode, niti_stats* st,
+                              uint32_t static_flags) {
+    const int bp = block_bp(load_acc(st, st->cur & 1), mu);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const int32_t g = g32[i];
-        if (g32_copy) g32_copy[i] = g;
-        int v = (int)w[i] - (int)round_i32(g, rk);
+        int v = (int)w[i] - (int)round_i32(g32[i], rk);
         v = v > 127 ? 127 : (v < -127 ? -127 : v);
         w[i] = (int8_t)v;
     }
-    __syncthreads();
-    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
-        finalize_stats(st, mu, ExpArgs{nullptr, nullptr, nullptr}, static_flags, 0, 0);
+    if (is_finisher()) finish_call(st, mu, ExpArgs{nullptr, nullptr, nullptr}, static_flags, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -95,6 +110,8 @@ __device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
 
 __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
                             int64_t* e64, int64_t batch, int64_t classes, niti_stats* st) {
+    const int slot = call_slot(st);
+    begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63;
     const int64_t sample = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
     int s_a = (int)*s_logits;
@@ -144,19 +161,17 @@ __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const 
         }
     }
     if (flag_sa && threadIdx.x == 0 && blockIdx.x == 0)
-        atomicOr(&st->wflags, NITI_FLAG_LOSS_SA);
-    block_publish_max(st, m);
+        atomicOr(&st->wflags[slot], NITI_FLAG_LOSS_SA);
+    block_publish_max(st, slot, m);
 }
 
 __global__ void loss_round_kernel(const int64_t* e64, int8_t* err, int64_t n, int mode, niti_stats* st) {
-    const int bp = block_bp(load_acc_max(st), 7);
+    const int bp = block_bp(load_acc(st, st->cur & 1), 7);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         err[i] = round_i64(e64[i], rk);
-    __syncthreads();
-    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
-        finalize_stats(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0, 0);
+    if (is_finisher()) finish_call(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -274,10 +289,16 @@ hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int tar
     return hipGetLastError();
 }
 
-hipError_t update_run(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu, int mode,
-                      niti_stats* st, uint32_t static_flags, hipStream_t s) {
-    hipLaunchKernelGGL(update_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, w, g32, g32_copy, n,
-                       mu, mode, st, static_flags);
+hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
+                          hipStream_t s) {
+    hipLaunchKernelGGL(reduce_max_kernel, dim3(grid_for(n, 4)), dim3(kThreads), 0, s, part, splits, g32, n, st);
+    return hipGetLastError();
+}
+
+hipError_t update_run(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode, niti_stats* st,
+                      uint32_t static_flags, hipStream_t s) {
+    hipLaunchKernelGGL(update_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, w, g32, n, mu, mode, st,
+                       static_flags);
     return hipGetLastError();
 }
 

@@ -18,9 +18,9 @@
 //
 // Exponent handling.  The rounding shift depends on the maximum over the
 // whole output tensor, which is known only when every tile is done.  The
-// first launch (PHASE_FIRST) computes every tile, folds its maximum into the
+// main launch computes every tile, folds its maximum into the
 // tensor maximum and writes the tile rounded with the shift the same stats
-// block reported last time.  The second launch (PHASE_FIXUP) derives the
+// block reported last time.  The fix-up launch derives the
 // true shift; when it matches, the output is already exact and the launch
 // only finalizes the statistics; otherwise it recomputes every tile with the
 // true shift.  Either way the result equals rounding the true accumulators
@@ -296,24 +296,33 @@ __device__ __forceinline__ void run_tile(const IgemmProblem& P, int tm, int tn, 
     }
 }
 
+// Main launch: every tile once, maximum folded in, output rounded with the
+// shift guessed from the previous call (no output when there is no guess).
 template <int TBM, int TBN>
-__global__ __launch_bounds__(NTHREADS) void igemm_kernel(IgemmBatch batch, IgemmCtl ctl) {
+__global__ __launch_bounds__(NTHREADS) void igemm_main(IgemmBatch batch, IgemmCtl ctl) {
     __shared__ Smem<TBM, TBN> sm;
     niti_stats* st = ctl.stats;
+    const int slot = call_slot(st);
     const int hint = st->bp_hint;
+    begin_call(st, slot, hint);
+    const Tile t = locate_tile(batch, blockIdx.x);
+    const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
+    uint64_t tmax = 0;
+    run_tile<TBM, TBN>(batch.p[t.prob], t.tm, t.tn, sm, rk, ctl.relu, hint >= 0, 1, tmax);
+    block_publish_max(st, slot, tmax);
+}
 
-    if (ctl.phase == kPhaseFirst) {
-        const Tile t = locate_tile(batch, blockIdx.x);
-        const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
-        uint64_t tmax = 0;
-        run_tile<TBM, TBN>(batch.p[t.prob], t.tm, t.tn, sm, rk, ctl.relu, hint >= 0, 1, tmax);
-        block_publish_max(st, tmax);
-        return;
-    }
-
-    // PHASE_FIXUP: every tile was computed once; acc_max is final.
-    const uint64_t mx = load_acc_max(st);
-    const int bp = block_bp(mx, ctl.target);
+// Fix-up launch: the tensor maximum is final.  If the guessed shift was
+// right there is nothing to redo; otherwise every tile is recomputed and
+// rounded with the true shift.  Workgroup 0 then records the statistics and
+// the output exponent.
+template <int TBM, int TBN>
+__global__ __launch_bounds__(NTHREADS) void igemm_fixup(IgemmBatch batch, IgemmCtl ctl) {
+    __shared__ Smem<TBM, TBN> sm;
+    niti_stats* st = ctl.stats;
+    const int cur = st->cur & 1;
+    const int hint = st->hint_used;
+    const int bp = block_bp(load_acc(st, cur), ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         for (int tt = blockIdx.x; tt < batch.total_tiles; tt += gridDim.x) {
@@ -323,9 +332,7 @@ __global__ __launch_bounds__(NTHREADS) void igemm_kernel(IgemmBatch batch, Igemm
             __syncthreads();
         }
     }
-    __syncthreads();
-    if (threadIdx.x == 0 && last_block_arrived(st, gridDim.x))
-        finalize_stats(st, ctl.target, ctl.ex, ctl.static_flags, 1, hint);
+    if (is_finisher()) finish_call(st, ctl.target, ctl.ex, ctl.static_flags, 1);
 }
 
 template <int TBM, int TBN>
@@ -339,13 +346,11 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         base += p.tiles_m * p.tiles_n;
     }
     b.total_tiles = base;
-    ctl.phase = kPhaseFirst;
-    hipLaunchKernelGGL((igemm_kernel<TBM, TBN>), dim3(base), dim3(NTHREADS), 0, stream, b, ctl);
+    hipLaunchKernelGGL((igemm_main<TBM, TBN>), dim3(base), dim3(NTHREADS), 0, stream, b, ctl);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    ctl.phase = kPhaseFixup;
     const int fix_grid = base < kFixupGrid ? base : kFixupGrid;
-    hipLaunchKernelGGL((igemm_kernel<TBM, TBN>), dim3(fix_grid), dim3(NTHREADS), 0, stream, b, ctl);
+    hipLaunchKernelGGL((igemm_fixup<TBM, TBN>), dim3(fix_grid), dim3(NTHREADS), 0, stream, b, ctl);
     return hipGetLastError();
 }
 

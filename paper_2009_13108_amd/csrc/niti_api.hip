@@ -77,8 +77,14 @@ size_t niti_workspace_bytes(int op, const niti_conv_desc* d, int64_t M, int64_t 
     switch (op) {
         case NITI_OP_CONV_BWD_DATA:
             return d ? (size_t)round_up(d->k * d->r * d->s * d->c, 256) : 0;
-        case NITI_OP_CONV_BWD_WEIGHT:
-            return d ? (size_t)round_up(d->k * d->r * d->s * d->c * 4, 256) : 0;
+        case NITI_OP_CONV_BWD_WEIGHT: {
+            if (!d) return 0;
+            int64_t P, Q;
+            if (check_conv(d, &P, &Q) != NITI_OK) return 0;
+            const int64_t nw = d->k * d->r * d->s * d->c;
+            const WgradPlan pl = wgrad_plan(d->k, d->r * d->s * d->c, d->n * P * Q);
+            return (size_t)(round_up(nw * 4, 256) + (pl.splits > 1 ? round_up((int64_t)pl.splits * nw * 4, 256) : 0));
+        }
         case NITI_OP_INT_CE_LOSS:
             return (M > 0 && N > 0) ? (size_t)round_up(M * N * 8, 256) : 0;
         default:
@@ -257,20 +263,20 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
     const int64_t nw = d->k * d->r * d->s * d->c;
-    int32_t* g32 = g32_out;
-    if (!g32) {
-        if (!ws || ws_bytes < (size_t)(nw * 4)) return NITI_ERR_WORKSPACE;
-        g32 = (int32_t*)ws;
-    }
     const int64_t npix = d->n * P * Q;
     if (too_big(npix)) return NITI_ERR_UNSUPPORTED;
+    const WgradPlan plan = wgrad_plan(d->k, d->r * d->s * d->c, npix);
+    const int64_t g_bytes = g32_out ? 0 : round_up(nw * 4, 256);
+    const int64_t p_bytes = plan.splits > 1 ? round_up((int64_t)plan.splits * nw * 4, 256) : 0;
+    if (too_big(p_bytes)) return NITI_ERR_UNSUPPORTED;
+    if (g_bytes + p_bytes > 0 && (!ws || ws_bytes < (size_t)(g_bytes + p_bytes))) return NITI_ERR_WORKSPACE;
+    int32_t* g32 = g32_out ? g32_out : (int32_t*)ws;
+    int32_t* part = plan.splits > 1 ? (int32_t*)((char*)ws + g_bytes) : g32;
     hipStream_t strm = as_stream(stream);
-    hipError_t e = fill_i32(g32, nw, 0, strm);
-    if (e != hipSuccess) return NITI_ERR_HIP;
     WgradProblem p{};
     p.x = x;
     p.dy = dy;
-    p.g32 = g32;
+    p.part = part;
     p.H = (int32_t)d->h;
     p.W = (int32_t)d->w;
     p.C = (int32_t)d->c;
@@ -290,11 +296,11 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     p.div_q = make_fastdiv((uint32_t)Q);
     p.div_l = make_fastdiv((uint32_t)p.L);
     p.div_c = make_fastdiv((uint32_t)p.C);
-    e = wgrad_run(p, strm);
+    hipError_t e = wgrad_run(p, plan, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
-    e = max_abs_i32(g32, nw, stats, strm);
+    e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
-    return hip_status(update_run(w, g32, nullptr, nw, mu, mode, stats, acc_flags(npix), strm));
+    return hip_status(update_run(w, g32, nw, mu, mode, stats, acc_flags(npix), strm));
 }
 
 niti_status niti_round_psr(const int32_t* x, int8_t* y, int64_t n, int bp, int target_bits,
@@ -339,7 +345,7 @@ niti_status niti_sgd_update(int8_t* w, const int32_t* g32, int64_t n, int mu, ni
     hipStream_t strm = as_stream(stream);
     hipError_t e = max_abs_i32(g32, n, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
-    return hip_status(update_run(w, g32, nullptr, n, mu, mode, stats, 0u, strm));
+    return hip_status(update_run(w, g32, n, mu, mode, stats, 0u, strm));
 }
 
 niti_status niti_quantize_u8(const uint8_t* px, int8_t* x, int64_t n, int64_t c, int64_t h, int64_t w,

@@ -150,19 +150,28 @@ __device__ __forceinline__ int64_t wave_max_i64(int64_t v) {
     return v;
 }
 
-__device__ __forceinline__ uint64_t load_acc_max(niti_stats* st) {
-    return __hip_atomic_load(&st->acc_max, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// ---------------------------------------------------------------------------
+// Statistics protocol.  A call made with a stats block runs an accumulating
+// launch (every workgroup folds its maximum into acc_max[slot], slot =
+// calls & 1) and later a finishing launch in which one thread derives b and
+// bp, records them, clears the other slot for the next call and counts the
+// call.  Each field is written only in a launch where no other workgroup
+// reads it, so no completion counter is needed.
+
+__device__ __forceinline__ int call_slot(const niti_stats* st) { return (int)(st->calls & 1u); }
+
+__device__ __forceinline__ uint64_t load_acc(niti_stats* st, int slot) {
+    return __hip_atomic_load(&st->acc_max[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Fold a block's maximum into the tensor maximum.  The tensor maximum only
-// grows, so a value not above one already observed can be skipped.
-__device__ __forceinline__ void publish_max(niti_stats* st, uint64_t m) {
-    if (m > load_acc_max(st)) atomicMax((unsigned long long*)&st->acc_max, (unsigned long long)m);
+// Fold a value into the tensor maximum.  The maximum only grows, so a value
+// not above one already observed can be skipped.
+__device__ __forceinline__ void publish_max(niti_stats* st, int slot, uint64_t m) {
+    if (m > load_acc(st, slot)) atomicMax((unsigned long long*)&st->acc_max[slot], (unsigned long long)m);
 }
 
-// Workgroup-wide maximum, folded into the tensor maximum by one thread.
-// Every thread of the block must call it.
-__device__ __forceinline__ void block_publish_max(niti_stats* st, uint64_t m) {
+// Workgroup-wide maximum folded in by one thread.  Every thread calls it.
+__device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint64_t m) {
     __shared__ uint64_t red[16];
     m = wave_max_u64(m);
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
@@ -172,7 +181,16 @@ __device__ __forceinline__ void block_publish_max(niti_stats* st, uint64_t m) {
         const int nw = (blockDim.x + kWave - 1) / kWave;
         uint64_t r = 0;
         for (int i = 0; i < nw; i++) r = red[i] > r ? red[i] : r;
-        if (r) publish_max(st, r);
+        if (r) publish_max(st, slot, r);
+    }
+}
+
+// In the accumulating launch: workgroup 0 records the slot and the guess
+// this call tries, for the finishing launch.
+__device__ __forceinline__ void begin_call(niti_stats* st, int slot, int hint) {
+    if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) {
+        st->cur = slot;
+        st->hint_used = hint;
     }
 }
 
@@ -183,17 +201,19 @@ struct ExpArgs {
     int8_t* s_out;      // output exponent (or NULL: not formed)
 };
 
-// Last step of a call: derive b and bp from the tensor maximum, form the
-// output exponent (Algorithm 2: s_q = s_q32 + bp), record the statistics,
-// make bp the next call's first guess, and leave the working fields zero.
-__device__ inline void finalize_stats(niti_stats* st, int target, ExpArgs ex, uint32_t static_flags,
-                                      int hinted, int hint) {
-    const uint64_t mx = __hip_atomic_load(&st->acc_max, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t wf = __hip_atomic_load(&st->wflags, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+// The finishing launch's single thread: derive b and bp from the tensor
+// maximum, form the output exponent (Algorithm 2: s_q = s_q32 + bp), record
+// the statistics, make bp the next call's first guess, clear the other
+// slot and count the call.
+__device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint32_t static_flags,
+                                   int hinted) {
+    const int cur = st->cur & 1;
+    const uint64_t mx = load_acc(st, cur);
+    const uint32_t wf = __hip_atomic_load(&st->wflags[cur], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int b = bitlen64(mx);
     const int bp = block_bp(mx, target);
     uint32_t fl = wf | static_flags;
-    if (hinted && bp != hint) {
+    if (hinted && bp != st->hint_used) {
         fl |= NITI_FLAG_HINT_MISS;
         st->misses += 1;
     }
@@ -210,18 +230,13 @@ __device__ inline void finalize_stats(niti_stats* st, int target, ExpArgs ex, ui
     st->flags = (int32_t)fl;
     st->s_out = s;
     st->bp_hint = bp;
+    st->acc_max[cur ^ 1] = 0;
+    st->wflags[cur ^ 1] = 0;
     st->calls += 1;
-    __hip_atomic_store(&st->acc_max, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&st->wflags, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&st->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Called once per workgroup by thread 0 after the group's work is issued;
-// returns true in exactly one workgroup, the last to arrive.
-__device__ __forceinline__ bool last_block_arrived(niti_stats* st, uint32_t nblocks) {
-    __threadfence();
-    const uint32_t t = __hip_atomic_fetch_add(&st->ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    return t == nblocks - 1;
+__device__ __forceinline__ bool is_finisher() {
+    return blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0;
 }
 
 }  // namespace niti

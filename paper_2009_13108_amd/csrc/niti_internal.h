@@ -7,9 +7,7 @@
 namespace niti {
 
 constexpr int kMaxProblems = 4;   // sub-pixel classes of a stride-2 back-propagation
-constexpr int kPhaseFirst = 0;
-constexpr int kPhaseFixup = 1;
-constexpr int kFixupGrid = 1024;  // workgroups of the fix-up launch
+constexpr int kFixupGrid = 512;   // workgroups of the fix-up launch
 
 // One implicit-GEMM problem (see igemm.hip for the index form).
 struct IgemmProblem {
@@ -41,18 +39,18 @@ struct IgemmCtl {
     int32_t target;
     int32_t relu;
     int32_t mode;
-    int32_t phase;
     uint32_t static_flags;
 };
 
 hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 
-// Weight-gradient contraction, split over the pixel reduction, accumulated
-// into g32 [K][R][S*C] with 32-bit atomic adds (exact mod 2^32).
+// Weight-gradient contraction.  The pixel reduction is split into `splits`
+// ranges; split z stores its partial sums to part + z*K*ncol (with one split
+// that is the final g32).
 struct WgradProblem {
     const int8_t* x;   // NHWC [img][H][W][C]
     const int8_t* dy;  // NHWC [img][P][Q][K]
-    int32_t* g32;      // [K][R*S*C], zero on entry
+    int32_t* part;     // [splits][K][R*S*C]
     int32_t H, W, C, K, R, S, P, Q;
     int32_t sh, sw, ph, pw;
     int32_t L, ncol;   // L = S*C, ncol = R*L
@@ -61,7 +59,14 @@ struct WgradProblem {
     FastDiv div_pq, div_q, div_l, div_c;
 };
 
-hipError_t wgrad_run(WgradProblem& p, hipStream_t stream);
+struct WgradPlan {
+    int32_t tbk;     // output-channel tile
+    int32_t splits;  // pixel ranges
+    int32_t chunk;   // pixels per range
+};
+
+WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix);
+hipError_t wgrad_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
 
 // Elementwise / reduction passes.
 hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
@@ -70,8 +75,10 @@ hipError_t max_abs_i32(const int32_t* x, int64_t n, niti_stats* st, hipStream_t 
 // from stats->acc_max (bp < 0), finalizing stats in the latter case.
 hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int target, int mode,
                          niti_stats* st, ExpArgs ex, hipStream_t s);
-hipError_t update_run(int8_t* w, const int32_t* g32, int32_t* g32_copy, int64_t n, int mu,
-                      int mode, niti_stats* st, uint32_t static_flags, hipStream_t s);
+hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
+                          hipStream_t s);
+hipError_t update_run(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode, niti_stats* st,
+                      uint32_t static_flags, hipStream_t s);
 hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
                     int8_t* err, int64_t* e64, int64_t batch, int64_t classes, int mode,
                     niti_stats* st, hipStream_t s);

@@ -5,10 +5,10 @@
 //                        dy[n][p][q][k] * x[n][p*sh - ph + r][q*sw - pw + s][c]
 //
 // The reduction runs over the N*P*Q output pixels, far longer than the
-// output, so the pixel range is split across workgroups and each group adds
-// its partial tile into g32 with 32-bit atomic adds.  Integer addition is
-// associative mod 2^32, so the result does not depend on the split or the
-// order of arrival.
+// output, so the pixel range may be split across workgroups: each group
+// stores its partial tile to its own slice, and a bandwidth pass sums the
+// slices (exact mod 2^32, independent of the split) while taking the
+// tensor maximum.
 //
 // Both operands arrive pixel-major from NHWC memory (channels contiguous)
 // while the MFMA wants each lane's 16 bytes along the reduction (pixels).
@@ -81,7 +81,6 @@ __global__ __launch_bounds__(NTHREADS) void wgrad_kernel(WgradProblem P) {
     const int k0 = blockIdx.y * TBK;
     const int pbeg = blockIdx.z * P.chunk;
     const int pend = min(P.npix, pbeg + P.chunk);
-    if (pbeg >= pend) return;
 
     // This thread's x column dword (fixed over the whole reduction).
     const int xcd = threadIdx.x % XCD, xg = threadIdx.x / XCD;
@@ -167,7 +166,7 @@ __global__ __launch_bounds__(NTHREADS) void wgrad_kernel(WgradProblem P) {
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[a][b][e] = 0;
 
-    const int nsteps = (pend - pbeg + BKP - 1) / BKP;
+    const int nsteps = pend > pbeg ? (pend - pbeg + BKP - 1) / BKP : 0;
     gload(pbeg);
     sstore(0);
     __syncthreads();
@@ -195,50 +194,62 @@ __global__ __launch_bounds__(NTHREADS) void wgrad_kernel(WgradProblem P) {
     }
 
     // acc[a][b] element 4*jj + i: column c0 + wc*WTC + a*32 + 8*jj + 4*(lane/32) + i,
-    // channel k0 + wk*WTK + b*32 + lane%32.
+    // channel k0 + wk*WTK + b*32 + lane%32: four consecutive columns per store.
+    int32_t* out = P.part + (int64_t)blockIdx.z * P.K * P.ncol;
 #pragma unroll
     for (int b = 0; b < FK; b++) {
         const int k = k0 + wk * WTK + b * 32 + (lane & 31);
         if (k >= P.K) continue;
-        int32_t* grow = P.g32 + (int64_t)k * P.ncol;
+        int32_t* grow = out + (int64_t)k * P.ncol;
 #pragma unroll
         for (int a = 0; a < FC; a++)
 #pragma unroll
-            for (int jj = 0; jj < 4; jj++)
-#pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    const int cidx = c0 + wc * WTC + a * 32 + 8 * jj + 4 * (lane >> 5) + i;
-                    const int32_t v = acc[a][b][4 * jj + i];
-                    if (cidx < P.ncol && v != 0)
-                        __hip_atomic_fetch_add(grow + cidx, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int jj = 0; jj < 4; jj++) {
+                const int cidx = c0 + wc * WTC + a * 32 + 8 * jj + 4 * (lane >> 5);
+                if (cidx >= P.ncol) continue;
+                int32_t* dst = grow + cidx;
+                if ((((uintptr_t)dst) & 15) == 0 && cidx + 4 <= P.ncol) {
+                    *(int4*)dst = make_int4(acc[a][b][4 * jj], acc[a][b][4 * jj + 1], acc[a][b][4 * jj + 2],
+                                            acc[a][b][4 * jj + 3]);
+                } else {
+                    for (int i = 0; i < 4 && cidx + i < P.ncol; i++) dst[i] = acc[a][b][4 * jj + i];
                 }
+            }
     }
 }
 
 template <int TBK, int TBC>
-hipError_t launch_wgrad(WgradProblem& p, hipStream_t stream) {
+hipError_t launch_wgrad(const WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {
     const int tc = (p.ncol + TBC - 1) / TBC;
     const int tk = (p.K + TBK - 1) / TBK;
-    const int tiles = tc * tk;
-    const int steps = (p.npix + BKP - 1) / BKP;
-    // Enough workgroups to fill the chip, but at least 8 steps per group so
-    // the atomic epilogue stays small next to the main loop.
-    int splits = (2048 + tiles - 1) / tiles;
-    int max_splits = (steps + 7) / 8;
-    if (splits > max_splits) splits = max_splits;
-    if (splits < 1) splits = 1;
-    int chunk_steps = (steps + splits - 1) / splits;
-    p.chunk = chunk_steps * BKP;
-    splits = (steps + chunk_steps - 1) / chunk_steps;
-    hipLaunchKernelGGL((wgrad_kernel<TBK, TBC>), dim3(tc, tk, splits), dim3(NTHREADS), 0, stream, p);
+    hipLaunchKernelGGL((wgrad_kernel<TBK, TBC>), dim3(tc, tk, plan.splits), dim3(NTHREADS), 0, stream, p);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t wgrad_run(WgradProblem& p, hipStream_t stream) {
-    if (p.K <= 64) return launch_wgrad<64, 128>(p, stream);
-    return launch_wgrad<128, 128>(p, stream);
+// Split of the pixel reduction: enough workgroups to give every compute
+// unit one tile, but at least 8 steps of 64 pixels per workgroup.
+WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix) {
+    WgradPlan pl;
+    pl.tbk = K <= 64 ? 64 : 128;
+    const int64_t tiles = ((K + pl.tbk - 1) / pl.tbk) * ((ncol + 127) / 128);
+    const int64_t steps = (npix + BKP - 1) / BKP;
+    int64_t splits = (256 + tiles - 1) / tiles;
+    const int64_t max_splits = steps / 8 > 1 ? steps / 8 : 1;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    const int64_t chunk_steps = (steps + splits - 1) / splits;
+    pl.chunk = (int32_t)(chunk_steps * BKP);
+    pl.splits = (int32_t)((steps + chunk_steps - 1) / chunk_steps);
+    if (pl.splits < 1) pl.splits = 1;
+    return pl;
+}
+
+hipError_t wgrad_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {
+    p.chunk = plan.chunk;
+    if (plan.tbk == 64) return launch_wgrad<64, 128>(p, plan, stream);
+    return launch_wgrad<128, 128>(p, plan, stream);
 }
 
 }  // namespace niti

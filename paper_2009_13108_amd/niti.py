@@ -31,11 +31,12 @@ OP_CONV_BWD_DATA = 2
 OP_CONV_BWD_WEIGHT = 3
 OP_INT_CE_LOSS = 4
 
-STATS_BYTES = 64
+STATS_BYTES = 128
 STATS_DTYPE = np.dtype([
-    ("acc_max", "<u8"), ("ticket", "<u4"), ("wflags", "<u4"), ("max_abs", "<u8"),
-    ("b", "<i4"), ("bp", "<i4"), ("flags", "<i4"), ("s_out", "<i4"), ("bp_hint", "<i4"),
-    ("calls", "<u4"), ("misses", "<u4"), ("reserved", "<u4", (3,)),
+    ("max_abs", "<u8"), ("b", "<i4"), ("bp", "<i4"), ("flags", "<i4"), ("s_out", "<i4"),
+    ("bp_hint", "<i4"), ("calls", "<u4"), ("misses", "<u4"), ("reserved0", "<u4"),
+    ("acc_max", "<u8", (2,)), ("wflags", "<u4", (2,)), ("cur", "<i4"), ("hint_used", "<i4"),
+    ("reserved", "<u4", (14,)),
 ])
 assert STATS_DTYPE.itemsize == STATS_BYTES
 
@@ -171,7 +172,7 @@ def _stats_ptr(stats, index=0):
 
 
 def new_stats(count: int = 1, device="cuda"):
-    """Zero-filled niti_stats blocks (count x 64 bytes of device memory)."""
+    """Zero-filled niti_stats blocks (count x 128 bytes of device memory)."""
     torch = _torch()
     return torch.zeros((count, STATS_BYTES), dtype=torch.uint8, device=device)
 
@@ -182,7 +183,8 @@ def read_stats(stats):
     recs = raw.view(STATS_DTYPE).reshape(-1)
     out = []
     for r in recs:
-        out.append({k: (int(r[k]) if k != "reserved" else None) for k in STATS_DTYPE.names})
+        out.append({k: (int(r[k]) if r[k].shape == () else [int(v) for v in r[k]])
+                    for k in STATS_DTYPE.names if not k.startswith("reserved")})
     return out
 
 

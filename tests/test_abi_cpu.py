@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_stats_layout_matches_header():
-    assert niti.lib().niti_stats_bytes() == 64 == niti.STATS_DTYPE.itemsize
+    assert niti.lib().niti_stats_bytes() == 128 == niti.STATS_DTYPE.itemsize
 
 
 def test_status_strings():
