@@ -146,6 +146,22 @@ class ResNetStep:
         st = self.niti.read_stats(self.stats)
         return sum(x["misses"] for x in st), sum(x["calls"] for x in st)
 
+    def miss_table(self):
+        """{layer/pass: misses} for stats blocks that missed at least once."""
+        st = self.niti.read_stats(self.stats)
+        out = {}
+        for L in self.layers:
+            for c in range(L["count"]):
+                for k, name in enumerate(("fwd", "bwd_data", "bwd_weight")):
+                    m = st[L["stats"] + 3 * c + k]["misses"]
+                    if m:
+                        out["%s#%d/%s" % (L["name"], c, name)] = m
+        for k, name in enumerate(("fwd", "loss", "bwd_data", "bwd_weight")):
+            m = st[self.fc_stats + k]["misses"]
+            if m:
+                out["fc/%s" % name] = m
+        return out
+
 
 class EventTimer:
     """HIP events around each call of a kernel family, on the stream the
@@ -295,7 +311,7 @@ def main():
                    "parallelism": "single GPU"},
         "pct_of_int8_mfma_peak": round(100.0 * value / PEAK_INT8_TOPS, 2),
         "ops_per_step": job.ops_per_step,
-        "hint": {"misses_timed": m1 - m0, "calls_timed": c1 - c0},
+        "hint": {"misses_timed": m1 - m0, "calls_timed": c1 - c0, "misses_by_call": job.miss_table()},
         "roofline": {"bound": "mfma", "kernel": fam, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                      "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": None,
                      "per_call_ms": round(per_call_ms, 5), "calls_per_step": job.fam_calls[fam],

@@ -44,18 +44,32 @@ __global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) 
 
 // Sum of the per-split partial weight gradients (exact mod 2^32) into g32,
 // and the tensor maximum of the sum.  With one split the partial already is
-// g32 and only the maximum is taken.
-__global__ void reduce_max_kernel(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st) {
+// g32 and only the maximum is taken.  A workgroup covers 64 consecutive
+// elements; its four waves take interleaved quarters of the splits (each
+// wave reads 256 contiguous bytes per split) and add their sums in LDS.
+__global__ __launch_bounds__(256) void reduce_max_kernel(const int32_t* part, int splits, int32_t* g32,
+                                                         int64_t n, niti_stats* st) {
+    __shared__ uint32_t sum4[4][64];
     const int slot = call_slot(st);
     begin_call(st, slot, -1);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * 64 + lane;
+    uint32_t v0 = 0, v1 = 0;
+    if (i < n) {
+        int z = wv;
+        for (; z + 4 < splits; z += 8) {
+            v0 += (uint32_t)part[(int64_t)z * n + i];
+            v1 += (uint32_t)part[(int64_t)(z + 4) * n + i];
+        }
+        if (z < splits) v0 += (uint32_t)part[(int64_t)z * n + i];
+    }
+    sum4[wv][lane] = v0 + v1;
+    __syncthreads();
     uint64_t m = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        uint32_t v = (uint32_t)part[i];
-        for (int z = 1; z < splits; z++) v += (uint32_t)part[(int64_t)z * n + i];
+    if (wv == 0 && i < n) {
+        const uint32_t v = sum4[0][lane] + sum4[1][lane] + sum4[2][lane] + sum4[3][lane];
         if (splits > 1) g32[i] = (int32_t)v;
-        const uint64_t a = mag32((int32_t)v);
-        m = a > m ? a : m;
+        m = mag32((int32_t)v);
     }
     block_publish_max(st, slot, m);
 }
@@ -291,7 +305,9 @@ hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int tar
 
 hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
                           hipStream_t s) {
-    hipLaunchKernelGGL(reduce_max_kernel, dim3(grid_for(n, 4)), dim3(kThreads), 0, s, part, splits, g32, n, st);
+    const int64_t blocks = (n + 63) / 64;
+    hipLaunchKernelGGL(reduce_max_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(256), 0, s, part, splits,
+                       g32, n, st);
     return hipGetLastError();
 }
 
