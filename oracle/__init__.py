@@ -173,6 +173,25 @@ def gemm_nt_raw(A, B):
     return S
 
 
+def gemm_nt_exact(A, B, block_rows=2048):
+    """Exact S = A @ B.T for large int8 matrices through a float64 matmul.
+
+    Every product is an integer of magnitude <= 127^2 and every partial sum
+    an integer of magnitude <= K * 127^2 < 2^53, so float64 arithmetic (with
+    or without fused multiply-add, in any summation order) is exact.  Rows
+    are processed in blocks to bound memory."""
+    A = np.ascontiguousarray(A, dtype=np.int8)
+    B = np.ascontiguousarray(B, dtype=np.int8)
+    M, K = A.shape
+    N, K2 = B.shape
+    assert K == K2 and K * 127 * 127 < 2 ** 53
+    Bf = B.astype(np.float64).T.copy()
+    S = np.empty((M, N), np.int64)
+    for r in range(0, M, block_rows):
+        S[r:r + block_rows] = (A[r:r + block_rows].astype(np.float64) @ Bf).astype(np.int64)
+    return S
+
+
 def gemm_nt_pick(A, B, rows, cols):
     """Exact sums S[rows[i], cols[i]] only."""
     A, pa = _c(A, np.int8)

@@ -357,6 +357,7 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
 }  // namespace
 
 hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    if (igemm_dma_eligible(b)) return igemm_dma_run(b, ctl, stream);
     // All problems of a batch share the tile shape; pick it from the largest.
     int maxM = 0, maxN = 0;
     for (int i = 0; i < b.nprob; i++) {

@@ -1,0 +1,385 @@
+// Implicit-GEMM int8 MFMA kernel with a multi-stage LDS ring filled by
+// direct-to-LDS buffer loads (gfx950 buffer_load_dwordx4 ... lds).  Same
+// problem form, epilogue and exponent speculation as igemm.hip, which keeps
+// the general path (odd channel counts such as a 4-channel image layer).
+//
+// Two load modes keep the per-step address work uniform:
+//   kGemm   plain matrix rows (H = W = 1, one tap): a lane's offset is fixed
+//           and the K step adds a uniform amount;
+//   kConv64 convolutions with C % 64 == 0: every 64-byte K step lies in one
+//           filter tap (r, s) and channel block c0, all uniform, so a lane
+//           only checks that its pixel's tap is inside the image.
+//
+// Loads.  Each wave instruction moves 64 lanes x 16 bytes into one 1 KiB LDS
+// block (lane l lands at block + 16 l); a block holds 16 operand rows of one
+// 64-byte K step.  A lane whose piece is outside the image, past the tensor
+// or past K uses an offset beyond the buffer's size, which the hardware
+// answers with zeros.  Within a row the four 16-byte chunks are stored
+// XOR-swizzled (position = chunk ^ f(row)) so the 32x32x32 MFMA fragment
+// reads (16 bytes per lane, 8 lanes per bank cycle) hit distinct banks.
+//
+// Pipeline.  NS stages; stage k+NS-1 is issued while stage k is computed.
+// Loads past the last K step are issued anyway (as zeros), so the wait
+// count before each step is a constant.
+#include "niti_internal.h"
+
+namespace niti {
+
+namespace {
+
+constexpr int KSTEP = 64;  // K bytes per stage
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kGemm = 0;
+constexpr int kConv64 = 1;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <int BM, int BN, int NS, int WGM, int WGN>
+struct Cfg {
+    static constexpr int NWAVES = WGM * WGN;
+    static constexpr int NT = 64 * NWAVES;
+    static constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile: pixels x channels
+    static constexpr int FM = WTM / 32, FN = WTN / 32;
+    static constexpr int BLOCKS = (BM + BN) / 16;           // 1 KiB blocks per stage
+    static constexpr int IPW = BLOCKS / NWAVES;             // load instructions per wave per stage
+    static constexpr int ABLK = BN / 16;                    // blocks holding weight rows
+    static constexpr int STAGE_BYTES = (BM + BN) * KSTEP;
+    static constexpr int LDS_BYTES = NS * STAGE_BYTES;
+    static_assert(BLOCKS % NWAVES == 0, "blocks per wave");
+};
+
+template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
+__device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, int8_t* lds, const RoundK& rk,
+                                         int relu, int do_store, int do_max, uint64_t& tmax) {
+    using T = Cfg<BM, BN, NS, WGM, WGN>;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave % WGM, wn = wave / WGM;
+
+    const __amdgpu_buffer_rsrc_t act_rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.act, 0, (int)P.act_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t wgt_rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.wgt, 0, (int)P.wgt_bytes, 0x00020000);
+
+    // Per-lane row state for each load instruction.
+    const int lrow = lane >> 2;
+    const uint32_t kpo = (uint32_t)(((lane & 3) ^ swz(lrow)) << 4);  // byte offset of this lane's chunk
+    uint32_t base[T::IPW];
+    int ih0[T::IPW], iw0[T::IPW];
+#pragma unroll
+    for (int i = 0; i < T::IPW; i++) {
+        const int blk = wave * T::IPW + i;   // uniform
+        if (blk < T::ABLK) {
+            const int n = tn * BN + blk * 16 + lrow;
+            base[i] = n < P.Nout ? (uint32_t)n * (uint32_t)P.Ktot + kpo : kOOB;
+            ih0[i] = 0;
+            iw0[i] = 0;
+        } else {
+            const int m = tm * BM + (blk - T::ABLK) * 16 + lrow;
+            if (MODE == kGemm) {
+                base[i] = m < P.M ? (uint32_t)m * (uint32_t)P.C + kpo : kOOB;
+                ih0[i] = 0;
+                iw0[i] = 0;
+            } else {
+                const bool ok = m < P.M;
+                const uint32_t mm = ok ? (uint32_t)m : 0u;
+                const uint32_t img = fdiv(mm, P.div_ohw);
+                const uint32_t rem = mm - img * (uint32_t)(P.OHc * P.OWc);
+                const uint32_t oh = fdiv(rem, P.div_ow);
+                const uint32_t ow = rem - oh * (uint32_t)P.OWc;
+                const int h0 = (int)oh * P.st + P.off_h;
+                const int w0 = (int)ow * P.st + P.off_w;
+                // an invalid row is pushed out of the image so every tap fails the check
+                ih0[i] = ok ? h0 : -(1 << 28);
+                iw0[i] = w0;
+                base[i] = (uint32_t)((int64_t)img * P.H * P.W * P.C + ((int64_t)h0 * P.W + w0) * P.C) + kpo;
+            }
+        }
+    }
+
+    const int nk = (P.Ktot + KSTEP - 1) / KSTEP;
+    // Uniform position of the next stage to issue: K offset, tap (r, s), channel block.
+    int next_kt = 0, tr = 0, ts = 0, tc = 0;
+
+    auto issue = [&]() {
+        int8_t* st = lds + (next_kt % NS) * T::STAGE_BYTES;
+        const uint32_t kb = (uint32_t)next_kt * KSTEP;
+        const bool kin = next_kt < nk;
+        const uint32_t tap_off = MODE == kConv64 ? (uint32_t)((tr * P.W + ts) * P.C + tc) : kb;
+#pragma unroll
+        for (int i = 0; i < T::IPW; i++) {
+            const int blk = wave * T::IPW + i;   // uniform
+            uint32_t off;
+            if (blk < T::ABLK) {
+                off = (base[i] != kOOB && kb + kpo < (uint32_t)P.Ktot) ? base[i] + kb : kOOB;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
+            } else {
+                if (MODE == kGemm) {
+                    off = (base[i] != kOOB && kb + kpo < (uint32_t)P.Ktot) ? base[i] + kb : kOOB;
+                } else {
+                    const bool ok = kin && (unsigned)(ih0[i] + tr) < (unsigned)P.H &&
+                                    (unsigned)(iw0[i] + ts) < (unsigned)P.W;
+                    off = ok ? base[i] + tap_off : kOOB;
+                }
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
+            }
+        }
+        next_kt++;
+        if (MODE == kConv64) {
+            tc += KSTEP;
+            if (tc == P.C) {
+                tc = 0;
+                if (++ts == P.S) {
+                    ts = 0;
+                    ++tr;
+                }
+            }
+        }
+    };
+
+    v16i acc[T::FN][T::FM];
+#pragma unroll
+    for (int a = 0; a < T::FN; a++)
+#pragma unroll
+        for (int b = 0; b < T::FM; b++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[a][b][e] = 0;
+
+    int a_off[T::FN], b_off[T::FM], a_sw[T::FN], b_sw[T::FM];
+#pragma unroll
+    for (int a = 0; a < T::FN; a++) {
+        const int row = wn * T::WTN + a * 32 + (lane & 31);
+        a_off[a] = row * KSTEP;
+        a_sw[a] = swz(row & 15);
+    }
+#pragma unroll
+    for (int b = 0; b < T::FM; b++) {
+        const int row = wm * T::WTM + b * 32 + (lane & 31);
+        b_off[b] = BN * KSTEP + row * KSTEP;
+        b_sw[b] = swz(row & 15);
+    }
+
+#pragma unroll
+    for (int s = 0; s < NS - 1; s++) issue();
+
+    for (int kt = 0; kt < nk; kt++) {
+        wait_vm<(NS - 2) * T::IPW>();
+        __builtin_amdgcn_s_barrier();
+        issue();
+        const int8_t* st = lds + (kt % NS) * T::STAGE_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < 2; ks++) {
+            const int kp = (lane >> 5) + 2 * ks;
+            v4i fa[T::FN], fb[T::FM];
+#pragma unroll
+            for (int a = 0; a < T::FN; a++) fa[a] = *(const v4i*)(st + a_off[a] + ((kp ^ a_sw[a]) << 4));
+#pragma unroll
+            for (int b = 0; b < T::FM; b++) fb[b] = *(const v4i*)(st + b_off[b] + ((kp ^ b_sw[b]) << 4));
+#pragma unroll
+            for (int a = 0; a < T::FN; a++)
+#pragma unroll
+                for (int b = 0; b < T::FM; b++)
+                    acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+        }
+    }
+    // Drain the loads issued past the end before the ring is reused.
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+
+    // Epilogue: acc[a][b] element 4*jj + i is channel
+    // tile_n + wn*WTN + a*32 + 8*jj + 4*(lane/32) + i of pixel tile_m + wm*WTM + b*32 + lane%32.
+#pragma unroll
+    for (int b = 0; b < T::FM; b++) {
+        const int m = tm * BM + wm * T::WTM + b * 32 + (lane & 31);
+        const bool mvalid = m < P.M;
+        int64_t ooff = 0;
+        if (mvalid) {
+            const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
+            const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
+            const uint32_t i0 = fdiv(rem, P.div_ow);
+            const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
+            const int oh = (int)i0 * P.os + P.oa;
+            const int ow = (int)j0 * P.os + P.ob;
+            ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
+        }
+#pragma unroll
+        for (int a = 0; a < T::FN; a++) {
+#pragma unroll
+            for (int jj = 0; jj < 4; jj++) {
+                const int n0 = tn * BN + wn * T::WTN + a * 32 + 8 * jj + 4 * (lane >> 5);
+                if (!mvalid || n0 >= P.Nout) continue;
+                const int nv = min(4, P.Nout - n0);
+                int32_t v[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int32_t x = acc[a][b][4 * jj + i];
+                    v[i] = (relu && x < 0) ? 0 : x;
+                }
+                if (do_max) {
+#pragma unroll
+                    for (int i = 0; i < 4; i++)
+                        if (i < nv) {
+                            const uint64_t mg = mag32(v[i]);
+                            tmax = mg > tmax ? mg : tmax;
+                        }
+                }
+                if (do_store) {
+                    uint32_t packed = 0;
+#pragma unroll
+                    for (int i = 0; i < 4; i++) packed |= (uint32_t)(uint8_t)round_i32(v[i], rk) << (8 * i);
+                    int8_t* dst = P.out + ooff + n0;
+                    if (P.mask) {
+                        const int8_t* ms = P.mask + ooff + n0;
+#pragma unroll
+                        for (int i = 0; i < 4; i++)
+                            if (i < nv && ms[i] <= 0) packed &= ~(0xFFu << (8 * i));
+                    }
+                    if (nv == 4 && ((((uintptr_t)dst) & 3) == 0)) {
+                        *(uint32_t*)dst = packed;
+                    } else {
+                        for (int i = 0; i < nv; i++) dst[i] = (int8_t)(packed >> (8 * i));
+                    }
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void locate(const IgemmBatch& b, int t, int& prob, int& tm, int& tn) {
+    int p = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxProblems; i++)
+        if (i < b.nprob && t >= b.p[i].tile_base) p = i;
+    const int local = t - b.p[p].tile_base;
+    prob = p;
+    tm = local / b.p[p].tiles_n;
+    tn = local - tm * b.p[p].tiles_n;
+}
+
+template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_main(IgemmBatch batch, IgemmCtl ctl) {
+    extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
+    niti_stats* st = ctl.stats;
+    const int slot = call_slot(st);
+    const int hint = st->bp_hint;
+    begin_call(st, slot, hint);
+    int prob, tm, tn;
+    locate(batch, blockIdx.x, prob, tm, tn);
+    const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
+    uint64_t tmax = 0;
+    dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, hint >= 0, 1, tmax);
+    block_publish_max(st, slot, tmax);
+}
+
+template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_fixup(IgemmBatch batch, IgemmCtl ctl) {
+    extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
+    niti_stats* st = ctl.stats;
+    const int cur = st->cur & 1;
+    const int hint = st->hint_used;
+    const int bp = block_bp(load_acc(st, cur), ctl.target);
+    if (bp != hint) {
+        const RoundK rk = make_round(bp, ctl.mode);
+        for (int t = blockIdx.x; t < batch.total_tiles; t += gridDim.x) {
+            int prob, tm, tn;
+            locate(batch, t, prob, tm, tn);
+            uint64_t dummy = 0;
+            dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, 1, 0, dummy);
+        }
+    }
+    if (is_finisher()) finish_call(st, ctl.target, ctl.ex, ctl.static_flags, 1);
+}
+
+template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
+hipError_t launch_dma(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    using T = Cfg<BM, BN, NS, WGM, WGN>;
+    static bool attr_done = false;
+    if (!attr_done) {
+        hipError_t e = hipFuncSetAttribute((const void*)igemm_dma_main<BM, BN, NS, WGM, WGN, MODE>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS_BYTES);
+        if (e != hipSuccess) return e;
+        e = hipFuncSetAttribute((const void*)igemm_dma_fixup<BM, BN, NS, WGM, WGN, MODE>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, T::LDS_BYTES);
+        if (e != hipSuccess) return e;
+        attr_done = true;
+    }
+    int base = 0;
+    for (int i = 0; i < b.nprob; i++) {
+        IgemmProblem& p = b.p[i];
+        p.tiles_m = (p.M + BM - 1) / BM;
+        p.tiles_n = (p.Nout + BN - 1) / BN;
+        p.tile_base = base;
+        base += p.tiles_m * p.tiles_n;
+    }
+    b.total_tiles = base;
+    hipLaunchKernelGGL((igemm_dma_main<BM, BN, NS, WGM, WGN, MODE>), dim3(base), dim3(T::NT), T::LDS_BYTES, stream,
+                       b, ctl);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int fix_grid = base < kFixupGrid ? base : kFixupGrid;
+    hipLaunchKernelGGL((igemm_dma_fixup<BM, BN, NS, WGM, WGN, MODE>), dim3(fix_grid), dim3(T::NT), T::LDS_BYTES,
+                       stream, b, ctl);
+    return hipGetLastError();
+}
+
+int problem_mode(const IgemmProblem& p) {
+    if (p.H == 1 && p.W == 1 && p.R == 1 && p.off_h == 0 && p.off_w == 0 && p.L == p.C) return kGemm;
+    return kConv64;
+}
+
+template <int MODE>
+hipError_t run_mode(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    int64_t work = 0;
+    int maxN = 0;
+    for (int i = 0; i < b.nprob; i++) {
+        work += (int64_t)b.p[i].M * b.p[i].Nout;
+        maxN = b.p[i].Nout > maxN ? b.p[i].Nout : maxN;
+    }
+    // The largest tile that still gives most compute units a workgroup.
+    if (maxN <= 64) return launch_dma<256, 64, 4, 4, 1, MODE>(b, ctl, stream);
+    if (maxN <= 128) {
+        if (work >= (int64_t)200 * 256 * 128) return launch_dma<256, 128, 4, 2, 2, MODE>(b, ctl, stream);
+        return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
+    }
+    if (work >= (int64_t)200 * 256 * 256) return launch_dma<256, 256, 3, 2, 4, MODE>(b, ctl, stream);
+    if (work >= (int64_t)200 * 256 * 128) return launch_dma<256, 128, 4, 2, 2, MODE>(b, ctl, stream);
+    return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
+}
+
+}  // namespace
+
+// True when every problem has whole 16-byte pieces handled by one of the two
+// load modes and both operands are addressable with 32-bit buffer offsets.
+bool igemm_dma_eligible(const IgemmBatch& b) {
+    int mode = -1;
+    for (int i = 0; i < b.nprob; i++) {
+        const IgemmProblem& p = b.p[i];
+        if (p.act_bytes <= 0 || p.act_bytes >= ((int64_t)1 << 31) || p.wgt_bytes <= 0 ||
+            p.wgt_bytes >= ((int64_t)1 << 31))
+            return false;
+        const int m = problem_mode(p);
+        if (mode >= 0 && m != mode) return false;
+        mode = m;
+        if (m == kGemm) {
+            if (p.C % 16 != 0 || p.Ktot != p.C) return false;
+        } else {
+            if (p.C % KSTEP != 0 || p.L != p.S * p.C || p.Lpad != p.L || p.Ktot != p.R * p.L) return false;
+        }
+    }
+    return true;
+}
+
+hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    if (problem_mode(b.p[0]) == kGemm) return run_mode<kGemm>(b, ctl, stream);
+    return run_mode<kConv64>(b, ctl, stream);
+}
+
+}  // namespace niti

@@ -112,6 +112,7 @@ niti_status niti_gemm_fwd(const int8_t* A, const int8_t* B, int8_t* C, int64_t M
     p.mask = nullptr;
     p.Nout = (int32_t)N;
     p.R = 1;
+    p.S = 1;
     p.L = (int32_t)K;
     p.Lpad = (int32_t)round_up(K, 16);
     p.Ktot = p.Lpad;
@@ -128,6 +129,8 @@ niti_status niti_gemm_fwd(const int8_t* A, const int8_t* B, int8_t* C, int64_t M
     p.os = 1;
     p.oa = 0;
     p.ob = 0;
+    p.act_bytes = M * K;
+    p.wgt_bytes = N * K;
     IgemmCtl ctl{};
     ctl.stats = stats;
     ctl.ex = ExpArgs{s_a, s_b, s_c};
@@ -158,6 +161,7 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
     p.mask = nullptr;
     p.Nout = (int32_t)d->k;
     p.R = (int32_t)d->r;
+    p.S = (int32_t)d->s;
     p.L = (int32_t)(d->s * d->c);
     p.Lpad = (int32_t)round_up(p.L, 16);
     p.Ktot = p.R * p.Lpad;
@@ -174,6 +178,8 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
     p.os = 1;
     p.oa = 0;
     p.ob = 0;
+    p.act_bytes = d->n * d->h * d->w * d->c;
+    p.wgt_bytes = d->k * d->r * d->s * d->c;
     IgemmCtl ctl{};
     ctl.stats = stats;
     ctl.ex = ExpArgs{s_x, s_w, s_y};
@@ -223,6 +229,7 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
             p.mask = relu_src;
             p.Nout = C;
             p.R = c.T;
+            p.S = c.U;
             p.L = c.U * K;
             p.Lpad = (int32_t)round_up(p.L, 16);
             p.Ktot = p.R * p.Lpad;
@@ -239,6 +246,8 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
             p.os = st;
             p.oa = a;
             p.ob = bb;
+            p.act_bytes = d->n * P * Q * d->k;
+            p.wgt_bytes = (int64_t)C * c.T * c.U * K;
         }
     }
     hipError_t e = repack_dgrad_run(w, (int8_t*)ws, cls, ncls, K, R, S, C, st, st, as_stream(stream));
@@ -296,7 +305,9 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     p.div_q = make_fastdiv((uint32_t)Q);
     p.div_l = make_fastdiv((uint32_t)p.L);
     p.div_c = make_fastdiv((uint32_t)p.C);
-    hipError_t e = wgrad_run(p, plan, strm);
+    p.x_bytes = d->n * d->h * d->w * d->c;
+    p.dy_bytes = npix * d->k;
+    hipError_t e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;

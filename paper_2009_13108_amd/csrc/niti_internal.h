@@ -17,7 +17,7 @@ struct IgemmProblem {
     const int8_t* mask;  // backward ReLU source, addressed like out (or NULL)
     int32_t M;           // output pixels of this problem: img * OHc * OWc
     int32_t Nout;        // output channels
-    int32_t R, L, Lpad, Ktot;
+    int32_t R, S, L, Lpad, Ktot;  // taps: R rows of S pixels; L = S*C bytes per tap row
     int32_t H, W, C;     // activation geometry
     int32_t OHc, OWc;    // this problem's output grid
     int32_t st, off_h, off_w;  // input row = out row * st + off (+ tap)
@@ -25,6 +25,8 @@ struct IgemmProblem {
     int32_t os, oa, ob;        // out row = grid row * os + oa (cols: ob)
     int32_t tiles_m, tiles_n, tile_base;
     FastDiv div_ohw, div_ow;
+    int64_t act_bytes;   // extent of act (bytes), for buffer bounds
+    int64_t wgt_bytes;   // extent of wgt (bytes)
 };
 
 struct IgemmBatch {
@@ -43,6 +45,8 @@ struct IgemmCtl {
 };
 
 hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
+bool igemm_dma_eligible(const IgemmBatch& b);
+hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 
 // Weight-gradient contraction.  The pixel reduction is split into `splits`
 // ranges; split z stores its partial sums to part + z*K*ncol (with one split
@@ -57,6 +61,7 @@ struct WgradProblem {
     int32_t npix;      // img*P*Q
     int32_t chunk;     // pixels per split (multiple of 64)
     FastDiv div_pq, div_q, div_l, div_c;
+    int64_t x_bytes, dy_bytes;  // extents, for buffer bounds
 };
 
 struct WgradPlan {
@@ -67,6 +72,8 @@ struct WgradPlan {
 
 WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix);
 hipError_t wgrad_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
+bool wgrad_dma_eligible(const WgradProblem& p);
+hipError_t wgrad_dma_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
 
 // Elementwise / reduction passes.
 hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

@@ -40,6 +40,10 @@ GEMM_CASES = [
     (64, 10, 128, False, oracle.PSR, "w"),
     (129, 300, 0, False, oracle.PSR, "w"),
     (513, 257, 333, True, oracle.PSR, "e5"),
+    (3000, 64, 128, False, oracle.PSR, "w"),      # 256x64 tiles
+    (70001, 100, 64, True, oracle.PSR, "w"),      # 256x128 tiles, ragged M
+    (4100, 4096, 272, False, oracle.PSR, "w"),    # 256x256 tiles, ragged M and K
+    (2000, 300, 512, False, oracle.RTN, "e5"),    # 128x128 tiles
 ]
 
 

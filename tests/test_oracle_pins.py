@@ -163,6 +163,15 @@ def test_gemm_matches_numpy_matmul():
         assert (oracle.gemm_nt_pick(A, B, rows, cols) == S[rows, cols]).all()
 
 
+def test_gemm_exact_large_route_matches_int64_loops():
+    # the float64 route used for the large GEMM digests equals the int64 loops
+    for (M, N, K) in [(300, 257, 4096), (64, 3000, 16384), (1, 1, 16384)]:
+        A = I.weights(M + K, (M, K)); B = I.weights(N + 2 * K, (N, K))
+        assert (oracle.gemm_nt_exact(A, B, block_rows=100) == oracle.gemm_nt_raw(A, B)).all()
+    A = np.full((2, 16384), -127, np.int8)
+    assert (oracle.gemm_nt_exact(A, A) == 16384 * 127 * 127).all()
+
+
 def test_gemm_all_ones_and_overflow_flag():
     K = 140000                          # 140000 * 127^2 > 2^31
     A = np.full((1, K), 127, np.int8)
