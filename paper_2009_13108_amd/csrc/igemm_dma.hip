@@ -53,8 +53,119 @@ struct Cfg {
     static constexpr int ABLK = BN / 16;                    // blocks holding weight rows
     static constexpr int STAGE_BYTES = (BM + BN) * KSTEP;
     static constexpr int LDS_BYTES = NS * STAGE_BYTES;
+    static constexpr int WGM_ = WGM, BN_ = BN;
     static_assert(BLOCKS % NWAVES == 0, "blocks per wave");
+    static_assert(BM * (BN + 16) <= LDS_BYTES, "output tile fits in the ring");
 };
+
+// Round one accumulator (Algorithm 3, or nearest) with the tile's uniform
+// shift; RELU: v is already non-negative.  Returns the int8 in the low byte.
+template <bool RELU, bool RTN>
+__device__ __forceinline__ uint32_t round_acc(int32_t v, const RoundK& k, uint64_t& tmax) {
+    const uint32_t x = RELU ? (uint32_t)v : (v < 0 ? 0u - (uint32_t)v : (uint32_t)v);
+    tmax = (uint64_t)x > tmax ? (uint64_t)x : tmax;
+    uint32_t q = x >> k.bp;
+    uint32_t up;
+    if (RTN) {
+        up = k.bp ? __builtin_amdgcn_ubfe(x, k.bp - 1, 1) : 0u;
+    } else {
+        const uint32_t thi = __builtin_amdgcn_ubfe(x, k.odd + k.h, k.h);
+        const uint32_t rlo = __builtin_amdgcn_ubfe(x, k.odd, k.h);
+        up = thi > rlo ? 1u : 0u;
+    }
+    q = min(q + up, 127u);
+    if (RELU) return q;
+    const uint32_t sgn = (uint32_t)(v >> 31);
+    return ((q ^ sgn) - sgn) & 0xFFu;
+}
+
+// Tile maximum and rounded bytes of the register accumulators; the bytes go
+// to an LDS tile [BM][BN + 16] (row = tile pixel).
+template <typename T, bool RELU, bool RTN>
+__device__ __forceinline__ void epilogue_regs(v16i (&acc)[T::FN][T::FM], int8_t* lds, const RoundK& rk,
+                                              int do_store, int do_max, uint64_t& tmax) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave % T::WGM_, wn = wave / T::WGM_;
+    constexpr int PITCH = T::BN_ + 16;
+    uint64_t mx = 0;
+#pragma unroll
+    for (int b = 0; b < T::FM; b++) {
+        const int row = wm * T::WTM + b * 32 + (lane & 31);
+#pragma unroll
+        for (int a = 0; a < T::FN; a++)
+#pragma unroll
+            for (int jj = 0; jj < 4; jj++) {
+                uint32_t packed = 0;
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    int32_t v = acc[a][b][4 * jj + i];
+                    if (RELU) v = v < 0 ? 0 : v;
+                    packed |= round_acc<RELU, RTN>(v, rk, mx) << (8 * i);
+                }
+                if (do_store) {
+                    const int col = wn * T::WTN + a * 32 + 8 * jj + 4 * (lane >> 5);
+                    *(uint32_t*)(lds + row * PITCH + col) = packed;
+                }
+            }
+    }
+    if (do_max) tmax = mx > tmax ? mx : tmax;
+}
+
+// Out-of-tile accumulators are zero (their operand rows were zero-filled),
+// so including them in the maximum is harmless.  The LDS tile is written to
+// the output in 16-byte row pieces, with the backward ReLU mask applied.
+template <typename T, int BM, int BN>
+__device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn, const int8_t* lds) {
+    constexpr int PITCH = BN + 16;
+    constexpr int PPR = BN / 16;  // pieces per row
+    for (int idx = threadIdx.x; idx < BM * PPR; idx += T::NT) {
+        const int row = idx / PPR, pc = idx - row * PPR;
+        const int m = tm * BM + row;
+        const int n0 = tn * BN + pc * 16;
+        if (m >= P.M || n0 >= P.Nout) continue;
+        const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
+        const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
+        const uint32_t i0 = fdiv(rem, P.div_ow);
+        const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
+        const int oh = (int)i0 * P.os + P.oa;
+        const int ow = (int)j0 * P.os + P.ob;
+        const int64_t ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo + n0;
+        uint4 v = *(const uint4*)(lds + row * PITCH + pc * 16);
+        const int nv = min(16, P.Nout - n0);
+        int8_t* dst = P.out + ooff;
+        const bool full = nv == 16 && (((uintptr_t)dst) & 15) == 0;
+        if (P.mask) {
+            const int8_t* ms = P.mask + ooff;
+            uint32_t mw[4];
+            if (full) {
+                const uint4 mv = *(const uint4*)ms;
+                mw[0] = mv.x; mw[1] = mv.y; mw[2] = mv.z; mw[3] = mv.w;
+            } else {
+                for (int q = 0; q < 4; q++) mw[q] = 0;
+                for (int e = 0; e < nv; e++) mw[e >> 2] |= (uint32_t)(uint8_t)ms[e] << (8 * (e & 3));
+            }
+            uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                uint32_t keep = 0;
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int8_t mb = (int8_t)(mw[q] >> (8 * e));
+                    keep |= (mb > 0 ? 0xFFu : 0u) << (8 * e);
+                }
+                vw[q] &= keep;
+            }
+            v = make_uint4(vw[0], vw[1], vw[2], vw[3]);
+        }
+        if (full) {
+            *(uint4*)dst = v;
+        } else {
+            const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+            for (int e = 0; e < nv; e++) dst[e] = (int8_t)(vw[e >> 2] >> (8 * (e & 3)));
+        }
+    }
+}
 
 template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
 __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, int8_t* lds, const RoundK& rk,
@@ -194,63 +305,21 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
 
-    // Epilogue: acc[a][b] element 4*jj + i is channel
-    // tile_n + wn*WTN + a*32 + 8*jj + 4*(lane/32) + i of pixel tile_m + wm*WTM + b*32 + lane%32.
-#pragma unroll
-    for (int b = 0; b < T::FM; b++) {
-        const int m = tm * BM + wm * T::WTM + b * 32 + (lane & 31);
-        const bool mvalid = m < P.M;
-        int64_t ooff = 0;
-        if (mvalid) {
-            const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
-            const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
-            const uint32_t i0 = fdiv(rem, P.div_ow);
-            const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
-            const int oh = (int)i0 * P.os + P.oa;
-            const int ow = (int)j0 * P.os + P.ob;
-            ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
-        }
-#pragma unroll
-        for (int a = 0; a < T::FN; a++) {
-#pragma unroll
-            for (int jj = 0; jj < 4; jj++) {
-                const int n0 = tn * BN + wn * T::WTN + a * 32 + 8 * jj + 4 * (lane >> 5);
-                if (!mvalid || n0 >= P.Nout) continue;
-                const int nv = min(4, P.Nout - n0);
-                int32_t v[4];
-#pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    const int32_t x = acc[a][b][4 * jj + i];
-                    v[i] = (relu && x < 0) ? 0 : x;
-                }
-                if (do_max) {
-#pragma unroll
-                    for (int i = 0; i < 4; i++)
-                        if (i < nv) {
-                            const uint64_t mg = mag32(v[i]);
-                            tmax = mg > tmax ? mg : tmax;
-                        }
-                }
-                if (do_store) {
-                    uint32_t packed = 0;
-#pragma unroll
-                    for (int i = 0; i < 4; i++) packed |= (uint32_t)(uint8_t)round_i32(v[i], rk) << (8 * i);
-                    int8_t* dst = P.out + ooff + n0;
-                    if (P.mask) {
-                        const int8_t* ms = P.mask + ooff + n0;
-#pragma unroll
-                        for (int i = 0; i < 4; i++)
-                            if (i < nv && ms[i] <= 0) packed &= ~(0xFFu << (8 * i));
-                    }
-                    if (nv == 4 && ((((uintptr_t)dst) & 3) == 0)) {
-                        *(uint32_t*)dst = packed;
-                    } else {
-                        for (int i = 0; i < nv; i++) dst[i] = (int8_t)(packed >> (8 * i));
-                    }
-                }
-            }
-        }
+    // Epilogue.  acc[a][b] element 4*jj + i is channel
+    // wn*WTN + a*32 + 8*jj + 4*(lane/32) + i of tile pixel wm*WTM + b*32 + lane%32.
+    // Rounded bytes go to the (drained) LDS ring as a [BM][BN] tile, then
+    // leave in 16-byte row pieces.
+    const int mode_sel = (relu ? 1 : 0) | (rk.rtn ? 2 : 0);
+    switch (mode_sel) {
+        case 0: epilogue_regs<T, false, false>(acc, lds, rk, do_store, do_max, tmax); break;
+        case 1: epilogue_regs<T, true, false>(acc, lds, rk, do_store, do_max, tmax); break;
+        case 2: epilogue_regs<T, false, true>(acc, lds, rk, do_store, do_max, tmax); break;
+        default: epilogue_regs<T, true, true>(acc, lds, rk, do_store, do_max, tmax); break;
     }
+    if (!do_store) return;
+    __syncthreads();
+    store_tile<T, BM, BN>(P, tm, tn, lds);
+    __syncthreads();
 }
 
 __device__ __forceinline__ void locate(const IgemmBatch& b, int t, int& prob, int& tm, int& tn) {
