@@ -44,32 +44,64 @@ __global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) 
 
 // Sum of the per-split partial weight gradients (exact mod 2^32) into g32,
 // and the tensor maximum of the sum.  With one split the partial already is
-// g32 and only the maximum is taken.  A workgroup covers 64 consecutive
-// elements; its four waves take interleaved quarters of the splits (each
-// wave reads 256 contiguous bytes per split) and add their sums in LDS.
+// g32 and only the maximum is taken.  A workgroup covers 256 consecutive
+// elements (4 per lane, 16-byte loads); its four waves take interleaved
+// quarters of the splits with four loads in flight each, and add their sums
+// in LDS.
 __global__ __launch_bounds__(256) void reduce_max_kernel(const int32_t* part, int splits, int32_t* g32,
                                                          int64_t n, niti_stats* st) {
-    __shared__ uint32_t sum4[4][64];
+    __shared__ uint4 sum4[4][64];
     const int slot = call_slot(st);
     begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int64_t i = (int64_t)blockIdx.x * 64 + lane;
-    uint32_t v0 = 0, v1 = 0;
-    if (i < n) {
+    const int64_t i0 = (int64_t)blockIdx.x * 256 + 4 * lane;
+    const bool vec = (n % 4) == 0 && i0 + 4 <= n;
+    uint32_t acc[4] = {0, 0, 0, 0};
+    if (vec) {
+        uint4 a = make_uint4(0, 0, 0, 0), b = a, c = a, d = a;
         int z = wv;
-        for (; z + 4 < splits; z += 8) {
-            v0 += (uint32_t)part[(int64_t)z * n + i];
-            v1 += (uint32_t)part[(int64_t)(z + 4) * n + i];
+        for (; z + 12 < splits; z += 16) {
+            const uint4 pa = *(const uint4*)(part + (int64_t)z * n + i0);
+            const uint4 pb = *(const uint4*)(part + (int64_t)(z + 4) * n + i0);
+            const uint4 pc = *(const uint4*)(part + (int64_t)(z + 8) * n + i0);
+            const uint4 pd = *(const uint4*)(part + (int64_t)(z + 12) * n + i0);
+            a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
+            b.x += pb.x; b.y += pb.y; b.z += pb.z; b.w += pb.w;
+            c.x += pc.x; c.y += pc.y; c.z += pc.z; c.w += pc.w;
+            d.x += pd.x; d.y += pd.y; d.z += pd.z; d.w += pd.w;
         }
-        if (z < splits) v0 += (uint32_t)part[(int64_t)z * n + i];
+        for (; z < splits; z += 4) {
+            const uint4 pa = *(const uint4*)(part + (int64_t)z * n + i0);
+            a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
+        }
+        acc[0] = a.x + b.x + c.x + d.x;
+        acc[1] = a.y + b.y + c.y + d.y;
+        acc[2] = a.z + b.z + c.z + d.z;
+        acc[3] = a.w + b.w + c.w + d.w;
+    } else {
+        for (int e = 0; e < 4; e++) {
+            const int64_t i = i0 + e;
+            if (i >= n) break;
+            for (int z = wv; z < splits; z += 4) acc[e] += (uint32_t)part[(int64_t)z * n + i];
+        }
     }
-    sum4[wv][lane] = v0 + v1;
+    sum4[wv][lane] = make_uint4(acc[0], acc[1], acc[2], acc[3]);
     __syncthreads();
     uint64_t m = 0;
-    if (wv == 0 && i < n) {
-        const uint32_t v = sum4[0][lane] + sum4[1][lane] + sum4[2][lane] + sum4[3][lane];
-        if (splits > 1) g32[i] = (int32_t)v;
-        m = mag32((int32_t)v);
+    if (wv == 0) {
+        uint32_t v[4];
+        const uint4 s0 = sum4[0][lane], s1 = sum4[1][lane], s2 = sum4[2][lane], s3 = sum4[3][lane];
+        v[0] = s0.x + s1.x + s2.x + s3.x;
+        v[1] = s0.y + s1.y + s2.y + s3.y;
+        v[2] = s0.z + s1.z + s2.z + s3.z;
+        v[3] = s0.w + s1.w + s2.w + s3.w;
+        for (int e = 0; e < 4; e++) {
+            const int64_t i = i0 + e;
+            if (i >= n) break;
+            if (splits > 1) g32[i] = (int32_t)v[e];
+            const uint64_t a = mag32((int32_t)v[e]);
+            m = a > m ? a : m;
+        }
     }
     block_publish_max(st, slot, m);
 }
@@ -305,7 +337,7 @@ hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int tar
 
 hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
                           hipStream_t s) {
-    const int64_t blocks = (n + 63) / 64;
+    const int64_t blocks = (n + 255) / 256;
     hipLaunchKernelGGL(reduce_max_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(256), 0, s, part, splits,
                        g32, n, st);
     return hipGetLastError();

@@ -7,7 +7,7 @@
 namespace niti {
 
 constexpr int kMaxProblems = 4;   // sub-pixel classes of a stride-2 back-propagation
-constexpr int kFixupGrid = 512;   // workgroups of the fix-up launch
+constexpr int kFixupGrid = 256;   // workgroups of the fix-up launch (one per compute unit)
 
 // One implicit-GEMM problem (see igemm.hip for the index form).
 struct IgemmProblem {
