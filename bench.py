@@ -77,7 +77,8 @@ class ResNetStep:
                  "stats": nst, "bwd_data": not name.startswith("stem"),
                  "macs": conv_macs(batch, c_real, hw, hw, cout, k, k, st, pd)}
             nst += 3 * count
-            ws = max(ws, niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d),
+            ws = max(ws, niti.workspace_bytes(niti.OP_CONV_FWD, d),
+                     niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d),
                      niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, d))
             self.layers.append(L)
         fin, fout = M.RESNET18_FC
@@ -121,7 +122,8 @@ class ResNetStep:
             for c in range(L["count"]):
                 w = L["w"][c]
                 s0 = L["stats"] + 3 * c
-                t("igemm", lambda: niti.conv_fwd(d, L["x"], w, L["y"], self.stats, relu=True, stats_index=s0))
+                t("igemm", lambda: niti.conv_fwd(d, L["x"], w, L["y"], self.stats, relu=True, stats_index=s0,
+                                                   ws=self.ws))
                 if L["bwd_data"]:
                     t("igemm", lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
                                                           relu_src=L["x"], stats_index=s0 + 1))
@@ -238,12 +240,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--batch", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-batch", type=int, default=8)
+    ap.add_argument("--cpu-batch", type=int, default=64)
     ap.add_argument("--layers", action="store_true", help="per-layer timing table on stderr")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(see the sharding notes in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path; "
+              "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -329,7 +331,7 @@ def report_layers(job, reps=5):
                                                  "dgTOPS", "wgTOPS"), file=sys.stderr)
     for L in job.layers:
         d, w, s0 = L["desc"], L["w"][0], L["stats"]
-        calls = [lambda: niti.conv_fwd(d, L["x"], w, L["y"], job.stats, relu=True, stats_index=s0),
+        calls = [lambda: niti.conv_fwd(d, L["x"], w, L["y"], job.stats, relu=True, stats_index=s0, ws=job.ws),
                  (lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], job.stats, job.ws, relu_src=L["x"],
                                              stats_index=s0 + 1)) if L["bwd_data"] else None,
                  lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, job.stats, job.ws, mu=job.mu,

@@ -16,6 +16,10 @@
  *               The library never allocates or frees device memory.  Calls
  *               that need temporary device memory take a caller-provided
  *               workspace (ws, ws_bytes); niti_workspace_bytes() sizes it.
+ *               Tensor and workspace pointers of the contraction, rounding,
+ *               loss and update calls must be 16-byte aligned (hipMalloc and
+ *               torch allocations are); others are rejected with
+ *               NITI_ERR_ARG.
  *   Layout      Activations and errors are NHWC int8 (channels fastest),
  *               convolution weights are KRSC int8 (output channel, filter
  *               row, filter column, input channel), matrices are row-major.
@@ -129,12 +133,14 @@ niti_status niti_gemm_fwd(const int8_t *A, const int8_t *B, int8_t *C,
 
 /* Convolution forward (Algorithm 1, forward loop; Section 3.2 reduces it to
  * an implicit GEMM).  y = round(conv(x, w)), exponents as niti_gemm_fwd
- * with target 7.  Needs c % 4 == 0 (pad image channels with zeros).  No
- * workspace. */
+ * with target 7.  Needs c % 4 == 0 (pad image channels with zeros).
+ * Workspace: niti_workspace_bytes(NITI_OP_CONV_FWD, d, ...), zero for most
+ * layers; layers with few channels (s*c <= 64) use it for a zero-padded
+ * copy of x. */
 niti_status niti_conv_fwd(const niti_conv_desc *d, const int8_t *x, const int8_t *w,
                           int8_t *y, const int8_t *s_x, const int8_t *s_w, int8_t *s_y,
                           int relu, niti_round_mode mode, niti_stats *stats,
-                          void *stream);
+                          void *ws, size_t ws_bytes, void *stream);
 
 /* Error back-propagation through a convolution (Algorithm 1,
  * e(l-1) = w(l) (x) e(l); Section 3.2): dx = round(adjoint of conv in x,

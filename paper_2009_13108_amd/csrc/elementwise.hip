@@ -309,6 +309,36 @@ __global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t*
     }
 }
 
+// One block per padded pixel row (image, row); threads walk its dwords.
+__global__ void pad_image_kernel(const uint32_t* x, uint32_t* xp, int32_t h, int32_t w, int32_t c4, int32_t hp,
+                                 int32_t wp, int32_t ph, int32_t pw) {
+    const uint32_t rid = blockIdx.x;                       // img * hp + padded row
+    const uint32_t img = rid / (uint32_t)hp;
+    const int row = (int)(rid - img * (uint32_t)hp) - ph;
+    const uint32_t len = (uint32_t)wp * (uint32_t)c4;
+    uint32_t* dst = xp + (size_t)rid * len;
+    const bool row_in = row >= 0 && row < h;
+    const uint32_t* src = x + ((size_t)img * h + (row_in ? row : 0)) * (size_t)w * c4;
+    for (uint32_t i = threadIdx.x; i < len; i += blockDim.x) {
+        const uint32_t pc = c4 == 1 ? i : i / (uint32_t)c4;
+        const int col = (int)pc - pw;
+        uint32_t v = 0;
+        if (row_in && col >= 0 && col < w) v = src[(uint32_t)col * (uint32_t)c4 + (i - pc * (uint32_t)c4)];
+        dst[i] = v;
+    }
+}
+
+__global__ void repack_window_kernel(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
+                                     int64_t ktot) {
+    const int64_t total = k * ktot;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t kk = i / ktot, t = i - kk * ktot;
+        const int64_t row = t / lw, j = t - row * lw;
+        wr[i] = (row < r && j < sc) ? w[(kk * r + row) * sc + j] : (int8_t)0;
+    }
+}
+
 __global__ void relu_mask_kernel(int8_t* e, const int8_t* a, int64_t n) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
@@ -404,6 +434,25 @@ hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int
     if (total <= 0) return hipSuccess;
     hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, dy, idx, dx, n,
                        h, w, c);
+    return hipGetLastError();
+}
+
+hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
+                         int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
+    const int64_t total = n * hp * wp * (c / 4);
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)(n * hp)), dim3(kThreads), 0, s, (const uint32_t*)x,
+                       (uint32_t*)xp, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)wp, (int32_t)ph,
+                       (int32_t)pw);
+    return hipGetLastError();
+}
+
+hipError_t repack_window_run(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
+                             int64_t ktot, hipStream_t s) {
+    const int64_t total = k * ktot;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(repack_window_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, w, wr, k, r, sc, lw,
+                       ktot);
     return hipGetLastError();
 }
 

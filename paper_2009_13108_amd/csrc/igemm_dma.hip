@@ -8,7 +8,12 @@
 //           and the K step adds a uniform amount;
 //   kConv64 convolutions with C % 64 == 0: every 64-byte K step lies in one
 //           filter tap (r, s) and channel block c0, all uniform, so a lane
-//           only checks that its pixel's tap is inside the image.
+//           only checks that its pixel's tap is inside the image;
+//   kWin    convolutions with few channels (S*C <= 64) over a zero-padded
+//           copy of the input: a filter row is one contiguous window of
+//           L = 16, 32 or 64 bytes (S pixels, zero weights past them), a K
+//           step covers 64/L filter rows, and every window is in bounds, so
+//           a lane's offset is fixed and the step adds a uniform amount.
 //
 // Loads.  Each wave instruction moves 64 lanes x 16 bytes into one 1 KiB LDS
 // block (lane l lands at block + 16 l); a block holds 16 operand rows of one
@@ -31,6 +36,7 @@ constexpr int KSTEP = 64;  // K bytes per stage
 constexpr uint32_t kOOB = 0x80000000u;
 constexpr int kGemm = 0;
 constexpr int kConv64 = 1;
+constexpr int kWin = 2;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -199,6 +205,19 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
                 base[i] = m < P.M ? (uint32_t)m * (uint32_t)P.C + kpo : kOOB;
                 ih0[i] = 0;
                 iw0[i] = 0;
+            } else if (MODE == kWin) {
+                const uint32_t mm = m < P.M ? (uint32_t)m : 0u;
+                const uint32_t img = fdiv(mm, P.div_ohw);
+                const uint32_t rem = mm - img * (uint32_t)(P.OHc * P.OWc);
+                const uint32_t oh = fdiv(rem, P.div_ow);
+                const uint32_t ow = rem - oh * (uint32_t)P.OWc;
+                const int rr = (int)kpo / P.L;              // filter row of this piece within a step
+                const int j0 = (int)kpo - rr * P.L;
+                ih0[i] = rr;
+                iw0[i] = 0;
+                base[i] = m < P.M ? (uint32_t)(((img * (uint32_t)P.H + oh * (uint32_t)P.st + (uint32_t)rr) *
+                                                    (uint32_t)P.W + ow * (uint32_t)P.st) * (uint32_t)P.C) + (uint32_t)j0
+                                  : kOOB;
             } else {
                 const bool ok = m < P.M;
                 const uint32_t mm = ok ? (uint32_t)m : 0u;
@@ -235,6 +254,11 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
             } else {
                 if (MODE == kGemm) {
                     off = (base[i] != kOOB && kb + kpo < (uint32_t)P.Ktot) ? base[i] + kb : kOOB;
+                } else if (MODE == kWin) {
+                    const int rps = KSTEP / P.L;             // filter rows per step (uniform)
+                    const int r = next_kt * rps + ih0[i];
+                    off = (base[i] != kOOB && r < P.R) ? base[i] + (uint32_t)(next_kt * rps) * (uint32_t)(P.W * P.C)
+                                                      : kOOB;
                 } else {
                     const bool ok = kin && (unsigned)(ih0[i] + tr) < (unsigned)P.H &&
                                     (unsigned)(iw0[i] + ts) < (unsigned)P.W;
@@ -400,6 +424,7 @@ hipError_t launch_dma(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
 }
 
 int problem_mode(const IgemmProblem& p) {
+    if (p.win) return kWin;
     if (p.H == 1 && p.W == 1 && p.R == 1 && p.off_h == 0 && p.off_w == 0 && p.L == p.C) return kGemm;
     return kConv64;
 }
@@ -439,6 +464,10 @@ bool igemm_dma_eligible(const IgemmBatch& b) {
         mode = m;
         if (m == kGemm) {
             if (p.C % 16 != 0 || p.Ktot != p.C) return false;
+        } else if (m == kWin) {
+            if ((p.L != 16 && p.L != 32 && p.L != 64) || p.Ktot != (p.R * p.L + KSTEP - 1) / KSTEP * KSTEP ||
+                p.off_h != 0 || p.off_w != 0)
+                return false;
         } else {
             if (p.C % KSTEP != 0 || p.L != p.S * p.C || p.Lpad != p.L || p.Ktot != p.R * p.L) return false;
         }
@@ -447,7 +476,9 @@ bool igemm_dma_eligible(const IgemmBatch& b) {
 }
 
 hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
-    if (problem_mode(b.p[0]) == kGemm) return run_mode<kGemm>(b, ctl, stream);
+    const int m = problem_mode(b.p[0]);
+    if (m == kGemm) return run_mode<kGemm>(b, ctl, stream);
+    if (m == kWin) return run_mode<kWin>(b, ctl, stream);
     return run_mode<kConv64>(b, ctl, stream);
 }
 

@@ -15,6 +15,8 @@ constexpr int64_t kAccLimit = (int64_t)1 << 31;
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 inline bool too_big(int64_t a) { return a < 0 || a >= kMaxBytes; }
+// Tensor and workspace pointers are read with 16-byte vector and buffer loads.
+inline bool mis16(const void* p) { return ((uintptr_t)p & 15) != 0; }
 
 inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
 
@@ -45,6 +47,33 @@ niti_status check_conv(const niti_conv_desc* d, int64_t* P, int64_t* Q) {
     return NITI_OK;
 }
 
+// Layers with few channels (S*C <= 64, C % 64 != 0) read a zero-padded copy
+// of their input in filter-row windows of lw bytes (igemm_dma.hip, wgrad_dma.hip).
+struct WinPlan {
+    bool on;
+    int64_t hp, wp, lw, ktot;
+    int64_t xpad_bytes, wr_bytes;  // workspace pieces, 256-byte rounded
+};
+
+WinPlan win_plan(const niti_conv_desc* d, int64_t P, int64_t Q) {
+    WinPlan w{};
+    const int64_t sc = d->s * d->c;
+    if (d->c % 64 == 0 || d->c % 4 != 0 || sc > 64) return w;
+    w.lw = sc <= 16 ? 16 : (sc <= 32 ? 32 : 64);
+    w.hp = d->h + 2 * (int64_t)d->pad_h;
+    const int64_t need_w = (Q - 1) * d->stride_w + (w.lw + d->c - 1) / d->c;  // last window in its row
+    w.wp = d->w + 2 * (int64_t)d->pad_w;
+    if (need_w > w.wp) w.wp = need_w;
+    w.ktot = round_up(d->r * w.lw, 64);
+    const int64_t xb = d->n * w.hp * w.wp * d->c;
+    if (too_big(xb) || too_big(d->k * w.ktot)) return w;
+    (void)P;
+    w.xpad_bytes = round_up(xb, 256);
+    w.wr_bytes = round_up(d->k * w.ktot, 256);
+    w.on = true;
+    return w;
+}
+
 void set_out_grid(IgemmProblem& p, int64_t n, int64_t ohc, int64_t owc) {
     p.OHc = (int32_t)ohc;
     p.OWc = (int32_t)owc;
@@ -72,18 +101,81 @@ const char* niti_status_str(niti_status s) {
     return "unknown status";
 }
 
+// Weight-gradient problem for a checked descriptor; shared by the workspace
+// query and the entry point so that both take the same decisions.
+struct WgradSetup {
+    WgradProblem p;
+    WinPlan wp;
+    bool win;
+    WgradPlan plan;
+};
+
+WgradSetup wgrad_setup(const niti_conv_desc* d, int64_t P, int64_t Q) {
+    WgradSetup r{};
+    WgradProblem& p = r.p;
+    const int64_t npix = d->n * P * Q;
+    p.K = (int32_t)d->k;
+    p.R = (int32_t)d->r;
+    p.S = (int32_t)d->s;
+    p.C = (int32_t)d->c;
+    p.P = (int32_t)P;
+    p.Q = (int32_t)Q;
+    p.sh = d->stride_h;
+    p.sw = d->stride_w;
+    p.L = p.S * p.C;
+    p.ncol = p.R * p.L;
+    p.npix = (int32_t)npix;
+    p.div_pq = make_fastdiv((uint32_t)(P * Q));
+    p.div_q = make_fastdiv((uint32_t)Q);
+    p.div_l = make_fastdiv((uint32_t)p.L);
+    p.div_c = make_fastdiv((uint32_t)p.C);
+    p.dy_bytes = npix * d->k;
+    // Window mode (few channels): a zero-padded copy of x, read in filter-row windows.
+    r.wp = win_plan(d, P, Q);
+    if (r.wp.on) {
+        p.H = (int32_t)r.wp.hp;
+        p.W = (int32_t)r.wp.wp;
+        p.ph = 0;
+        p.pw = 0;
+        p.x_bytes = d->n * r.wp.hp * r.wp.wp * d->c;
+        p.win = 1;
+        p.Lw = (int32_t)r.wp.lw;
+        p.ncol_w = p.R * p.Lw;
+        r.win = wgrad_dma_eligible(p);
+    }
+    if (!r.win) {
+        p.H = (int32_t)d->h;
+        p.W = (int32_t)d->w;
+        p.ph = d->pad_h;
+        p.pw = d->pad_w;
+        p.x_bytes = d->n * d->h * d->w * d->c;
+        p.win = 0;
+        p.Lw = 0;
+        p.ncol_w = 0;
+    }
+    r.plan = wgrad_plan(d->k, r.win ? p.ncol_w : p.ncol, npix);
+    return r;
+}
+
 size_t niti_workspace_bytes(int op, const niti_conv_desc* d, int64_t M, int64_t N, int64_t K) {
     (void)K;
+    int64_t P = 0, Q = 0;
+    if ((op == NITI_OP_CONV_FWD || op == NITI_OP_CONV_BWD_DATA || op == NITI_OP_CONV_BWD_WEIGHT) &&
+        (!d || check_conv(d, &P, &Q) != NITI_OK))
+        return 0;
     switch (op) {
+        case NITI_OP_CONV_FWD: {
+            const WinPlan w = win_plan(d, P, Q);
+            return w.on ? (size_t)(w.xpad_bytes + w.wr_bytes) : 0;
+        }
         case NITI_OP_CONV_BWD_DATA:
-            return d ? (size_t)round_up(d->k * d->r * d->s * d->c, 256) : 0;
+            return (size_t)round_up(d->k * d->r * d->s * d->c, 256);
         case NITI_OP_CONV_BWD_WEIGHT: {
-            if (!d) return 0;
-            int64_t P, Q;
-            if (check_conv(d, &P, &Q) != NITI_OK) return 0;
             const int64_t nw = d->k * d->r * d->s * d->c;
-            const WgradPlan pl = wgrad_plan(d->k, d->r * d->s * d->c, d->n * P * Q);
-            return (size_t)(round_up(nw * 4, 256) + (pl.splits > 1 ? round_up((int64_t)pl.splits * nw * 4, 256) : 0));
+            const WgradSetup w = wgrad_setup(d, P, Q);
+            return (size_t)(round_up(nw * 4, 256) +
+                            (w.plan.splits > 1 ? round_up((int64_t)w.plan.splits * nw * 4, 256) : 0) +
+                            (w.win ? w.wp.xpad_bytes : 0));
         }
         case NITI_OP_INT_CE_LOSS:
             return (M > 0 && N > 0) ? (size_t)round_up(M * N * 8, 256) : 0;
@@ -98,6 +190,7 @@ niti_status niti_gemm_fwd(const int8_t* A, const int8_t* B, int8_t* C, int64_t M
     if (!C || !stats) return NITI_ERR_NULL;
     if (M < 1 || N < 1 || K < 0) return NITI_ERR_SHAPE;
     if ((!A || !B) && K > 0) return NITI_ERR_NULL;
+    if (mis16(A) || mis16(B) || mis16(C)) return NITI_ERR_ARG;
     if (target_bits < 1 || target_bits > 31 || !valid_mode(mode)) return NITI_ERR_ARG;
     const int nexp = (s_a != nullptr) + (s_b != nullptr) + (s_c != nullptr);
     if (nexp != 0 && nexp != 3) return NITI_ERR_NULL;
@@ -143,43 +236,19 @@ niti_status niti_gemm_fwd(const int8_t* A, const int8_t* B, int8_t* C, int64_t M
 
 niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t* w, int8_t* y,
                           const int8_t* s_x, const int8_t* s_w, int8_t* s_y, int relu, niti_round_mode mode,
-                          niti_stats* stats, void* stream) {
+                          niti_stats* stats, void* ws, size_t ws_bytes, void* stream) {
     int64_t P, Q;
     if (!d) return NITI_ERR_NULL;
     if (!x || !w || !y || !stats) return NITI_ERR_NULL;
+    if (mis16(x) || mis16(w) || mis16(y) || mis16(ws)) return NITI_ERR_ARG;
     const int nexp = (s_x != nullptr) + (s_w != nullptr) + (s_y != nullptr);
     if (nexp != 0 && nexp != 3) return NITI_ERR_NULL;
     if (!valid_mode(mode)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
-    IgemmBatch b{};
-    b.nprob = 1;
-    IgemmProblem& p = b.p[0];
-    p.act = x;
-    p.wgt = w;
-    p.out = y;
-    p.mask = nullptr;
-    p.Nout = (int32_t)d->k;
-    p.R = (int32_t)d->r;
-    p.S = (int32_t)d->s;
-    p.L = (int32_t)(d->s * d->c);
-    p.Lpad = (int32_t)round_up(p.L, 16);
-    p.Ktot = p.R * p.Lpad;
-    p.H = (int32_t)d->h;
-    p.W = (int32_t)d->w;
-    p.C = (int32_t)d->c;
-    p.st = d->stride_h;
-    p.off_h = -d->pad_h;
-    p.off_w = -d->pad_w;
-    set_out_grid(p, d->n, P, Q);
-    p.OH = (int32_t)P;
-    p.OW = (int32_t)Q;
-    p.ldo = (int32_t)d->k;
-    p.os = 1;
-    p.oa = 0;
-    p.ob = 0;
-    p.act_bytes = d->n * d->h * d->w * d->c;
-    p.wgt_bytes = d->k * d->r * d->s * d->c;
+    const size_t need = niti_workspace_bytes(NITI_OP_CONV_FWD, d, 0, 0, 0);
+    if (need > 0 && (!ws || ws_bytes < need)) return NITI_ERR_WORKSPACE;
+    hipStream_t strm = as_stream(stream);
     IgemmCtl ctl{};
     ctl.stats = stats;
     ctl.ex = ExpArgs{s_x, s_w, s_y};
@@ -187,7 +256,63 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
     ctl.relu = relu ? 1 : 0;
     ctl.mode = mode;
     ctl.static_flags = acc_flags(d->r * d->s * d->c);
-    return hip_status(igemm_run(b, ctl, as_stream(stream)));
+
+    IgemmBatch b{};
+    b.nprob = 1;
+    IgemmProblem& p = b.p[0];
+    p.out = y;
+    p.mask = nullptr;
+    p.Nout = (int32_t)d->k;
+    p.R = (int32_t)d->r;
+    p.S = (int32_t)d->s;
+    p.C = (int32_t)d->c;
+    p.st = d->stride_h;
+    set_out_grid(p, d->n, P, Q);
+    p.OH = (int32_t)P;
+    p.OW = (int32_t)Q;
+    p.ldo = (int32_t)d->k;
+    p.os = 1;
+    p.oa = 0;
+    p.ob = 0;
+
+    const WinPlan wp = win_plan(d, P, Q);
+    if (wp.on) {
+        // zero-padded input and window-extended filter rows in the workspace
+        int8_t* xpad = (int8_t*)ws;
+        int8_t* wr = xpad + wp.xpad_bytes;
+        p.act = xpad;
+        p.wgt = wr;
+        p.H = (int32_t)wp.hp;
+        p.W = (int32_t)wp.wp;
+        p.off_h = 0;
+        p.off_w = 0;
+        p.L = (int32_t)wp.lw;
+        p.Lpad = p.L;
+        p.Ktot = (int32_t)wp.ktot;
+        p.act_bytes = d->n * wp.hp * wp.wp * d->c;
+        p.wgt_bytes = d->k * wp.ktot;
+        p.win = 1;
+        if (igemm_dma_eligible(b)) {
+            hipError_t e = pad_image_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, strm);
+            if (e != hipSuccess) return NITI_ERR_HIP;
+            e = repack_window_run(w, wr, d->k, d->r, d->s * d->c, wp.lw, wp.ktot, strm);
+            if (e != hipSuccess) return NITI_ERR_HIP;
+            return hip_status(igemm_run(b, ctl, strm));
+        }
+    }
+    p.act = x;
+    p.wgt = w;
+    p.H = (int32_t)d->h;
+    p.W = (int32_t)d->w;
+    p.off_h = -d->pad_h;
+    p.off_w = -d->pad_w;
+    p.L = (int32_t)(d->s * d->c);
+    p.Lpad = (int32_t)round_up(p.L, 16);
+    p.Ktot = p.R * p.Lpad;
+    p.act_bytes = d->n * d->h * d->w * d->c;
+    p.wgt_bytes = d->k * d->r * d->s * d->c;
+    p.win = 0;
+    return hip_status(igemm_run(b, ctl, strm));
 }
 
 niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const int8_t* w, int8_t* dx,
@@ -196,6 +321,7 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
     int64_t P, Q;
     if (!d) return NITI_ERR_NULL;
     if (!dy || !w || !dx || !stats) return NITI_ERR_NULL;
+    if (mis16(dy) || mis16(w) || mis16(dx) || mis16(relu_src) || mis16(ws)) return NITI_ERR_ARG;
     if (!valid_mode(mode)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
@@ -268,46 +394,38 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     int64_t P, Q;
     if (!d) return NITI_ERR_NULL;
     if (!x || !dy || !w || !stats) return NITI_ERR_NULL;
+    if (mis16(x) || mis16(dy) || mis16(w) || mis16(g32_out) || mis16(ws)) return NITI_ERR_ARG;
     if (mu < 1 || mu > 8 || !valid_mode(mode)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
     const int64_t nw = d->k * d->r * d->s * d->c;
     const int64_t npix = d->n * P * Q;
     if (too_big(npix)) return NITI_ERR_UNSUPPORTED;
-    const WgradPlan plan = wgrad_plan(d->k, d->r * d->s * d->c, npix);
+    hipStream_t strm = as_stream(stream);
+    const WgradSetup ws_ = wgrad_setup(d, P, Q);
+    WgradProblem p = ws_.p;
+    const bool win = ws_.win;
+    const WinPlan& wp = ws_.wp;
+    const WgradPlan& plan = ws_.plan;
+    p.dy = dy;
+    p.x = x;
     const int64_t g_bytes = g32_out ? 0 : round_up(nw * 4, 256);
     const int64_t p_bytes = plan.splits > 1 ? round_up((int64_t)plan.splits * nw * 4, 256) : 0;
+    const int64_t x_bytes = win ? wp.xpad_bytes : 0;
     if (too_big(p_bytes)) return NITI_ERR_UNSUPPORTED;
-    if (g_bytes + p_bytes > 0 && (!ws || ws_bytes < (size_t)(g_bytes + p_bytes))) return NITI_ERR_WORKSPACE;
+    if (g_bytes + p_bytes + x_bytes > 0 && (!ws || ws_bytes < (size_t)(g_bytes + p_bytes + x_bytes)))
+        return NITI_ERR_WORKSPACE;
     int32_t* g32 = g32_out ? g32_out : (int32_t*)ws;
     int32_t* part = plan.splits > 1 ? (int32_t*)((char*)ws + g_bytes) : g32;
-    hipStream_t strm = as_stream(stream);
-    WgradProblem p{};
-    p.x = x;
-    p.dy = dy;
+    hipError_t e;
+    if (win) {
+        int8_t* xpad = (int8_t*)ws + g_bytes + p_bytes;
+        e = pad_image_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, strm);
+        if (e != hipSuccess) return NITI_ERR_HIP;
+        p.x = xpad;
+    }
     p.part = part;
-    p.H = (int32_t)d->h;
-    p.W = (int32_t)d->w;
-    p.C = (int32_t)d->c;
-    p.K = (int32_t)d->k;
-    p.R = (int32_t)d->r;
-    p.S = (int32_t)d->s;
-    p.P = (int32_t)P;
-    p.Q = (int32_t)Q;
-    p.sh = d->stride_h;
-    p.sw = d->stride_w;
-    p.ph = d->pad_h;
-    p.pw = d->pad_w;
-    p.L = p.S * p.C;
-    p.ncol = p.R * p.L;
-    p.npix = (int32_t)npix;
-    p.div_pq = make_fastdiv((uint32_t)(P * Q));
-    p.div_q = make_fastdiv((uint32_t)Q);
-    p.div_l = make_fastdiv((uint32_t)p.L);
-    p.div_c = make_fastdiv((uint32_t)p.C);
-    p.x_bytes = d->n * d->h * d->w * d->c;
-    p.dy_bytes = npix * d->k;
-    hipError_t e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
+    e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
@@ -319,6 +437,7 @@ niti_status niti_round_psr(const int32_t* x, int8_t* y, int64_t n, int bp, int t
                            void* stream) {
     if (n < 0) return NITI_ERR_SHAPE;
     if ((!x || !y) && n > 0) return NITI_ERR_NULL;
+    if (mis16(x) || mis16(y)) return NITI_ERR_ARG;
     if (!valid_mode(mode) || bp > 31) return NITI_ERR_ARG;
     if ((s_in == nullptr) != (s_out == nullptr)) return NITI_ERR_NULL;
     if (bp < 0) {
@@ -338,6 +457,7 @@ niti_status niti_int_ce_loss_grad(const int8_t* logits, const int8_t* s_logits, 
                                   int8_t* err, int64_t batch, int64_t classes, niti_round_mode mode,
                                   niti_stats* stats, void* ws, size_t ws_bytes, void* stream) {
     if (!logits || !s_logits || !labels || !err || !stats) return NITI_ERR_NULL;
+    if (mis16(logits) || mis16(labels) || mis16(err) || mis16(ws)) return NITI_ERR_ARG;
     if (batch < 1 || classes < 1) return NITI_ERR_SHAPE;
     if (classes > 65536 || !valid_mode(mode)) return NITI_ERR_ARG;
     if (too_big(batch * classes * 8)) return NITI_ERR_UNSUPPORTED;
@@ -351,6 +471,7 @@ niti_status niti_sgd_update(int8_t* w, const int32_t* g32, int64_t n, int mu, ni
                             niti_stats* stats, void* stream) {
     if (n < 0) return NITI_ERR_SHAPE;
     if (((!w || !g32) && n > 0) || !stats) return NITI_ERR_NULL;
+    if (mis16(w) || mis16(g32)) return NITI_ERR_ARG;
     if (mu < 1 || mu > 8 || !valid_mode(mode)) return NITI_ERR_ARG;
     if (too_big(n * 4)) return NITI_ERR_UNSUPPORTED;
     hipStream_t strm = as_stream(stream);

@@ -27,6 +27,7 @@ struct IgemmProblem {
     FastDiv div_ohw, div_ow;
     int64_t act_bytes;   // extent of act (bytes), for buffer bounds
     int64_t wgt_bytes;   // extent of wgt (bytes)
+    int32_t win;         // act is a zero-padded image read in filter-row windows of L bytes
 };
 
 struct IgemmBatch {
@@ -62,6 +63,8 @@ struct WgradProblem {
     int32_t chunk;     // pixels per split (multiple of 64)
     FastDiv div_pq, div_q, div_l, div_c;
     int64_t x_bytes, dy_bytes;  // extents, for buffer bounds
+    int32_t win;       // x is a zero-padded image read in filter-row windows of Lw bytes
+    int32_t Lw, ncol_w;         // window bytes per filter row, R*Lw
 };
 
 struct WgradPlan {
@@ -103,5 +106,13 @@ hipError_t maxpool_fwd_run(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, 
 hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
                            int64_t w, int64_t c, hipStream_t s);
 hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s);
+// Zero-padded copy of an NHWC image (C % 4 == 0): xp[n][Hp][Wp][C] with the
+// input at rows ph.., columns pw..; everything else zero.
+hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
+                         int64_t wp, int64_t ph, int64_t pw, hipStream_t s);
+// Filter rows as zero-extended windows: wr[k][t], t < ktot: row t / lw, byte
+// t % lw of w[k][row][S*C] (zero past S*C and past R rows).
+hipError_t repack_window_run(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
+                             int64_t ktot, hipStream_t s);
 
 }  // namespace niti

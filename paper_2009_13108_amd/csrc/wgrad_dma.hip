@@ -17,6 +17,12 @@
 //
 // Each workgroup reduces one pixel range for one output tile and stores the
 // partial tile to its own slice; a bandwidth pass sums the slices.
+//
+// Window mode (few channels, S*C <= 64): x is a zero-padded copy of the
+// input, and a filter row (r) is one window of Lw bytes (S pixels and zero
+// columns past them), so column col = r*Lw + j of X is x_pad at pixel row
+// oh*sh + r, byte (ow*sw)*C + j: always in bounds.  Only columns with j <
+// S*C are stored, compacted to r*S*C + j.
 #include "niti_internal.h"
 
 namespace niti {
@@ -110,14 +116,23 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P) {
             const int chunk = (lane & 7) ^ swz<TBC>(p);
             const int col = c0 + 16 * chunk;
             prow[i] = p;
-            cok[i] = col < P.ncol;
-            const int cc = cok[i] ? col : 0;
-            const int r = (int)fdiv((uint32_t)cc, P.div_l);
-            const int jj = cc - r * P.L;
-            const int s = (int)fdiv((uint32_t)jj, P.div_c);
-            tdh[i] = r - P.ph;
-            tdw[i] = s - P.pw;
-            toff[i] = (uint32_t)(jj - s * P.C);
+            if (P.win) {
+                cok[i] = col < P.ncol_w;
+                const int cc = cok[i] ? col : 0;
+                const int r = cc / P.Lw;
+                tdh[i] = 0;
+                tdw[i] = 0;
+                toff[i] = (uint32_t)(r * P.W * P.C + (cc - r * P.Lw));
+            } else {
+                cok[i] = col < P.ncol;
+                const int cc = cok[i] ? col : 0;
+                const int r = (int)fdiv((uint32_t)cc, P.div_l);
+                const int jj = cc - r * P.L;
+                const int s = (int)fdiv((uint32_t)jj, P.div_c);
+                tdh[i] = r - P.ph;
+                tdw[i] = s - P.pw;
+                toff[i] = (uint32_t)(jj - s * P.C);
+            }
         } else {
             const int b = blk - T::XBLK;
             constexpr int PPB = 1024 / TBK;          // pixels per block
@@ -151,7 +166,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P) {
                     const int ow = rem - oh * P.Q;
                     const int ih = oh * P.sh + tdh[i];
                     const int iw = ow * P.sw + tdw[i];
-                    if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W)
+                    if (P.win || ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W))
                         off = (uint32_t)(((n * P.H + ih) * P.W + iw) * P.C) + toff[i];
                 }
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
@@ -207,7 +222,14 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P) {
         for (int a = 0; a < T::FC; a++)
 #pragma unroll
             for (int jj = 0; jj < 4; jj++) {
-                const int cidx = c0 + wc * T::WTC + a * 32 + 8 * jj + 4 * (lane >> 5);
+                int cidx = c0 + wc * T::WTC + a * 32 + 8 * jj + 4 * (lane >> 5);
+                if (P.win) {
+                    // window column r*Lw + j -> stored column r*L + j, j < L (groups of 4 stay whole)
+                    if (cidx >= P.ncol_w) continue;
+                    const int r = cidx / P.Lw, j = cidx - r * P.Lw;
+                    if (j >= P.L) continue;
+                    cidx = r * P.L + j;
+                }
                 if (cidx >= P.ncol) continue;
                 int32_t* dst = grow + cidx;
                 if ((((uintptr_t)dst) & 15) == 0 && cidx + 4 <= P.ncol) {
@@ -230,7 +252,7 @@ hipError_t launch(const WgradProblem& p, const WgradPlan& plan, hipStream_t stre
         if (e != hipSuccess) return e;
         attr_done = true;
     }
-    const int tc = (p.ncol + TBC - 1) / TBC;
+    const int tc = ((p.win ? p.ncol_w : p.ncol) + TBC - 1) / TBC;
     const int tk = (p.K + TBK - 1) / TBK;
     hipLaunchKernelGGL((wgrad_dma_kernel<TBK, TBC, NS>), dim3(tc, tk, plan.splits), dim3(256), T::LDS, stream, p);
     return hipGetLastError();
@@ -239,8 +261,9 @@ hipError_t launch(const WgradProblem& p, const WgradPlan& plan, hipStream_t stre
 }  // namespace
 
 bool wgrad_dma_eligible(const WgradProblem& p) {
-    return p.C % 16 == 0 && p.K % 16 == 0 && p.x_bytes > 0 && p.x_bytes < ((int64_t)1 << 31) &&
-           p.dy_bytes > 0 && p.dy_bytes < ((int64_t)1 << 31);
+    const bool cols = p.win ? (p.Lw % 16 == 0 && p.L % 4 == 0 && p.ph == 0 && p.pw == 0) : p.C % 16 == 0;
+    return cols && p.K % 16 == 0 && p.x_bytes > 0 && p.x_bytes < ((int64_t)1 << 31) && p.dy_bytes > 0 &&
+           p.dy_bytes < ((int64_t)1 << 31);
 }
 
 hipError_t wgrad_dma_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {

@@ -86,7 +86,8 @@ class IntNet:
         ws = 0
         for L in self.layers:
             if L["kind"] in ("conv", "fc"):
-                ws = max(ws, niti.workspace_bytes(niti.OP_CONV_BWD_DATA, L["desc"]),
+                ws = max(ws, niti.workspace_bytes(niti.OP_CONV_FWD, L["desc"]),
+                         niti.workspace_bytes(niti.OP_CONV_BWD_DATA, L["desc"]),
                          niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, L["desc"]))
         n_cls = self.layers[-1]["out_shape"][2]
         ws = max(ws, niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, batch, n_cls))
@@ -100,7 +101,7 @@ class IntNet:
             k = L["kind"]
             if k == "conv":
                 niti.conv_fwd(L["desc"], a, L["w"], L["y"], self.stats, s_a, L["s_w"], L["s_y"],
-                              relu=L["relu"], mode=self.mode, stats_index=L["stats"])
+                              relu=L["relu"], mode=self.mode, stats_index=L["stats"], ws=self.ws)
             elif k == "fc":
                 niti.gemm_fwd(a.view(self.batch, L["nin"]), L["w"], L["y"].view(self.batch, L["nout"]),
                               self.stats, s_a, L["s_w"], L["s_y"], 7, L["relu"], self.mode,

@@ -98,7 +98,7 @@ def lib():
             P, I64, I, Z = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
             sig = {
                 "niti_gemm_fwd": [P, P, P, I64, I64, I64, P, P, P, I, I, I, P, P],
-                "niti_conv_fwd": [P, P, P, P, P, P, P, I, I, P, P],
+                "niti_conv_fwd": [P, P, P, P, P, P, P, I, I, P, P, Z, P],
                 "niti_conv_bwd_data": [P, P, P, P, P, I, P, P, Z, P],
                 "niti_conv_bwd_weight": [P, P, P, P, P, I, I, P, P, Z, P],
                 "niti_round_psr": [P, P, I64, I, I, I, P, P, P, P],
@@ -236,12 +236,17 @@ def _conv_check(d: ConvDesc, **tensors):
 
 
 def conv_fwd(d: ConvDesc, x, w, y, stats, s_x=None, s_w=None, s_y=None, relu=False, mode=PSR,
-             stats_index=0, stream=None):
+             stats_index=0, ws=None, stream=None):
+    """Forward convolution; ws is needed when workspace_bytes(OP_CONV_FWD, d) > 0."""
+    torch = _torch()
     _conv_check(d, x=x, w=w, y=y)
     _exp3(s_x, s_w, s_y, "conv_fwd")
+    if ws is not None:
+        _dev(ws, torch.uint8, "ws")
     _check(lib().niti_conv_fwd(ctypes.byref(d), _ptr(x), _ptr(w), _ptr(y), _ptr(s_x), _ptr(s_w),
                                _ptr(s_y), int(bool(relu)), int(mode), _stats_ptr(stats, stats_index),
-                               _stream(stream)), "niti_conv_fwd")
+                               _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
+           "niti_conv_fwd")
 
 
 def conv_bwd_data(d: ConvDesc, dy, w, dx, stats, ws, relu_src=None, mode=PSR, stats_index=0, stream=None):

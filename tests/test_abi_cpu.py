@@ -69,13 +69,13 @@ def test_gemm_rejects_on_host():
 def test_conv_rejects_on_host():
     L = niti.lib()
     d = niti.ConvDesc.make(2, 8, 8, 3, 16, 3, 3, 1, 1)           # c % 4 != 0
-    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -3
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -3
     d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 3, 1)           # stride 3
-    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -3
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -3
     d = niti.ConvDesc.make(2, 2, 2, 4, 16, 5, 5, 1, 0)           # filter larger than padded input
-    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -2
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -2
     d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 1, 1)
-    assert L.niti_conv_fwd(None, FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None) == -1
+    assert L.niti_conv_fwd(None, FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -1
     assert L.niti_conv_bwd_data(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, None, 0, None) == -4
     assert L.niti_conv_bwd_data(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, 16, None) == -4
     assert L.niti_conv_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, 5, 0, FAKE, None, 0, None) == -4
@@ -97,3 +97,31 @@ def test_other_calls_reject_on_host():
     assert L.niti_maxpool2_fwd(FAKE, FAKE, FAKE, 1, 3, 4, 4, None) == -2
     assert L.niti_quantize_u8(FAKE, FAKE, 1, 3, 4, 4, 2, None) == -2
     assert L.niti_relu_mask(FAKE, FAKE, -4, None) == -2
+
+
+def test_conv_fwd_workspace_rules():
+    """Few-channel layers need a forward workspace; wide ones need none."""
+    L = niti.lib()
+    stem = niti.ConvDesc.make(128, 224, 224, 4, 64, 7, 7, 2, 3)
+    need = niti.workspace_bytes(niti.OP_CONV_FWD, stem)
+    # padded 230x230 image copy plus 64 filters of 7 rows x 32 bytes (rounded to 256 bytes)
+    assert need == 128 * 230 * 230 * 4 + 64 * 256
+    assert L.niti_conv_fwd(ctypes.byref(stem), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE,
+                           None, 0, None) == -4
+    assert L.niti_conv_fwd(ctypes.byref(stem), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE,
+                           FAKE, need - 1, None) == -4
+    wide = niti.ConvDesc.make(8, 14, 14, 64, 64, 3, 3, 1, 1)
+    assert niti.workspace_bytes(niti.OP_CONV_FWD, wide) == 0
+    # the weight-gradient workspace of a few-channel layer also holds the padded copy
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, stem) > 128 * 230 * 230 * 4
+
+
+def test_misaligned_pointers_rejected():
+    L = niti.lib()
+    odd = ctypes.c_void_p(0x100008)
+    S = FAKE
+    assert L.niti_gemm_fwd(odd, FAKE, FAKE, 4, 4, 16, None, None, None, 7, 0, 0, S, None) == -6
+    d = niti.ConvDesc.make(2, 8, 8, 64, 16, 3, 3, 1, 1)
+    assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, odd, None, None, None, 0, 0, FAKE,
+                           None, 0, None) == -6
+    assert L.niti_sgd_update(FAKE, odd, 16, 5, 0, S, None) == -6

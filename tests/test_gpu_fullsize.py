@@ -100,10 +100,11 @@ def test_resnet18_layer_fullsize(rec):
     y = torch.empty(d.y_shape(), dtype=torch.int8, device="cuda")
     dx = torch.empty(d.x_shape(), dtype=torch.int8, device="cuda")
     g32 = torch.empty(d.w_shape(), dtype=torch.int32, device="cuda")
-    ws = niti.new_workspace(max(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d),
+    ws = niti.new_workspace(max(niti.workspace_bytes(niti.OP_CONV_FWD, d),
+                                niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d),
                                 niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, d)))
     for rep in range(2):
-        niti.conv_fwd(d, x, w0, y, stats, relu=True, stats_index=0)
+        niti.conv_fwd(d, x, w0, y, stats, relu=True, stats_index=0, ws=ws)
         if "bwd_data" in rec:
             niti.conv_bwd_data(d, dy, w0, dx, stats, ws, relu_src=x, stats_index=1)
         w = w0.clone()

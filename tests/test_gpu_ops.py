@@ -105,6 +105,11 @@ CONV_CASES = [
     (2, 32, 16, 16, 96, 1, 1, 2, 0, True),
     (1, 4, 32, 32, 64, 7, 7, 2, 3, True),
     (4, 128, 7, 7, 130, 3, 3, 1, 1, False),
+    # few channels: padded-copy window path (s*c <= 64), windows of 16/32/64 bytes
+    (2, 12, 9, 9, 16, 3, 3, 1, 1, True),
+    (2, 8, 10, 10, 32, 3, 3, 2, 1, False),
+    (3, 4, 13, 12, 48, 5, 5, 2, 2, True),
+    (2, 16, 7, 7, 32, 2, 2, 1, 0, False),
 ]
 
 
@@ -131,9 +136,11 @@ def test_conv_fwd_parity(case):
     stats = niti.new_stats()
     sx, sw, sy = _i8(-3), _i8(-8), _i8(0)
     dx_, dw_ = dev(nhwc(x)), dev(krsc(wt))
+    nws = niti.workspace_bytes(niti.OP_CONV_FWD, gd)
+    ws = niti.new_workspace(nws) if nws else None
     for rep in range(2):
         y.fill_(77)
-        niti.conv_fwd(gd, dx_, dw_, y, stats, sx, sw, sy, relu=relu)
+        niti.conv_fwd(gd, dx_, dw_, y, stats, sx, sw, sy, relu=relu, ws=ws)
         torch.cuda.synchronize()
         g = niti.read_stats(stats)[0]
         assert (nchw(host(y)) == exp_out).all(), "rep %d" % rep
@@ -171,7 +178,8 @@ def test_conv_bwd_weight_parity(case, mu):
     w_dev = dev(krsc(wt))
     g32 = torch.empty(gd.w_shape(), dtype=torch.int32, device="cuda")
     stats = niti.new_stats()
-    niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w_dev, stats, None, g32_out=g32, mu=mu)
+    ws = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gd))
+    niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w_dev, stats, ws, g32_out=g32, mu=mu)
     torch.cuda.synchronize()
     g = niti.read_stats(stats)[0]
     assert (kcrs(host(g32)) == exp_g32).all()
@@ -179,7 +187,6 @@ def test_conv_bwd_weight_parity(case, mu):
     assert same_stats(g, st)
     # same again through the workspace (no g32_out), from the original weights
     w2 = dev(krsc(wt))
-    ws = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gd))
     niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w2, stats, ws, mu=mu)
     torch.cuda.synchronize()
     assert (kcrs(host(w2)) == exp_w).all()
