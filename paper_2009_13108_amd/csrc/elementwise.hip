@@ -106,6 +106,56 @@ __global__ __launch_bounds__(256) void reduce_max_kernel(const int32_t* part, in
     block_publish_max(st, slot, m);
 }
 
+// The same sum for few splits (NZ <= 8, n % 4 == 0): every lane owns four
+// consecutive elements at a time and adds all NZ partials itself (NZ
+// independent 16-byte loads in flight), striding over the tensor; one
+// maximum per workgroup is folded in at the end.
+template <int NZ>
+__global__ __launch_bounds__(256) void reduce_max_flat_kernel(const int32_t* part, int32_t* g32, int64_t n,
+                                                              niti_stats* st) {
+    const int slot = call_slot(st);
+    begin_call(st, slot, -1);
+    const int64_t nq = n >> 2;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    uint64_t m = 0;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += step) {
+        uint4 v[NZ];
+#pragma unroll
+        for (int z = 0; z < NZ; z++) v[z] = *(const uint4*)(part + (int64_t)z * n + 4 * q);
+        uint4 a = v[0];
+#pragma unroll
+        for (int z = 1; z < NZ; z++) {
+            a.x += v[z].x;
+            a.y += v[z].y;
+            a.z += v[z].z;
+            a.w += v[z].w;
+        }
+        if (NZ > 1) *(uint4*)(g32 + 4 * q) = a;
+        const uint64_t m01 = max(mag32((int32_t)a.x), mag32((int32_t)a.y));
+        const uint64_t m23 = max(mag32((int32_t)a.z), mag32((int32_t)a.w));
+        const uint64_t mq = max(m01, m23);
+        m = mq > m ? mq : m;
+    }
+    block_publish_max(st, slot, m);
+}
+
+// Rows of the strided back-propagation output that belong to sub-pixel
+// classes with no filter taps are exact zeros: out[img][y][x][:] = 0 for every
+// (y % st, x % st) whose bit (y % st) * st + x % st is set in mask.  One
+// workgroup per output row; rows whose classes all have taps return at once.
+__global__ void zero_classes_kernel(uint32_t* out, int32_t h, int32_t w, int32_t c4, int32_t st, uint32_t mask) {
+    const uint32_t rid = blockIdx.x;   // img * h + y
+    const int y = (int)(rid % (uint32_t)h);
+    const uint32_t rowbits = (mask >> ((y % st) * st)) & ((1u << st) - 1u);
+    if (rowbits == 0) return;
+    const uint32_t len = (uint32_t)w * (uint32_t)c4;
+    uint32_t* row = out + (size_t)rid * len;
+    for (uint32_t i = threadIdx.x; i < len; i += blockDim.x) {
+        const uint32_t x = c4 == 1 ? i : i / (uint32_t)c4;
+        if ((rowbits >> (x % (uint32_t)st)) & 1u) row[i] = 0u;
+    }
+}
+
 // bp_fixed >= 0: that binary point.  bp_fixed < 0: the block binary point of
 // the call in progress; this is its finishing launch.
 __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_fixed, int target,
@@ -367,6 +417,25 @@ hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int tar
 
 hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
                           hipStream_t s) {
+    if (n > 0 && n % 4 == 0 && splits >= 1 && splits <= 8) {
+        const int g = grid_for(n / 4, 1, 2048);
+#define NITI_FLAT(NZ)                                                                                             \
+    case NZ:                                                                                                      \
+        hipLaunchKernelGGL(reduce_max_flat_kernel<NZ>, dim3(g), dim3(256), 0, s, part, g32, n, st);               \
+        break;
+        switch (splits) {
+            NITI_FLAT(1)
+            NITI_FLAT(2)
+            NITI_FLAT(3)
+            NITI_FLAT(4)
+            NITI_FLAT(5)
+            NITI_FLAT(6)
+            NITI_FLAT(7)
+            NITI_FLAT(8)
+        }
+#undef NITI_FLAT
+        return hipGetLastError();
+    }
     const int64_t blocks = (n + 255) / 256;
     hipLaunchKernelGGL(reduce_max_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(256), 0, s, part, splits,
                        g32, n, st);
@@ -444,6 +513,14 @@ hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int6
     hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)(n * hp)), dim3(kThreads), 0, s, (const uint32_t*)x,
                        (uint32_t*)xp, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)wp, (int32_t)ph,
                        (int32_t)pw);
+    return hipGetLastError();
+}
+
+hipError_t zero_classes_run(int8_t* out, int64_t n, int64_t h, int64_t w, int64_t c, int st, uint32_t mask,
+                            hipStream_t s) {
+    if (mask == 0 || n * h * w * c == 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_classes_kernel, dim3((uint32_t)(n * h)), dim3(kThreads), 0, s, (uint32_t*)out,
+                       (int32_t)h, (int32_t)w, (int32_t)(c / 4), st, mask);
     return hipGetLastError();
 }
 

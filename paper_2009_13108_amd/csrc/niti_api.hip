@@ -332,6 +332,7 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
     DgradClass cls[kMaxProblems];
     IgemmBatch b{};
     int ncls = 0;
+    uint32_t zero_mask = 0;  // classes without taps: exact zeros, written apart
     int64_t off = 0;
     for (int a = 0; a < st; a++) {
         for (int bb = 0; bb < st; bb++) {
@@ -346,6 +347,10 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
             const int64_t wc = bb < d->w ? (d->w - bb + st - 1) / st : 0;
             ncls++;
             if (hc == 0 || wc == 0) continue;
+            if (c.T == 0 || c.U == 0) {
+                zero_mask |= 1u << (a * st + bb);
+                continue;
+            }
             IgemmProblem& p = b.p[b.nprob++];
             const int da = (a + d->pad_h - c.r0) / st;
             const int db = (bb + d->pad_w - c.s0) / st;
@@ -378,6 +383,16 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
     }
     hipError_t e = repack_dgrad_run(w, (int8_t*)ws, cls, ncls, K, R, S, C, st, st, as_stream(stream));
     if (e != hipSuccess) return NITI_ERR_HIP;
+    e = zero_classes_run(dx, d->n, d->h, d->w, d->c, st, zero_mask, as_stream(stream));
+    if (e != hipSuccess) return NITI_ERR_HIP;
+    if (b.nprob == 0) {
+        // No class has taps (a 1x1 filter that only ever sees padding): dx is
+        // all zeros and the call's maximum is 0.
+        e = max_abs_i32(nullptr, 0, stats, as_stream(stream));
+        if (e != hipSuccess) return NITI_ERR_HIP;
+        return hip_status(round_i32_run(nullptr, nullptr, 0, -1, 7, mode, stats, ExpArgs{nullptr, nullptr, nullptr},
+                                        as_stream(stream)));
+    }
     IgemmCtl ctl{};
     ctl.stats = stats;
     ctl.ex = ExpArgs{nullptr, nullptr, nullptr};

@@ -106,6 +106,10 @@ hipError_t maxpool_fwd_run(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, 
 hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
                            int64_t w, int64_t c, hipStream_t s);
 hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s);
+// Zero the pixels of out (NHWC, c % 4 == 0) whose sub-pixel class
+// (y % st, x % st) has bit (y % st) * st + x % st set in mask.
+hipError_t zero_classes_run(int8_t* out, int64_t n, int64_t h, int64_t w, int64_t c, int st, uint32_t mask,
+                            hipStream_t s);
 // Zero-padded copy of an NHWC image (C % 4 == 0): xp[n][Hp][Wp][C] with the
 // input at rows ph.., columns pw..; everything else zero.
 hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
