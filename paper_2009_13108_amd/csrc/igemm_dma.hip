@@ -369,7 +369,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_main(IgemmBatch b
     const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
     uint64_t tmax = 0;
     dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, hint >= 0, 1, tmax);
-    block_publish_max(st, slot, tmax);
+    // The ring is drained and the tile stored: its first bytes serve the
+    // reduction (no static LDS, so two 80 KiB workgroups fit one CU).
+    block_publish_max_in(st, slot, tmax, (uint64_t*)dyn_lds);
 }
 
 template <int BM, int BN, int NS, int WGM, int WGN, int MODE>

@@ -171,9 +171,9 @@ __device__ __forceinline__ void publish_max(niti_stats* st, int slot, uint64_t m
     if (m > load_acc(st, slot)) atomicMax((unsigned long long*)&st->acc_max[slot], (unsigned long long)m);
 }
 
-// Workgroup-wide maximum folded in by one thread.  Every thread calls it.
-__device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint64_t m) {
-    __shared__ uint64_t red[16];
+// Workgroup-wide maximum folded in by one thread.  Every thread calls it;
+// red is LDS scratch for one value per wave.
+__device__ __forceinline__ void block_publish_max_in(niti_stats* st, int slot, uint64_t m, uint64_t* red) {
     m = wave_max_u64(m);
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     if (lane == 0) red[wv] = m;
@@ -184,6 +184,11 @@ __device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint
         for (int i = 0; i < nw; i++) r = red[i] > r ? red[i] : r;
         if (r) publish_max(st, slot, r);
     }
+}
+
+__device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint64_t m) {
+    __shared__ uint64_t red[16];
+    block_publish_max_in(st, slot, m, red);
 }
 
 // In the accumulating launch: workgroup 0 records the slot and the guess
