@@ -57,6 +57,9 @@ struct Cfg {
     static constexpr int BLOCKS = (BM + BN) / 16;           // 1 KiB blocks per stage
     static constexpr int IPW = BLOCKS / NWAVES;             // load instructions per wave per stage
     static constexpr int ABLK = BN / 16;                    // blocks holding weight rows
+    static constexpr int IPW_W = ABLK / NWAVES;             // of which weight blocks
+    static constexpr int IPW_A = IPW - IPW_W;               // and activation blocks
+    static_assert(ABLK % NWAVES == 0 && (BLOCKS - ABLK) % NWAVES == 0, "blocks split evenly over waves");
     static constexpr int STAGE_BYTES = (BM + BN) * KSTEP;
     static constexpr int LDS_BYTES = NS * STAGE_BYTES;
     static constexpr int WGM_ = WGM, BN_ = BN;
@@ -125,18 +128,24 @@ template <typename T, int BM, int BN>
 __device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn, const int8_t* lds) {
     constexpr int PITCH = BN + 16;
     constexpr int PPR = BN / 16;  // pieces per row
+    const bool dense = P.os == 1 && P.OHc == P.OH && P.OWc == P.OW;
     for (int idx = threadIdx.x; idx < BM * PPR; idx += T::NT) {
         const int row = idx / PPR, pc = idx - row * PPR;
         const int m = tm * BM + row;
         const int n0 = tn * BN + pc * 16;
         if (m >= P.M || n0 >= P.Nout) continue;
-        const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
-        const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
-        const uint32_t i0 = fdiv(rem, P.div_ow);
-        const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
-        const int oh = (int)i0 * P.os + P.oa;
-        const int ow = (int)j0 * P.os + P.ob;
-        const int64_t ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo + n0;
+        int64_t ooff;
+        if (dense) {
+            ooff = (int64_t)m * P.ldo + n0;   // the output grid is the pixel grid
+        } else {
+            const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
+            const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
+            const uint32_t i0 = fdiv(rem, P.div_ow);
+            const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
+            const int oh = (int)i0 * P.os + P.oa;
+            const int ow = (int)j0 * P.os + P.ob;
+            ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo + n0;
+        }
         uint4 v = *(const uint4*)(lds + row * PITCH + pc * 16);
         const int nv = min(16, P.Nout - n0);
         int8_t* dst = P.out + ooff;
@@ -186,51 +195,49 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     const __amdgpu_buffer_rsrc_t wgt_rs =
         __builtin_amdgcn_make_buffer_rsrc((void*)P.wgt, 0, (int)P.wgt_bytes, 0x00020000);
 
-    // Per-lane row state for each load instruction.
+    // Per-lane row state for each load instruction: a wave issues IPW_W
+    // weight blocks and IPW_A activation blocks per stage; wb / ab is the
+    // lane's byte offset at K step 0 (kOOB for a row past the operand).
     const int lrow = lane >> 2;
     const uint32_t kpo = (uint32_t)(((lane & 3) ^ swz(lrow)) << 4);  // byte offset of this lane's chunk
-    uint32_t base[T::IPW];
-    int ih0[T::IPW], iw0[T::IPW];
+    uint32_t wb[T::IPW_W], ab[T::IPW_A];
+    uint32_t aux[T::IPW_A];   // kConv64: taps (bit r*S+s) outside the image; kWin: filter row of the piece
 #pragma unroll
-    for (int i = 0; i < T::IPW; i++) {
-        const int blk = wave * T::IPW + i;   // uniform
-        if (blk < T::ABLK) {
-            const int n = tn * BN + blk * 16 + lrow;
-            base[i] = n < P.Nout ? (uint32_t)n * (uint32_t)P.Ktot + kpo : kOOB;
-            ih0[i] = 0;
-            iw0[i] = 0;
+    for (int i = 0; i < T::IPW_W; i++) {
+        const int n = tn * BN + (wave * T::IPW_W + i) * 16 + lrow;
+        wb[i] = n < P.Nout ? (uint32_t)n * (uint32_t)P.Ktot + kpo : kOOB;
+    }
+#pragma unroll
+    for (int i = 0; i < T::IPW_A; i++) {
+        const int m = tm * BM + (wave * T::IPW_A + i) * 16 + lrow;
+        aux[i] = 0;
+        if (MODE == kGemm) {
+            ab[i] = m < P.M ? (uint32_t)m * (uint32_t)P.C + kpo : kOOB;
         } else {
-            const int m = tm * BM + (blk - T::ABLK) * 16 + lrow;
-            if (MODE == kGemm) {
-                base[i] = m < P.M ? (uint32_t)m * (uint32_t)P.C + kpo : kOOB;
-                ih0[i] = 0;
-                iw0[i] = 0;
-            } else if (MODE == kWin) {
-                const uint32_t mm = m < P.M ? (uint32_t)m : 0u;
-                const uint32_t img = fdiv(mm, P.div_ohw);
-                const uint32_t rem = mm - img * (uint32_t)(P.OHc * P.OWc);
-                const uint32_t oh = fdiv(rem, P.div_ow);
-                const uint32_t ow = rem - oh * (uint32_t)P.OWc;
+            const uint32_t mm = m < P.M ? (uint32_t)m : 0u;
+            const uint32_t img = fdiv(mm, P.div_ohw);
+            const uint32_t rem = mm - img * (uint32_t)(P.OHc * P.OWc);
+            const uint32_t oh = fdiv(rem, P.div_ow);
+            const uint32_t ow = rem - oh * (uint32_t)P.OWc;
+            if (MODE == kWin) {
                 const int rr = (int)kpo / P.L;              // filter row of this piece within a step
                 const int j0 = (int)kpo - rr * P.L;
-                ih0[i] = rr;
-                iw0[i] = 0;
-                base[i] = m < P.M ? (uint32_t)(((img * (uint32_t)P.H + oh * (uint32_t)P.st + (uint32_t)rr) *
-                                                    (uint32_t)P.W + ow * (uint32_t)P.st) * (uint32_t)P.C) + (uint32_t)j0
-                                  : kOOB;
+                aux[i] = (uint32_t)rr;
+                ab[i] = m < P.M ? (uint32_t)(((img * (uint32_t)P.H + oh * (uint32_t)P.st + (uint32_t)rr) *
+                                                  (uint32_t)P.W + ow * (uint32_t)P.st) * (uint32_t)P.C) + (uint32_t)j0
+                                : kOOB;
             } else {
-                const bool ok = m < P.M;
-                const uint32_t mm = ok ? (uint32_t)m : 0u;
-                const uint32_t img = fdiv(mm, P.div_ohw);
-                const uint32_t rem = mm - img * (uint32_t)(P.OHc * P.OWc);
-                const uint32_t oh = fdiv(rem, P.div_ow);
-                const uint32_t ow = rem - oh * (uint32_t)P.OWc;
                 const int h0 = (int)oh * P.st + P.off_h;
                 const int w0 = (int)ow * P.st + P.off_w;
-                // an invalid row is pushed out of the image so every tap fails the check
-                ih0[i] = ok ? h0 : -(1 << 28);
-                iw0[i] = w0;
-                base[i] = (uint32_t)((int64_t)img * P.H * P.W * P.C + ((int64_t)h0 * P.W + w0) * P.C) + kpo;
+                ab[i] = (uint32_t)((int64_t)img * P.H * P.W * P.C + ((int64_t)h0 * P.W + w0) * P.C) + kpo;
+                // taps (r, s) whose input pixel lies outside the image (all of
+                // them for a row past M)
+                uint32_t rows = 0, cols = 0, valid = 0;
+                for (int r = 0; r < P.R; r++) rows |= (uint32_t)((unsigned)(h0 + r) < (unsigned)P.H) << r;
+                for (int c = 0; c < P.S; c++) cols |= (uint32_t)((unsigned)(w0 + c) < (unsigned)P.W) << c;
+                for (int r = 0; r < P.R; r++)
+                    if ((rows >> r) & 1u) valid |= cols << (r * P.S);
+                aux[i] = m < P.M ? ~valid : ~0u;
             }
         }
     }
@@ -239,36 +246,57 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     // Uniform position of the next stage to issue: K offset, tap (r, s), channel block.
     int next_kt = 0, tr = 0, ts = 0, tc = 0;
 
+    // The uniform part of an offset rides in the instruction's SGPR offset
+    // wherever the lane part is a fixed in-bounds position; every lane offset
+    // that is not kOOB stays inside its buffer by construction, and lanes
+    // whose piece is past K, past R or outside the image get kOOB.
     auto issue = [&]() {
         int8_t* st = lds + (next_kt % NS) * T::STAGE_BYTES;
-        const uint32_t kb = (uint32_t)next_kt * KSTEP;
-        const bool kin = next_kt < nk;
-        const uint32_t tap_off = MODE == kConv64 ? (uint32_t)((tr * P.W + ts) * P.C + tc) : kb;
+        int8_t* wst = st + wave * T::IPW_W * 1024;
+        int8_t* ast = st + (T::ABLK + wave * T::IPW_A) * 1024;
+        if (next_kt >= nk) {
+            // loads past the last K step keep the wait counts constant
 #pragma unroll
-        for (int i = 0; i < T::IPW; i++) {
-            const int blk = wave * T::IPW + i;   // uniform
-            uint32_t off;
-            if (blk < T::ABLK) {
-                off = (base[i] != kOOB && kb + kpo < (uint32_t)P.Ktot) ? base[i] + kb : kOOB;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
-            } else {
-                if (MODE == kGemm) {
-                    off = (base[i] != kOOB && kb + kpo < (uint32_t)P.Ktot) ? base[i] + kb : kOOB;
-                } else if (MODE == kWin) {
-                    const int rps = KSTEP / P.L;             // filter rows per step (uniform)
-                    const int r = next_kt * rps + ih0[i];
-                    off = (base[i] != kOOB && r < P.R) ? base[i] + (uint32_t)(next_kt * rps) * (uint32_t)(P.W * P.C)
-                                                      : kOOB;
-                } else {
-                    const bool ok = kin && (unsigned)(ih0[i] + tr) < (unsigned)P.H &&
-                                    (unsigned)(iw0[i] + ts) < (unsigned)P.W;
-                    off = ok ? base[i] + tap_off : kOOB;
-                }
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
-            }
+            for (int i = 0; i < T::IPW_W; i++)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)kOOB, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < T::IPW_A; i++)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)kOOB, 0, 0, 0);
+            next_kt++;
+            return;
         }
-        next_kt++;
-        if (MODE == kConv64) {
+        const uint32_t kb = (uint32_t)next_kt * KSTEP;
+        // kGemm: bytes of this K step inside the row (64 except on a partial last step)
+        const uint32_t klim = min((uint32_t)P.Ktot - kb, (uint32_t)KSTEP);
+#pragma unroll
+        for (int i = 0; i < T::IPW_W; i++) {
+            const uint32_t v = (MODE == kGemm && kpo >= klim) ? kOOB : wb[i];
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)v, (int)kb, 0, 0);
+        }
+        if (MODE == kGemm) {
+#pragma unroll
+            for (int i = 0; i < T::IPW_A; i++) {
+                const uint32_t v = kpo >= klim ? kOOB : ab[i];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, (int)kb, 0, 0);
+            }
+        } else if (MODE == kWin) {
+            const int rps = KSTEP / P.L;                      // filter rows per step (uniform)
+            const int rlim = P.R - next_kt * rps;             // pieces at row rr >= rlim are past R
+            const uint32_t soff = (uint32_t)(next_kt * rps) * (uint32_t)(P.W * P.C);
+#pragma unroll
+            for (int i = 0; i < T::IPW_A; i++) {
+                const uint32_t v = (int)aux[i] >= rlim ? kOOB : ab[i];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, (int)soff, 0, 0);
+            }
+        } else {
+            const uint32_t tap_off = (uint32_t)((tr * P.W + ts) * P.C + tc);
+            const int tap = tr * P.S + ts;
+#pragma unroll
+            for (int i = 0; i < T::IPW_A; i++) {
+                // bit 31 set for a tap outside the image: past any buffer size
+                const uint32_t v = (__builtin_amdgcn_ubfe(aux[i], tap, 1) << 31) | (ab[i] + tap_off);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, 0, 0, 0);
+            }
             tc += KSTEP;
             if (tc == P.C) {
                 tc = 0;
@@ -278,6 +306,7 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
                 }
             }
         }
+        next_kt++;
     };
 
     v16i acc[T::FN][T::FM];
@@ -471,7 +500,8 @@ bool igemm_dma_eligible(const IgemmBatch& b) {
                 p.off_h != 0 || p.off_w != 0)
                 return false;
         } else {
-            if (p.C % KSTEP != 0 || p.L != p.S * p.C || p.Lpad != p.L || p.Ktot != p.R * p.L) return false;
+            if (p.C % KSTEP != 0 || p.L != p.S * p.C || p.Lpad != p.L || p.Ktot != p.R * p.L || p.R * p.S > 32)
+                return false;
         }
     }
     return true;
