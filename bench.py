@@ -114,35 +114,31 @@ class ResNetStep:
         self.fam_calls["igemm"] += 2
         self.fam_calls["wgrad"] += 1
 
-    def step(self, timer=None):
+    def step(self):
         niti = self.niti
-        t = timer or (lambda fam, fn: fn())
         for L in self.layers:
             d = L["desc"]
             for c in range(L["count"]):
                 w = L["w"][c]
                 s0 = L["stats"] + 3 * c
-                t("igemm", lambda: niti.conv_fwd(d, L["x"], w, L["y"], self.stats, relu=True, stats_index=s0,
-                                                   ws=self.ws))
+                niti.conv_fwd(d, L["x"], w, L["y"], self.stats, relu=True, stats_index=s0, ws=self.ws)
                 if L["bwd_data"]:
-                    t("igemm", lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
-                                                          relu_src=L["x"], stats_index=s0 + 1))
-                t("wgrad", lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws,
-                                                        mu=self.mu, stats_index=s0 + 2))
+                    niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws, relu_src=L["x"],
+                                       stats_index=s0 + 1)
+                niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu, stats_index=s0 + 2)
         B = self.batch
         fin, fout = self.fc_desc.c, self.fc_desc.k
         s = self.fc_stats
-        t("igemm", lambda: niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc,
-                                         self.s_logits, 7, False, stats_index=s))
+        fd = self.fc_desc
+        niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc, self.s_logits, 7, False,
+                      stats_index=s)
         niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats, self.ws,
                               stats_index=s + 1)
-        fd = self.fc_desc
-        t("igemm", lambda: niti.conv_bwd_data(fd, self.err.view(B, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
-                                              self.dfeat.view(B, 1, 1, fin), self.stats, self.ws,
-                                              relu_src=self.feat.view(B, 1, 1, fin), stats_index=s + 2))
-        t("wgrad", lambda: niti.conv_bwd_weight(fd, self.feat.view(B, 1, 1, fin), self.err.view(B, 1, 1, fout),
-                                                self.wfc.view(fout, 1, 1, fin), self.stats, self.ws,
-                                                mu=self.mu, stats_index=s + 3))
+        niti.conv_bwd_data(fd, self.err.view(B, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
+                           self.dfeat.view(B, 1, 1, fin), self.stats, self.ws,
+                           relu_src=self.feat.view(B, 1, 1, fin), stats_index=s + 2)
+        niti.conv_bwd_weight(fd, self.feat.view(B, 1, 1, fin), self.err.view(B, 1, 1, fout),
+                             self.wfc.view(fout, 1, 1, fin), self.stats, self.ws, mu=self.mu, stats_index=s + 3)
 
     def misses(self):
         st = self.niti.read_stats(self.stats)
@@ -163,26 +159,6 @@ class ResNetStep:
             if m:
                 out["fc/%s" % name] = m
         return out
-
-
-class EventTimer:
-    """HIP events around each call of a kernel family, on the stream the
-    library launches on (torch's current stream)."""
-
-    def __init__(self):
-        self.pairs = {"igemm": [], "wgrad": []}
-
-    def __call__(self, fam, fn):
-        import torch
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record()
-        fn()
-        b.record()
-        self.pairs[fam].append((a, b))
-
-    def totals_ms(self):
-        return {f: sum(a.elapsed_time(b) for a, b in p) for f, p in self.pairs.items()}
 
 
 # ----------------------------------------------------------------------------
@@ -266,21 +242,35 @@ def main():
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
+    h0 = time.perf_counter()
     for _ in range(args.steps):
         job.step()
+    host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
     m1, c1 = job.misses()
 
-    # roofline: the same steps again with events around every contraction call
-    timer = EventTimer()
-    for _ in range(args.steps):
-        job.step(timer)
+    # roofline: the same steps again, with the library's own HIP events
+    # recorded on the launch stream around every contraction launch.  A spin
+    # kernel first lets the host queue run ahead, so that no event waits on
+    # the host.
     torch.cuda.synchronize()
-    tot = timer.totals_ms()
-    fam = max(tot, key=lambda f: tot[f])
-    per_call_ms = tot[fam] / (args.steps * job.fam_calls[fam])
+    try:
+        torch.cuda._sleep(int(0.05 * 2.4e9))
+    except Exception:
+        pass
+    niti = job.niti
+    niti.timing_enable(True)
+    for _ in range(args.steps):
+        job.step()
+    niti.timing_enable(False)
+    torch.cuda.synchronize()
+    fams = {"igemm": niti.timing_read(niti.TIMING_IGEMM), "wgrad": niti.timing_read(niti.TIMING_WGRAD)}
+    for f, (_, n) in fams.items():
+        assert n == args.steps * job.fam_calls[f], (f, n)
+    fam = max(fams, key=lambda f: fams[f][0])
+    per_call_ms = fams[fam][0] / fams[fam][1]
     ops_per_call = job.fam_ops[fam] / job.fam_calls[fam]
     achieved = ops_per_call / (per_call_ms * 1e-3) / 1e12
     value = job.ops_per_step / (ms * 1e-3) / 1e12
@@ -301,6 +291,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "host_enqueue_ms_per_step": round(host_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -317,7 +308,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": fam, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                      "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": None,
                      "per_call_ms": round(per_call_ms, 5), "calls_per_step": job.fam_calls[fam],
-                     "family_ms_per_step": {f: round(v / args.steps, 4) for f, v in tot.items()}},
+                     "family_ms_per_step": {f: round(v[0] / args.steps, 4) for f, v in fams.items()},
+                     "family_tops": {f: round(job.fam_ops[f] * args.steps / (v[0] * 1e-3) / 1e12, 2)
+                                     for f, v in fams.items()}},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -226,6 +226,22 @@ niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
 /* Size of niti_stats (128), for bindings. */
 size_t niti_stats_bytes(void);
 
+/* ---- Kernel timing (a profiling aid; no effect on results) ----
+ * While enabled, every call records a HIP event pair on its own stream
+ * around its contraction launches: family NITI_TIMING_IGEMM brackets the
+ * implicit-GEMM kernel and its finishing launch (niti_gemm_fwd,
+ * niti_conv_fwd, niti_conv_bwd_data), NITI_TIMING_WGRAD the weight-gradient
+ * contraction kernel of niti_conv_bwd_weight (not its sum, maximum and
+ * update passes).  niti_timing_enable(1) clears the record and starts,
+ * niti_timing_enable(0) stops.  niti_timing_read waits for the recorded
+ * events and returns the summed milliseconds and the number of calls of a
+ * family.  The record is process-wide and not guarded against calls from
+ * several host threads at once.  Returns NITI_ERR_ARG for an unknown
+ * family, NITI_ERR_HIP if an event fails. */
+enum { NITI_TIMING_IGEMM = 0, NITI_TIMING_WGRAD = 1 };
+niti_status niti_timing_enable(int on);
+niti_status niti_timing_read(int family, double *ms, int64_t *calls);
+
 #ifdef __cplusplus
 }
 #endif

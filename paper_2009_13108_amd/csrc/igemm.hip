@@ -356,7 +356,9 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
 
 }  // namespace
 
-hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+namespace {
+
+hipError_t igemm_dispatch(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     if (igemm_dma_eligible(b)) return igemm_dma_run(b, ctl, stream);
     // All problems of a batch share the tile shape; pick it from the largest.
     int maxM = 0, maxN = 0;
@@ -367,6 +369,15 @@ hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     (void)maxM;
     if (maxN <= 64) return launch_igemm<256, 64>(b, ctl, stream);
     return launch_igemm<128, 128>(b, ctl, stream);
+}
+
+}  // namespace
+
+hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    const int t = timing_begin(NITI_TIMING_IGEMM, stream);
+    const hipError_t e = igemm_dispatch(b, ctl, stream);
+    timing_end(t, stream);
+    return e;
 }
 
 }  // namespace niti

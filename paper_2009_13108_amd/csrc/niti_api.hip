@@ -440,7 +440,9 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
         p.x = xpad;
     }
     p.part = part;
+    const int tix = timing_begin(NITI_TIMING_WGRAD, strm);
     e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
+    timing_end(tix, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;

@@ -46,6 +46,10 @@ struct IgemmCtl {
 };
 
 hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
+// Kernel timing hooks (timing.hip): begin returns a record index, or -1 when
+// timing is off; end closes that record on the same stream.
+int timing_begin(int family, hipStream_t s);
+void timing_end(int idx, hipStream_t s);
 bool igemm_dma_eligible(const IgemmBatch& b);
 hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 

@@ -83,8 +83,11 @@ EXPORTS = [
     "niti_gemm_fwd", "niti_conv_fwd", "niti_conv_bwd_data", "niti_conv_bwd_weight",
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
-    "niti_relu_mask", "niti_stats_bytes",
+    "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read",
 ]
+
+TIMING_IGEMM = 0
+TIMING_WGRAD = 1
 
 
 def lib():
@@ -108,6 +111,8 @@ def lib():
                 "niti_maxpool2_fwd": [P, P, P, I64, I64, I64, I64, P],
                 "niti_maxpool2_bwd": [P, P, P, I64, I64, I64, I64, P],
                 "niti_relu_mask": [P, P, I64, P],
+                "niti_timing_enable": [I],
+                "niti_timing_read": [I, P, P],
             }
             for name, args in sig.items():
                 f = getattr(L, name)
@@ -126,6 +131,19 @@ def lib():
 
 def status_str(s: int) -> str:
     return lib().niti_status_str(int(s)).decode()
+
+
+def timing_enable(on: bool):
+    """Start (clearing earlier records) or stop the library's kernel timing."""
+    _check(lib().niti_timing_enable(int(bool(on))), "niti_timing_enable")
+
+
+def timing_read(family: int):
+    """(summed milliseconds, calls) of a timing family; waits for its events."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(lib().niti_timing_read(int(family), ctypes.byref(ms), ctypes.byref(n)), "niti_timing_read")
+    return ms.value, n.value
 
 
 # ------------------------------------------------------------------ helpers
