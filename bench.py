@@ -209,6 +209,34 @@ def cpu_baseline(batch=2):
 
 
 # ----------------------------------------------------------------------------
+def summarize_kernel_trace(path):
+    """Per-kernel and per-family durations from a rocprofv3 kernel-trace CSV
+    (--kernel-trace --output-format csv), grouped the way the library's timing
+    hooks group them: igemm = implicit-GEMM kernels and their finishing
+    launches, wgrad = weight-gradient contraction kernels."""
+    import collections
+    import csv
+    import re
+
+    rows = list(csv.DictReader(open(path)))
+    per = collections.OrderedDict()
+    for r in rows:
+        name = re.sub(r"\(.*", "", r["Kernel_Name"].replace("(anonymous namespace)::", "")).replace("void ", "")
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        per.setdefault(name, []).append(dur)
+    print("%-58s %7s %11s %9s" % ("kernel", "calls", "total_us", "avg_us"))
+    for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        if "niti::" in name:
+            print("%-58s %7d %11.1f %9.2f" % (name[:58], len(v), sum(v), sum(v) / len(v)))
+    fam = {"igemm": (r"niti::igemm_(dma_)?(main|fixup)<", r"niti::igemm_(dma_)?main<"),
+           "wgrad": (r"niti::wgrad_(dma_)?kernel<", r"niti::wgrad_(dma_)?kernel<")}
+    for f, (member, counter) in fam.items():
+        tot = sum(sum(v) for n, v in per.items() if re.search(member, n))
+        calls = sum(len(v) for n, v in per.items() if re.search(counter, n))
+        if calls:
+            print("family %-6s calls %6d  total %11.1f us  per call %8.2f us" % (f, calls, tot, tot / calls))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,7 +246,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=64)
     ap.add_argument("--layers", action="store_true", help="per-layer timing table on stderr")
+    ap.add_argument("--kernel-trace", metavar="CSV",
+                    help="summarize a rocprofv3 kernel-trace CSV of a bench run and exit (no GPU)")
     args = ap.parse_args()
+    if args.kernel_trace:
+        summarize_kernel_trace(args.kernel_trace)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path; "
               "run with --gpus 1", file=sys.stderr)

@@ -32,6 +32,7 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
 // Accumulating launch of a call: the tensor maximum of x.
 __global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) {
     const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     uint64_t m = 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -39,7 +40,8 @@ __global__ void max_abs_i32_kernel(const int32_t* x, int64_t n, niti_stats* st) 
         const uint64_t a = mag32(x[i]);
         m = a > m ? a : m;
     }
-    block_publish_max(st, slot, m);
+    __shared__ uint32_t red[kThreads / 64];
+    block_publish_max32(st, slot, (uint32_t)m, red, snap);  // magnitudes <= 2^31
 }
 
 // Sum of the per-split partial weight gradients (exact mod 2^32) into g32,
@@ -52,6 +54,7 @@ __global__ __launch_bounds__(256) void reduce_max_kernel(const int32_t* part, in
                                                          int64_t n, niti_stats* st) {
     __shared__ uint4 sum4[4][64];
     const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int64_t i0 = (int64_t)blockIdx.x * 256 + 4 * lane;
@@ -103,7 +106,8 @@ __global__ __launch_bounds__(256) void reduce_max_kernel(const int32_t* part, in
             m = a > m ? a : m;
         }
     }
-    block_publish_max(st, slot, m);
+    __shared__ uint32_t red[kThreads / 64];
+    block_publish_max32(st, slot, (uint32_t)m, red, snap);  // magnitudes <= 2^31
 }
 
 // The same sum for few splits (NZ <= 8, n % 4 == 0): every lane owns four
@@ -114,6 +118,7 @@ template <int NZ>
 __global__ __launch_bounds__(256) void reduce_max_flat_kernel(const int32_t* part, int32_t* g32, int64_t n,
                                                               niti_stats* st) {
     const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     const int64_t nq = n >> 2;
     const int64_t step = (int64_t)gridDim.x * blockDim.x;
@@ -136,7 +141,8 @@ __global__ __launch_bounds__(256) void reduce_max_flat_kernel(const int32_t* par
         const uint64_t mq = max(m01, m23);
         m = mq > m ? mq : m;
     }
-    block_publish_max(st, slot, m);
+    __shared__ uint32_t red[kThreads / 64];
+    block_publish_max32(st, slot, (uint32_t)m, red, snap);  // magnitudes <= 2^31
 }
 
 // Rows of the strided back-propagation output that belong to sub-pixel
@@ -207,6 +213,7 @@ __device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
 __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
                             int64_t* e64, int64_t batch, int64_t classes, niti_stats* st) {
     const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63;
     const int64_t sample = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
@@ -258,7 +265,7 @@ __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const 
     }
     if (flag_sa && threadIdx.x == 0 && blockIdx.x == 0)
         atomicOr(&st->wflags[slot], NITI_FLAG_LOSS_SA);
-    block_publish_max(st, slot, m);
+    block_publish_max(st, slot, m, snap);
 }
 
 __global__ void loss_round_kernel(const int64_t* e64, int8_t* err, int64_t n, int mode, niti_stats* st) {
@@ -404,7 +411,7 @@ hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
 }
 
 hipError_t max_abs_i32(const int32_t* x, int64_t n, niti_stats* st, hipStream_t s) {
-    hipLaunchKernelGGL(max_abs_i32_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, x, n, st);
+    hipLaunchKernelGGL(max_abs_i32_kernel, dim3(grid_for(n, 8, 256)), dim3(kThreads), 0, s, x, n, st);
     return hipGetLastError();
 }
 
@@ -418,7 +425,9 @@ hipError_t round_i32_run(const int32_t* x, int8_t* y, int64_t n, int bp, int tar
 hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t n, niti_stats* st,
                           hipStream_t s) {
     if (n > 0 && n % 4 == 0 && splits >= 1 && splits <= 8) {
-        const int g = grid_for(n / 4, 1, 2048);
+        // At most one workgroup per CU: each folds its maximum in with one
+        // atomic, and atomics on the one address serialize.
+        const int g = grid_for(n / 4, 1, 256);
 #define NITI_FLAT(NZ)                                                                                             \
     case NZ:                                                                                                      \
         hipLaunchKernelGGL(reduce_max_flat_kernel<NZ>, dim3(g), dim3(256), 0, s, part, g32, n, st);               \

@@ -303,13 +303,15 @@ __global__ __launch_bounds__(NTHREADS) void igemm_main(IgemmBatch batch, IgemmCt
     __shared__ Smem<TBM, TBN> sm;
     niti_stats* st = ctl.stats;
     const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
     const int hint = st->bp_hint;
     begin_call(st, slot, hint);
     const Tile t = locate_tile(batch, blockIdx.x);
     const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
     uint64_t tmax = 0;
     run_tile<TBM, TBN>(batch.p[t.prob], t.tm, t.tn, sm, rk, ctl.relu, hint >= 0, 1, tmax);
-    block_publish_max(st, slot, tmax);
+    __shared__ uint32_t red[NTHREADS / 64];
+    block_publish_max32(st, slot, (uint32_t)tmax, red, snap);  // magnitudes <= 2^31
 }
 
 // Fix-up launch: the tensor maximum is final.  If the guessed shift was

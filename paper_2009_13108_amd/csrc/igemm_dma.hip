@@ -184,7 +184,8 @@ __device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn
 
 template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
 __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, int8_t* lds, const RoundK& rk,
-                                         int relu, int do_store, int do_max, uint64_t& tmax) {
+                                         int relu, int do_store, int do_max, uint64_t& tmax, niti_stats* snap_st,
+                                         int snap_slot, uint64_t& snap) {
     using T = Cfg<BM, BN, NS, WGM, WGN>;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -357,6 +358,10 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     // Drain the loads issued past the end before the ring is reused.
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
+    // Snapshot of the tensor maximum for the skip test of the publishing
+    // thread: read now, used after the epilogue, so its latency is hidden
+    // and it includes the workgroups that finished meanwhile.
+    if (snap_st && threadIdx.x == 0) snap = load_acc(snap_st, snap_slot);
 
     // Epilogue.  acc[a][b] element 4*jj + i is channel
     // wn*WTN + a*32 + 8*jj + 4*(lane/32) + i of tile pixel wm*WTM + b*32 + lane%32.
@@ -391,16 +396,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_main(IgemmBatch b
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
     const int slot = call_slot(st);
+    uint64_t snap = 0;
     const int hint = st->bp_hint;
     begin_call(st, slot, hint);
     int prob, tm, tn;
     locate(batch, blockIdx.x, prob, tm, tn);
     const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
     uint64_t tmax = 0;
-    dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, hint >= 0, 1, tmax);
+    dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, hint >= 0, 1, tmax, st, slot,
+                                         snap);
+    // Accumulator magnitudes are at most 2^31: 32-bit reductions are exact.
     // The ring is drained and the tile stored: its first bytes serve the
     // reduction (no static LDS, so two 80 KiB workgroups fit one CU).
-    block_publish_max_in(st, slot, tmax, (uint64_t*)dyn_lds);
+    block_publish_max32(st, slot, (uint32_t)tmax, (uint32_t*)dyn_lds, snap);
 }
 
 template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
@@ -415,8 +423,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_fixup(IgemmBatch 
         for (int t = blockIdx.x; t < batch.total_tiles; t += gridDim.x) {
             int prob, tm, tn;
             locate(batch, t, prob, tm, tn);
-            uint64_t dummy = 0;
-            dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, 1, 0, dummy);
+            uint64_t dummy = 0, nosnap = 0;
+            dma_tile<BM, BN, NS, WGM, WGN, MODE>(batch.p[prob], tm, tn, dyn_lds, rk, ctl.relu, 1, 0, dummy, nullptr, 0,
+                                                 nosnap);
         }
     }
     if (is_finisher()) finish_call(st, ctl.target, ctl.ex, ctl.static_flags, 1);

@@ -136,6 +136,20 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return v;
 }
 
+// Wave maximum of a 32-bit value with row-local DPP steps and four lane
+// reads; the result is uniform.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    return max(max(a, b), max(c, d));
+}
+
 __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
@@ -165,15 +179,22 @@ __device__ __forceinline__ uint64_t load_acc(niti_stats* st, int slot) {
     return __hip_atomic_load(&st->acc_max[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Fold a value into the tensor maximum.  The maximum only grows, so a value
-// not above one already observed can be skipped.
-__device__ __forceinline__ void publish_max(niti_stats* st, int slot, uint64_t m) {
-    if (m > load_acc(st, slot)) atomicMax((unsigned long long*)&st->acc_max[slot], (unsigned long long)m);
+// Snapshot of the tensor maximum taken when a workgroup starts (by thread 0,
+// the one that publishes).  The maximum only grows, so a workgroup maximum
+// not above the snapshot can be skipped without a fresh read at the end.
+__device__ __forceinline__ uint64_t max_snapshot(niti_stats* st, int slot) {
+    return threadIdx.x == 0 ? load_acc(st, slot) : 0ull;
 }
 
-// Workgroup-wide maximum folded in by one thread.  Every thread calls it;
-// red is LDS scratch for one value per wave.
-__device__ __forceinline__ void block_publish_max_in(niti_stats* st, int slot, uint64_t m, uint64_t* red) {
+// Fold a value into the tensor maximum (no-return atomic).
+__device__ __forceinline__ void publish_max(niti_stats* st, int slot, uint64_t m, uint64_t snap) {
+    if (m > snap) atomicMax((unsigned long long*)&st->acc_max[slot], (unsigned long long)m);
+}
+
+// Workgroup-wide maximum folded in by thread 0.  Every thread calls it;
+// red is LDS scratch for one value per wave; snap is max_snapshot().
+__device__ __forceinline__ void block_publish_max_in(niti_stats* st, int slot, uint64_t m, uint64_t* red,
+                                                     uint64_t snap) {
     m = wave_max_u64(m);
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     if (lane == 0) red[wv] = m;
@@ -182,13 +203,30 @@ __device__ __forceinline__ void block_publish_max_in(niti_stats* st, int slot, u
         const int nw = (blockDim.x + kWave - 1) / kWave;
         uint64_t r = 0;
         for (int i = 0; i < nw; i++) r = red[i] > r ? red[i] : r;
-        if (r) publish_max(st, slot, r);
+        publish_max(st, slot, r, snap);
     }
 }
 
-__device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint64_t m) {
+// Workgroup maximum of values below 2^32 (32-bit wave reductions), folded in
+// by thread 0 with one atomic; red is LDS scratch for one value per wave and
+// snap a snapshot held by thread 0.
+__device__ __forceinline__ void block_publish_max32(niti_stats* st, int slot, uint32_t m, uint32_t* red,
+                                                    uint64_t snap) {
+    m = wave_max_u32(m);
+    const int wv = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[wv] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int nw = (blockDim.x + kWave - 1) / kWave;
+        uint32_t r = 0;
+        for (int i = 0; i < nw; i++) r = max(r, red[i]);
+        publish_max(st, slot, r, snap);
+    }
+}
+
+__device__ __forceinline__ void block_publish_max(niti_stats* st, int slot, uint64_t m, uint64_t snap) {
     __shared__ uint64_t red[16];
-    block_publish_max_in(st, slot, m, red);
+    block_publish_max_in(st, slot, m, red, snap);
 }
 
 // In the accumulating launch: workgroup 0 records the slot and the guess
