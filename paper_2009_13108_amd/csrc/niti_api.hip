@@ -107,6 +107,7 @@ struct WgradSetup {
     WgradProblem p;
     WinPlan wp;
     bool win;
+    bool tap;  // the nine-tap kernel
     WgradPlan plan;
 };
 
@@ -153,7 +154,8 @@ WgradSetup wgrad_setup(const niti_conv_desc* d, int64_t P, int64_t Q) {
         p.Lw = 0;
         p.ncol_w = 0;
     }
-    r.plan = wgrad_plan(d->k, r.win ? p.ncol_w : p.ncol, npix);
+    r.tap = !r.win && wgrad_tap_eligible(p);
+    r.plan = r.tap ? wgrad_tap_plan(d->k, d->c, npix) : wgrad_plan(d->k, r.win ? p.ncol_w : p.ncol, npix);
     return r;
 }
 
@@ -441,7 +443,10 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     }
     p.part = part;
     const int tix = timing_begin(NITI_TIMING_WGRAD, strm);
-    e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
+    if (ws_.tap)
+        e = wgrad_tap_run(p, plan, strm);
+    else
+        e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
     timing_end(tix, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);

@@ -81,6 +81,11 @@ WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix);
 hipError_t wgrad_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
 bool wgrad_dma_eligible(const WgradProblem& p);
 hipError_t wgrad_dma_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
+// 3x3 filters, C and K multiples of 64: all nine taps of a channel chunk per
+// workgroup (wgrad_tap.hip).
+bool wgrad_tap_eligible(const WgradProblem& p);
+WgradPlan wgrad_tap_plan(int64_t K, int64_t C, int64_t npix);
+hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
 
 // Elementwise / reduction passes.
 hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);

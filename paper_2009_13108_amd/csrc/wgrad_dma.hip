@@ -83,16 +83,28 @@ __device__ __forceinline__ v4i tr_fragment(const int8_t* region, int p0, int cba
     return r;
 }
 
+// Workgroup order.  Workgroups go to the eight XCDs (each with its own L2)
+// in turn by linear index, so workgroup L runs on XCD L % 8.  The work items
+// (split, tile), tile fastest, are cut into eight equal consecutive runs, one
+// per XCD: the output tiles of one pixel range, which read the same input
+// pixels (shifted per tap) and the same errors, then mostly share an XCD and
+// meet in its L2, and every XCD gets the same amount of work.
 template <int TBK, int TBC, int NS>
-__global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P) {
+__global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P, int tiles_c, int tiles_k, int splits) {
     using T = WCfg<TBK, TBC, NS>;
     extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wk = wave & 1, wc = wave >> 1;
-    const int c0 = blockIdx.x * TBC;
-    const int k0 = blockIdx.y * TBK;
-    const int pbeg = blockIdx.z * P.chunk;
+    const int ntiles = tiles_c * tiles_k;
+    const int per_xcd = (ntiles * splits + 7) / 8;
+    const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if ((blockIdx.x >> 3) >= per_xcd || item >= ntiles * splits) return;
+    const int split = item / ntiles;
+    const int tile = item - split * ntiles;
+    const int c0 = (tile % tiles_c) * TBC;
+    const int k0 = (tile / tiles_c) * TBK;
+    const int pbeg = split * P.chunk;
     const int pend = min(P.npix, pbeg + P.chunk);
     const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
 
@@ -212,7 +224,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P) {
 
     // acc[a][b] element 4*jj + i: column c0 + wc*WTC + a*32 + 8*jj + 4*(lane/32) + i,
     // channel k0 + wk*WTK + b*32 + lane%32: four consecutive columns per store.
-    int32_t* out = P.part + (int64_t)blockIdx.z * P.K * P.ncol;
+    int32_t* out = P.part + (int64_t)split * P.K * P.ncol;
 #pragma unroll
     for (int b = 0; b < T::FK; b++) {
         const int k = k0 + wk * T::WTK + b * 32 + (lane & 31);
@@ -254,7 +266,9 @@ hipError_t launch(const WgradProblem& p, const WgradPlan& plan, hipStream_t stre
     }
     const int tc = ((p.win ? p.ncol_w : p.ncol) + TBC - 1) / TBC;
     const int tk = (p.K + TBK - 1) / TBK;
-    hipLaunchKernelGGL((wgrad_dma_kernel<TBK, TBC, NS>), dim3(tc, tk, plan.splits), dim3(256), T::LDS, stream, p);
+    const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
+    hipLaunchKernelGGL((wgrad_dma_kernel<TBK, TBC, NS>), dim3((unsigned)grid), dim3(256), T::LDS, stream, p, tc, tk,
+                       plan.splits);
     return hipGetLastError();
 }
 

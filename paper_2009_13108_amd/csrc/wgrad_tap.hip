@@ -1,0 +1,214 @@
+// Weight-gradient contraction for 3x3 convolutions with channel counts that
+// are multiples of 64 (Algorithm 1, g(l) = a(l-1) (x) e(l); Section 3.3):
+//
+//   g32[k][(r*3 + s)*C + c] = sum over pixels pix of dy[pix][k] * x[n][oh*sh - ph + r][ow*sw - pw + s][c]
+//
+// The nine taps of one 64-channel chunk read the same input pixels, shifted.
+// A workgroup therefore owns an output tile of 64 output channels x (all nine
+// taps of a 64-channel chunk) and, per stage of 64 output pixels, loads the
+// nine shifted 64-pixel x 64-byte slices and the 64 x 64-byte error slice.
+// The nine slices of one stage touch the same few input rows at nearly the
+// same time, so they meet in L2 instead of re-reading memory past it, which
+// is what bounds a kernel that tiles the im2col columns independently.
+//
+// Layout of a stage in LDS: nine x regions [64 pixels][64 bytes] (one per tap)
+// and one dy region [64 pixels][64 bytes], 16-byte chunks XOR-swizzled by
+// pixel; the MFMA operands come out of them with transpose reads (the same
+// fragment reader as wgrad_dma.hip).  Wave (wk, wc) of four computes output
+// channels k0 + 32*wk .. +31 x channels c0 + 32*wc .. +31 for all nine taps:
+// per 32 pixels one error fragment and nine input fragments feed nine MFMAs.
+//
+// Loads.  Wave w fills pixels 16w .. 16w+15 of every region of a stage (ten
+// direct-to-LDS loads of 1 KiB); a lane keeps the input offset of its pixel
+// and a 9-bit mask of the taps that fall outside the image, so each tap's
+// load is one add and one bit test.  Each workgroup stores its partial tile
+// to its own slice; the split-sum pass adds the slices.
+#include "niti_internal.h"
+
+namespace niti {
+
+namespace {
+
+constexpr int PIX = 64;                 // output pixels per stage
+constexpr int NTAP = 9;
+constexpr int REG = PIX * 64;           // bytes of one [64 pixels][64 bytes] region
+constexpr int STAGE = (NTAP + 1) * REG; // nine tap regions and the error region
+constexpr uint32_t kOOB = 0x80000000u;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v2i lds_v2i;
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Chunk swizzle of 64-byte pixel rows: conflict-free transpose reads over 8
+// consecutive pixels.
+__device__ __forceinline__ int swz(int pix) { return (pix >> 1) & 3; }
+
+// One 32 x 32-pixel fragment of a [pixel][64 bytes] region: the lane gets 16
+// pixel bytes (pixels p0 + 16*(lane/32) ...) of column cbase + lane%32.
+__device__ __forceinline__ v4i tr_frag(const int8_t* region, int p0, int cbase, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int chunk = (cbase >> 4) + (g & 1);
+    const int prow = p0 + 16 * (g >> 1) + (j >> 1);
+    const int half = (j & 1) * 8;
+    const int8_t* a0 = region + prow * 64 + ((chunk ^ swz(prow)) << 4) + half;
+    const int8_t* a1 = region + (prow + 8) * 64 + ((chunk ^ swz(prow + 8)) << 4) + half;
+    const v2i lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)a0);
+    const v2i hi = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)a1);
+    v4i r;
+    r[0] = lo[0];
+    r[1] = lo[1];
+    r[2] = hi[0];
+    r[3] = hi[1];
+    return r;
+}
+
+// Work items (split, tile), tile fastest, cut into eight equal consecutive
+// runs, one per XCD (workgroup L runs on XCD L % 8), so the tiles of one pixel
+// range share an XCD and its L2.
+template <int NS>
+__global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int tiles_c, int tiles_k, int splits) {
+    extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wk = wave & 1, wc = wave >> 1;
+    const int ntiles = tiles_c * tiles_k;
+    const int per_xcd = (ntiles * splits + 7) / 8;
+    const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if ((blockIdx.x >> 3) >= per_xcd || item >= ntiles * splits) return;
+    const int split = item / ntiles;
+    const int tile = item - split * ntiles;
+    const int c0 = (tile % tiles_c) * 64;
+    const int k0 = (tile / tiles_c) * 64;
+    const int pbeg = split * P.chunk;
+    const int pend = min(P.npix, pbeg + P.chunk);
+    const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
+
+    const __amdgpu_buffer_rsrc_t xrs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.x, 0, (int)P.x_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t drs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.dy, 0, (int)P.dy_bytes, 0x00020000);
+
+    // This lane's pixel row in every region and the chunk it fetches so that
+    // it lands in its fixed slot (lane l -> row l/4, slot l%4).
+    const int prow = 16 * wave + (lane >> 2);
+    const uint32_t cbyte = (uint32_t)((((lane & 3) ^ swz(prow))) << 4);
+    const uint32_t WC = (uint32_t)P.W * (uint32_t)P.C;
+
+    int next = 0;
+    auto issue = [&]() {
+        int8_t* st = lds + (next % NS) * STAGE + wave * 1024;
+        const int pix = pbeg + next * PIX + prow;
+        const bool ok = next < nsteps && pix < pend;
+        const uint32_t pp = ok ? (uint32_t)pix : 0u;
+        const uint32_t n = fdiv(pp, P.div_pq);
+        const uint32_t rem = pp - n * (uint32_t)(P.P * P.Q);
+        const uint32_t oh = fdiv(rem, P.div_q);
+        const uint32_t ow = rem - oh * (uint32_t)P.Q;
+        const int h0 = (int)oh * P.sh - P.ph;
+        const int w0 = (int)ow * P.sw - P.pw;
+        uint32_t rows = 0, cols = 0;
+#pragma unroll
+        for (int r = 0; r < 3; r++) rows |= (uint32_t)((unsigned)(h0 + r) < (unsigned)P.H) << r;
+#pragma unroll
+        for (int s = 0; s < 3; s++) cols |= (uint32_t)((unsigned)(w0 + s) < (unsigned)P.W) << s;
+        // bit r*3+s set: tap (r, s) outside the image (all taps for a pixel past the range)
+        uint32_t outside = ok ? ~((((rows & 1u) ? cols : 0u)) | (((rows & 2u) ? cols : 0u) << 3) |
+                                  (((rows & 4u) ? cols : 0u) << 6))
+                              : ~0u;
+        const uint32_t base = (uint32_t)(((int)n * P.H + h0) * P.W + w0) * (uint32_t)P.C + (uint32_t)c0 + cbyte;
+#pragma unroll
+        for (int t = 0; t < NTAP; t++) {
+            const uint32_t tap_off = (uint32_t)(t / 3) * WC + (uint32_t)(t % 3) * (uint32_t)P.C;
+            const uint32_t v = (__builtin_amdgcn_ubfe(outside, t, 1) << 31) | (base + tap_off);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(st + t * REG), 16, (int)v, 0, 0, 0);
+        }
+        const uint32_t dv = ok ? pp * (uint32_t)P.K + (uint32_t)k0 + cbyte : kOOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(drs, (lds_void*)(st + NTAP * REG), 16, (int)dv, 0, 0, 0);
+        next++;
+    };
+
+    v16i acc[NTAP];
+#pragma unroll
+    for (int t = 0; t < NTAP; t++)
+#pragma unroll
+        for (int e = 0; e < 16; e++) acc[t][e] = 0;
+
+#pragma unroll
+    for (int s = 0; s < NS - 1; s++) issue();
+    for (int it = 0; it < nsteps; it++) {
+        wait_vm<(NS - 2) * (NTAP + 1)>();
+        __builtin_amdgcn_s_barrier();
+        issue();
+        const int8_t* st = lds + (it % NS) * STAGE;
+#pragma unroll
+        for (int ks = 0; ks < 2; ks++) {
+            const v4i fd = tr_frag(st + NTAP * REG, 32 * ks, 32 * wk, lane);
+#pragma unroll
+            for (int t = 0; t < NTAP; t++) {
+                const v4i fx = tr_frag(st + t * REG, 32 * ks, 32 * wc, lane);
+                acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fx, fd, acc[t], 0, 0, 0);
+            }
+        }
+    }
+    wait_vm<0>();
+
+    // acc[t] element 4*jj + i: channel c0 + 32*wc + 8*jj + 4*(lane/32) + i of
+    // tap t, output channel k0 + 32*wk + lane%32: four consecutive columns per store.
+    int32_t* out = P.part + (int64_t)split * P.K * P.ncol + (int64_t)(k0 + 32 * wk + (lane & 31)) * P.ncol;
+#pragma unroll
+    for (int t = 0; t < NTAP; t++)
+#pragma unroll
+        for (int jj = 0; jj < 4; jj++) {
+            const int col = t * P.C + c0 + 32 * wc + 8 * jj + 4 * (lane >> 5);
+            *(int4*)(out + col) =
+                make_int4(acc[t][4 * jj], acc[t][4 * jj + 1], acc[t][4 * jj + 2], acc[t][4 * jj + 3]);
+        }
+}
+
+}  // namespace
+
+bool wgrad_tap_eligible(const WgradProblem& p) {
+    return !p.win && p.R == 3 && p.S == 3 && p.C % 64 == 0 && p.K % 64 == 0 && p.x_bytes > 0 &&
+           p.x_bytes < ((int64_t)1 << 31) && p.dy_bytes > 0 && p.dy_bytes < ((int64_t)1 << 31);
+}
+
+WgradPlan wgrad_tap_plan(int64_t K, int64_t C, int64_t npix) {
+    WgradPlan pl;
+    pl.tbk = 64;
+    const int64_t tiles = (K / 64) * (C / 64);
+    const int64_t steps = (npix + PIX - 1) / PIX;
+    // about one workgroup per CU, at least four stages each
+    int64_t splits = (256 + tiles - 1) / tiles;
+    const int64_t max_splits = steps / 4 > 1 ? steps / 4 : 1;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    const int64_t chunk_steps = (steps + splits - 1) / splits;
+    pl.chunk = (int32_t)(chunk_steps * PIX);
+    pl.splits = (int32_t)((steps + chunk_steps - 1) / chunk_steps);
+    if (pl.splits < 1) pl.splits = 1;
+    return pl;
+}
+
+hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {
+    constexpr int NS = 3;
+    constexpr int LDS = NS * STAGE;
+    static bool attr_done = false;
+    if (!attr_done) {
+        hipError_t e = hipFuncSetAttribute((const void*)wgrad_tap_kernel<NS>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+        if (e != hipSuccess) return e;
+        attr_done = true;
+    }
+    p.chunk = plan.chunk;
+    const int tc = p.C / 64, tk = p.K / 64;
+    const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
+    hipLaunchKernelGGL((wgrad_tap_kernel<NS>), dim3((unsigned)grid), dim3(256), LDS, stream, p, tc, tk, plan.splits);
+    return hipGetLastError();
+}
+
+}  // namespace niti
