@@ -136,6 +136,41 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return v;
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS loads issued as inline assembly.  Kernels that read their
+// LDS ring with transpose reads use these: the compiler cannot tell which
+// ring stage a transpose read touches, so with the load builtin it waits for
+// every direct-to-LDS load in flight before each read, which serializes the
+// ring.  Issued this way the loads are invisible to its wait counting, and
+// the kernel's own per-stage vmcnt waits and barriers order them.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor (stride 0): base address and size in bytes; accesses
+// at offsets >= bytes return zeros.  Uniform.
+__device__ __forceinline__ u32x4 raw_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    u32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    r.y = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xFFFFu);
+    r.z = __builtin_amdgcn_readfirstlane(bytes);
+    r.w = 0x00020000u;
+    return r;
+}
+
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes per lane from offset voff + soff of the buffer to LDS address
+// m0 + 16 * lane (m0 uniform).
+__device__ __forceinline__ void lds_dma16(u32x4 rs, uint32_t m0, uint32_t voff, uint32_t soff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(m0)), "v"(voff), "s"(rs), "s"(soff)
+                 : "memory", "m0");
+}
+
 // Wave maximum of a 32-bit value with row-local DPP steps and four lane
 // reads; the result is uniform.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {

@@ -32,7 +32,6 @@ namespace {
 constexpr int PIX = 64;                 // pixels per stage
 constexpr uint32_t kOOB = 0x80000000u;
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v2i lds_v2i;
 
 template <int N>
@@ -108,10 +107,11 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P, int t
     const int pend = min(P.npix, pbeg + P.chunk);
     const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
 
-    const __amdgpu_buffer_rsrc_t xrs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.x, 0, (int)P.x_bytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t drs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.dy, 0, (int)P.dy_bytes, 0x00020000);
+    // Loads go out as inline assembly (lds_dma16): with the load builtin the
+    // compiler waits for the whole ring before every transpose read.
+    const u32x4 xrs = raw_rsrc(P.x, (uint32_t)P.x_bytes);
+    const u32x4 drs = raw_rsrc(P.dy, (uint32_t)P.dy_bytes);
+    const uint32_t lds0 = lds_address(lds);
 
     // Per load instruction: pixel row within the stage, and the column /
     // channel this lane's chunk covers (fixed over the reduction).
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P, int t
 
     int next = 0;
     auto issue = [&]() {
-        int8_t* st = lds + (next % NS) * T::STAGE;
+        const uint32_t st = lds0 + (uint32_t)((next % NS) * T::STAGE);
         const int pb = pbeg + next * PIX;
 #pragma unroll
         for (int i = 0; i < T::IPW; i++) {
@@ -181,10 +181,10 @@ __global__ __launch_bounds__(256, 1) void wgrad_dma_kernel(WgradProblem P, int t
                     if (P.win || ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W))
                         off = (uint32_t)(((n * P.H + ih) * P.W + iw) * P.C) + toff[i];
                 }
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
+                lds_dma16(xrs, st + blk * 1024, off, 0);
             } else {
                 if (pok) off = (uint32_t)pix * (uint32_t)P.K + toff[i];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(drs, (lds_void*)(st + blk * 1024), 16, (int)off, 0, 0, 0);
+                lds_dma16(drs, st + blk * 1024, off, 0);
             }
         }
         next++;

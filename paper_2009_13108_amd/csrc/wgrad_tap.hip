@@ -19,7 +19,9 @@
 // per 32 pixels one error fragment and nine input fragments feed nine MFMAs.
 //
 // Loads.  Wave w fills pixels 16w .. 16w+15 of every region of a stage (ten
-// direct-to-LDS loads of 1 KiB); a lane keeps the input offset of its pixel
+// direct-to-LDS loads of 1 KiB, issued as inline assembly so the compiler
+// does not wait for the whole ring before each transpose read); a lane keeps
+// the input offset of its pixel
 // and a 9-bit mask of the taps that fall outside the image, so each tap's
 // load is one add and one bit test.  Each workgroup stores its partial tile
 // to its own slice; the split-sum pass adds the slices.
@@ -35,7 +37,6 @@ constexpr int REG = PIX * 64;           // bytes of one [64 pixels][64 bytes] re
 constexpr int STAGE = (NTAP + 1) * REG; // nine tap regions and the error region
 constexpr uint32_t kOOB = 0x80000000u;
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v2i lds_v2i;
 
 template <int N>
@@ -48,17 +49,28 @@ __device__ __forceinline__ void wait_vm() {
 // consecutive pixels.
 __device__ __forceinline__ int swz(int pix) { return (pix >> 1) & 3; }
 
-// One 32 x 32-pixel fragment of a [pixel][64 bytes] region: the lane gets 16
-// pixel bytes (pixels p0 + 16*(lane/32) ...) of column cbase + lane%32.
-__device__ __forceinline__ v4i tr_frag(const int8_t* region, int p0, int cbase, int lane) {
+// Lane byte offsets, within a [pixel][64 bytes] region, of the two transpose
+// reads that give a 32 x 32-pixel fragment: the lane gets 16 pixel bytes
+// (pixels p0 + 16*(lane/32) ...) of column cbase + lane%32.  They depend on
+// the lane, p0 and cbase only, so a workgroup computes them once.
+struct FragOff {
+    int lo, hi;
+};
+
+__device__ __forceinline__ FragOff frag_off(int p0, int cbase, int lane) {
     const int g = lane >> 4, j = lane & 15;
     const int chunk = (cbase >> 4) + (g & 1);
     const int prow = p0 + 16 * (g >> 1) + (j >> 1);
     const int half = (j & 1) * 8;
-    const int8_t* a0 = region + prow * 64 + ((chunk ^ swz(prow)) << 4) + half;
-    const int8_t* a1 = region + (prow + 8) * 64 + ((chunk ^ swz(prow + 8)) << 4) + half;
-    const v2i lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)a0);
-    const v2i hi = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)a1);
+    FragOff f;
+    f.lo = prow * 64 + ((chunk ^ swz(prow)) << 4) + half;
+    f.hi = (prow + 8) * 64 + ((chunk ^ swz(prow + 8)) << 4) + half;
+    return f;
+}
+
+__device__ __forceinline__ v4i tr_frag(const int8_t* region, FragOff f) {
+    const v2i lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(region + f.lo));
+    const v2i hi = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(region + f.hi));
     v4i r;
     r[0] = lo[0];
     r[1] = lo[1];
@@ -88,10 +100,9 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     const int pend = min(P.npix, pbeg + P.chunk);
     const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
 
-    const __amdgpu_buffer_rsrc_t xrs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.x, 0, (int)P.x_bytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t drs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.dy, 0, (int)P.dy_bytes, 0x00020000);
+    const u32x4 xrs = raw_rsrc(P.x, (uint32_t)P.x_bytes);
+    const u32x4 drs = raw_rsrc(P.dy, (uint32_t)P.dy_bytes);
+    const uint32_t lds0 = lds_address(lds);
 
     // This lane's pixel row in every region and the chunk it fetches so that
     // it lands in its fixed slot (lane l -> row l/4, slot l%4).
@@ -101,7 +112,7 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
 
     int next = 0;
     auto issue = [&]() {
-        int8_t* st = lds + (next % NS) * STAGE + wave * 1024;
+        const uint32_t st = lds0 + (uint32_t)((next % NS) * STAGE + wave * 1024);
         const int pix = pbeg + next * PIX + prow;
         const bool ok = next < nsteps && pix < pend;
         const uint32_t pp = ok ? (uint32_t)pix : 0u;
@@ -125,12 +136,15 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
         for (int t = 0; t < NTAP; t++) {
             const uint32_t tap_off = (uint32_t)(t / 3) * WC + (uint32_t)(t % 3) * (uint32_t)P.C;
             const uint32_t v = (__builtin_amdgcn_ubfe(outside, t, 1) << 31) | (base + tap_off);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(xrs, (lds_void*)(st + t * REG), 16, (int)v, 0, 0, 0);
+            lds_dma16(xrs, st + t * REG, v, 0);
         }
         const uint32_t dv = ok ? pp * (uint32_t)P.K + (uint32_t)k0 + cbyte : kOOB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(drs, (lds_void*)(st + NTAP * REG), 16, (int)dv, 0, 0, 0);
+        lds_dma16(drs, st + NTAP * REG, dv, 0);
         next++;
     };
+
+    const FragOff fo_x[2] = {frag_off(0, 32 * wc, lane), frag_off(32, 32 * wc, lane)};
+    const FragOff fo_d[2] = {frag_off(0, 32 * wk, lane), frag_off(32, 32 * wk, lane)};
 
     v16i acc[NTAP];
 #pragma unroll
@@ -147,10 +161,10 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
         const int8_t* st = lds + (it % NS) * STAGE;
 #pragma unroll
         for (int ks = 0; ks < 2; ks++) {
-            const v4i fd = tr_frag(st + NTAP * REG, 32 * ks, 32 * wk, lane);
+            const v4i fd = tr_frag(st + NTAP * REG, fo_d[ks]);
 #pragma unroll
             for (int t = 0; t < NTAP; t++) {
-                const v4i fx = tr_frag(st + t * REG, 32 * ks, 32 * wc, lane);
+                const v4i fx = tr_frag(st + t * REG, fo_x[ks]);
                 acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fx, fd, acc[t], 0, 0, 0);
             }
         }
