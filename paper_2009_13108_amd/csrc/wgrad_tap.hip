@@ -68,14 +68,19 @@ __device__ __forceinline__ FragOff frag_off(int p0, int cbase, int lane) {
     return f;
 }
 
-__device__ __forceinline__ v4i tr_frag(const int8_t* region, FragOff f) {
-    const v2i lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(region + f.lo));
-    const v2i hi = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(region + f.hi));
+// Fragment of region `reg` (a compile-time region index, folded into the
+// instructions' offset field) from LDS byte addresses lo / hi of region 0.
+template <int REG_BYTES>
+__device__ __forceinline__ v4i tr_frag(uint32_t lo_addr, uint32_t hi_addr, int reg) {
+    const lds_v2i* lo = (const lds_v2i*)(uintptr_t)lo_addr;
+    const lds_v2i* hi = (const lds_v2i*)(uintptr_t)hi_addr;
+    const v2i a = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(lo + reg * (REG_BYTES / 8)));
+    const v2i b = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(hi + reg * (REG_BYTES / 8)));
     v4i r;
-    r[0] = lo[0];
-    r[1] = lo[1];
-    r[2] = hi[0];
-    r[3] = hi[1];
+    r[0] = a[0];
+    r[1] = a[1];
+    r[2] = b[0];
+    r[3] = b[1];
     return r;
 }
 
@@ -158,13 +163,13 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
         wait_vm<(NS - 2) * (NTAP + 1)>();
         __builtin_amdgcn_s_barrier();
         issue();
-        const int8_t* st = lds + (it % NS) * STAGE;
+        const uint32_t st = lds0 + (uint32_t)((it % NS) * STAGE);
 #pragma unroll
         for (int ks = 0; ks < 2; ks++) {
-            const v4i fd = tr_frag(st + NTAP * REG, fo_d[ks]);
+            const v4i fd = tr_frag<REG>(st + fo_d[ks].lo, st + fo_d[ks].hi, NTAP);
 #pragma unroll
             for (int t = 0; t < NTAP; t++) {
-                const v4i fx = tr_frag(st + t * REG, fo_x[ks]);
+                const v4i fx = tr_frag<REG>(st + fo_x[ks].lo, st + fo_x[ks].hi, t);
                 acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fx, fd, acc[t], 0, 0, 0);
             }
         }
