@@ -479,10 +479,8 @@ hipError_t run_mode(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     }
     // The largest tile that still gives most compute units a workgroup.
     if (maxN <= 64) return launch_dma<256, 64, 4, 4, 1, MODE>(b, ctl, stream);
-    if (maxN <= 128) {
-        if (work >= (int64_t)200 * 256 * 128) return launch_dma<256, 128, 4, 2, 2, MODE>(b, ctl, stream);
-        return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
-    }
+    // 128 x 128 fits two workgroups per CU (256 x 128 fits one, by registers).
+    if (maxN <= 128) return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
     if (work >= (int64_t)200 * 256 * 256) return launch_dma<256, 256, 3, 2, 4, MODE>(b, ctl, stream);
     if (work >= (int64_t)200 * 256 * 128) return launch_dma<256, 128, 4, 2, 2, MODE>(b, ctl, stream);
     return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
