@@ -107,6 +107,19 @@ class ResNetStep:
         self.fam_ops["igemm"] += 2 * 2 * self.fc_macs
         self.fam_ops["wgrad"] += 2 * self.fc_macs
         self.ops_per_step = self.fam_ops["igemm"] + self.fam_ops["wgrad"]
+        # algorithmic bytes (operands, output, mask) per step, per family
+        self.fam_bytes = {"igemm": 0, "wgrad": 0}
+        for L in self.layers:
+            d = L["desc"]
+            xb = d.n * d.h * d.w * d.c
+            yb = d.n * d.p * d.q * d.k
+            wb = d.k * d.r * d.s * d.c
+            self.fam_bytes["igemm"] += L["count"] * (xb + wb + yb)                              # x, w -> y
+            if L["bwd_data"]:
+                self.fam_bytes["igemm"] += L["count"] * (yb + wb + xb + xb)                     # dy, w, mask -> dx
+            self.fam_bytes["wgrad"] += L["count"] * (xb + yb + 4 * wb)                         # x, dy -> g32
+        self.fam_bytes["igemm"] += 2 * (batch * fin + fout * fin + batch * fout) + batch * fin  # head fwd, bwd
+        self.fam_bytes["wgrad"] += batch * fin + batch * fout + 4 * fin * fout
         self.fam_calls = {"igemm": 0, "wgrad": 0}
         for L in self.layers:
             self.fam_calls["igemm"] += L["count"] * (2 if L["bwd_data"] else 1)
@@ -209,6 +222,38 @@ def cpu_baseline(batch=2):
 
 
 # ----------------------------------------------------------------------------
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "resnet18_b128_traffic.md")
+
+
+def kernel_sources_digest():
+    """sha256 over the library's kernel sources (name and bytes, sorted)."""
+    import glob
+    import hashlib
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2009_13108_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(family):
+    """HBM bytes per call of a family from the committed counter summary, or
+    None when the kernel sources changed since the counters were taken."""
+    try:
+        vals = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                vals[k.strip()] = v.strip()
+        if vals.get("kernel_sources_sha256") != kernel_sources_digest():
+            return None
+        return int(vals["%s_hbm_bytes_per_call" % family])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def summarize_kernel_trace(path):
     """Per-kernel and per-family durations from a rocprofv3 kernel-trace CSV
     (--kernel-trace --output-format csv), grouped the way the library's timing
@@ -229,12 +274,53 @@ def summarize_kernel_trace(path):
         if "niti::" in name:
             print("%-58s %7d %11.1f %9.2f" % (name[:58], len(v), sum(v), sum(v) / len(v)))
     fam = {"igemm": (r"niti::igemm_(dma_)?(main|fixup)<", r"niti::igemm_(dma_)?main<"),
-           "wgrad": (r"niti::wgrad_(dma_)?kernel<", r"niti::wgrad_(dma_)?kernel<")}
+           "wgrad": (r"niti::wgrad_\w*kernel<", r"niti::wgrad_\w*kernel<")}
     for f, (member, counter) in fam.items():
         tot = sum(sum(v) for n, v in per.items() if re.search(member, n))
         calls = sum(len(v) for n, v in per.items() if re.search(counter, n))
         if calls:
             print("family %-6s calls %6d  total %11.1f us  per call %8.2f us" % (f, calls, tot, tot / calls))
+
+
+def summarize_counters(path):
+    """Per-family sums of a rocprofv3 --pmc counter CSV (one counter per run,
+    e.g. FETCH_SIZE or WRITE_SIZE in KiB per dispatch): total over the
+    family's kernels divided by its calls, plus the calibration copy."""
+    import collections
+    import csv
+    import re
+
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    disp = collections.defaultdict(set)
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"]
+        per[r["Counter_Name"]][name] += float(r["Counter_Value"])
+        disp[name].add(r["Dispatch_Id"])
+    calls = {n: len(d) for n, d in disp.items()}
+    fam = {"igemm": (r"niti::\(anonymous namespace\)::igemm_(dma_)?(main|fixup)<", r"igemm_(dma_)?main<"),
+           "wgrad": (r"niti::\(anonymous namespace\)::wgrad_\w*kernel<", r"wgrad_\w*kernel<")}
+    for cname, vals in per.items():
+        for f, (member, counter) in fam.items():
+            tot = sum(v for n, v in vals.items() if re.search(member, n))
+            n = sum(c for k, c in calls.items() if re.search(counter, k))
+            if n:
+                print("%s family %-6s calls %6d  per call %12.1f KiB" % (cname, f, n, tot / n))
+        cp = [(n, v) for n, v in vals.items() if "copy" in n.lower() or "elementwise" in n.lower()]
+        for n, v in cp:
+            print("%s copy-like kernel %s... calls %d per call %.1f KiB" % (cname, n[:60], calls[n], v / max(1, calls[n])))
+
+
+def copy_calibration(nbytes):
+    """A plain device copy of nbytes (torch's copy kernel), five times: the
+    reference for scaling FETCH_SIZE / WRITE_SIZE to bytes."""
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print("copied %d bytes x5" % nbytes, flush=True)
 
 
 def main():
@@ -248,9 +334,19 @@ def main():
     ap.add_argument("--layers", action="store_true", help="per-layer timing table on stderr")
     ap.add_argument("--kernel-trace", metavar="CSV",
                     help="summarize a rocprofv3 kernel-trace CSV of a bench run and exit (no GPU)")
+    ap.add_argument("--counters", metavar="CSV",
+                    help="summarize a rocprofv3 --pmc counter CSV per kernel family and exit (no GPU)")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="run only a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
     if args.kernel_trace:
         summarize_kernel_trace(args.kernel_trace)
+        return
+    if args.counters:
+        summarize_counters(args.counters)
+        return
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path; "
@@ -339,7 +435,10 @@ def main():
         "ops_per_step": job.ops_per_step,
         "hint": {"misses_timed": m1 - m0, "calls_timed": c1 - c0, "misses_by_call": job.miss_table()},
         "roofline": {"bound": "mfma", "kernel": fam, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
-                     "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4), "traffic": None,
+                     "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4),
+                     "traffic": measured_traffic(fam),
+                     "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "algorithmic_bytes_per_call": job.fam_bytes[fam] // job.fam_calls[fam],
                      "per_call_ms": round(per_call_ms, 5), "calls_per_step": job.fam_calls[fam],
                      "family_ms_per_step": {f: round(v[0] / args.steps, 4) for f, v in fams.items()},
                      "family_tops": {f: round(job.fam_ops[f] * args.steps / (v[0] * 1e-3) / 1e12, 2)
