@@ -145,6 +145,68 @@ __global__ __launch_bounds__(256) void reduce_max_flat_kernel(const int32_t* par
     block_publish_max32(st, slot, (uint32_t)m, red, snap);  // magnitudes <= 2^31
 }
 
+// The same sum for many splits (n % 4 == 0).  A workgroup takes 256
+// consecutive elements at a time: each wave reads them as one 1 KiB row piece
+// per split (lane l holds elements 4l .. 4l+3), wave w adds splits w, w + 4,
+// ... with eight 16-byte loads in flight, and the four wave sums are added in
+// LDS.  At most one workgroup per CU strides over the tensor, so one atomic
+// per CU folds the maximum in.
+__global__ __launch_bounds__(256) void reduce_max_many_kernel(const int32_t* part, int splits, int32_t* g32,
+                                                              int64_t n, niti_stats* st) {
+    __shared__ uint4 sums[4][64];
+    __shared__ uint32_t red[4];
+    const int slot = call_slot(st);
+    const uint64_t snap = max_snapshot(st, slot);
+    begin_call(st, slot, -1);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    uint32_t m = 0;
+    for (int64_t i0 = (int64_t)blockIdx.x * 256; i0 < n; i0 += (int64_t)gridDim.x * 256) {
+        const int64_t i = i0 + 4 * lane;
+        uint4 a = make_uint4(0, 0, 0, 0);
+        if (i < n) {
+            const int32_t* src = part + i;
+            int z = wv;
+            for (; z + 28 < splits; z += 32) {
+                uint4 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; u++) v[u] = *(const uint4*)(src + (int64_t)(z + 4 * u) * n);
+#pragma unroll
+                for (int u = 0; u < 8; u++) {
+                    a.x += v[u].x;
+                    a.y += v[u].y;
+                    a.z += v[u].z;
+                    a.w += v[u].w;
+                }
+            }
+            for (; z < splits; z += 4) {
+                const uint4 v = *(const uint4*)(src + (int64_t)z * n);
+                a.x += v.x;
+                a.y += v.y;
+                a.z += v.z;
+                a.w += v.w;
+            }
+        }
+        sums[wv][lane] = a;
+        __syncthreads();
+        if (wv == 0 && i < n) {
+#pragma unroll
+            for (int h = 1; h < 4; h++) {
+                const uint4 v = sums[h][lane];
+                a.x += v.x;
+                a.y += v.y;
+                a.z += v.z;
+                a.w += v.w;
+            }
+            *(uint4*)(g32 + i) = a;
+            const uint32_t mq =
+                max(max(mag32((int32_t)a.x), mag32((int32_t)a.y)), max(mag32((int32_t)a.z), mag32((int32_t)a.w)));
+            m = max(m, mq);
+        }
+        __syncthreads();   // sums is rewritten by the next pass
+    }
+    block_publish_max32(st, slot, m, red, snap);  // magnitudes <= 2^31
+}
+
 // Rows of the strided back-propagation output that belong to sub-pixel
 // classes with no filter taps are exact zeros: out[img][y][x][:] = 0 for every
 // (y % st, x % st) whose bit (y % st) * st + x % st is set in mask.  One
@@ -443,6 +505,12 @@ hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t
             NITI_FLAT(8)
         }
 #undef NITI_FLAT
+        return hipGetLastError();
+    }
+    if (n > 0 && n % 4 == 0 && splits > 8) {
+        int64_t blocks = (n + 255) / 256;
+        if (blocks > 256) blocks = 256;
+        hipLaunchKernelGGL(reduce_max_many_kernel, dim3((unsigned)blocks), dim3(256), 0, s, part, splits, g32, n, st);
         return hipGetLastError();
     }
     const int64_t blocks = (n + 255) / 256;
