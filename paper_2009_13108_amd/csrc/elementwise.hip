@@ -349,24 +349,63 @@ struct DgradClasses {
     int n;
 };
 
-__global__ void repack_dgrad_kernel(const int8_t* w, int8_t* out, DgradClasses cl, int K, int R, int S,
-                                    int C, int sh, int sw, int64_t total) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += stride) {
-        int ci = 0;
-        for (int i = 1; i < cl.n; i++)
-            if (idx >= cl.c[i].offset) ci = i;
-        const DgradClass& d = cl.c[ci];
-        int64_t o = idx - d.offset;  // within class: [c][t][u][k]
-        const int k = (int)(o % K);
-        o /= K;
-        const int u = (int)(o % d.U);
-        o /= d.U;
-        const int t = (int)(o % d.T);
-        const int c = (int)(o / d.T);
-        const int r = d.r0 + sh * (d.T - 1 - t);
-        const int s = d.s0 + sw * (d.U - 1 - u);
-        out[idx] = w[(((int64_t)k * R + r) * S + s) * C + c];
+
+// Tiled form: one workgroup per (tap of a class, 64-channel block c0,
+// 64-filter block k0).  The [64 k][64 c] slice of w at that tap is staged in
+// LDS (row pitch 68 bytes, so column reads spread over banks) and written
+// transposed as 64-byte runs out[c][t][u][k0 .. k0+63].
+__global__ __launch_bounds__(256) void repack_dgrad_tiled_kernel(const int8_t* w, int8_t* out, DgradClasses cl,
+                                                                 int K, int R, int S, int C, int sh, int sw) {
+    __shared__ uint32_t tile32[64 * 17];   // [64 k][68 bytes]
+    uint8_t* tile = (uint8_t*)tile32;
+    int f = blockIdx.x;                    // flat tap index over the classes (uniform)
+    int ci = 0;
+    for (; ci < cl.n; ci++) {
+        const int nt = cl.c[ci].T * cl.c[ci].U;
+        if (f < nt) break;
+        f -= nt;
+    }
+    if (ci >= cl.n) return;
+    const DgradClass d = cl.c[ci];
+    const int t = f / d.U, u = f - t * d.U;
+    const int r = d.r0 + sh * (d.T - 1 - t);
+    const int s = d.s0 + sw * (d.U - 1 - u);
+    const int c0 = blockIdx.y * 64, k0 = blockIdx.z * 64;
+    const int i = threadIdx.x;
+    {
+        const int kl = i >> 2, cb = (i & 3) * 16;
+        const int k = k0 + kl;
+        uint32_t v[4] = {0u, 0u, 0u, 0u};
+        if (k < K) {
+            const int8_t* src = w + (((int64_t)k * R + r) * S + s) * C + c0 + cb;
+            if (c0 + cb + 16 <= C && (((uintptr_t)src) & 15) == 0) {
+                const uint4 q = *(const uint4*)src;
+                v[0] = q.x;
+                v[1] = q.y;
+                v[2] = q.z;
+                v[3] = q.w;
+            } else {
+                for (int j = 0; j < 16 && c0 + cb + j < C; j++) v[j >> 2] |= (uint32_t)(uint8_t)src[j] << (8 * (j & 3));
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; q++) tile32[kl * 17 + (cb >> 2) + q] = v[q];
+    }
+    __syncthreads();
+    {
+        const int cc = i >> 2, kb = (i & 3) * 16;
+        const int c = c0 + cc;
+        if (c < C) {
+            uint32_t v[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 16; j++) v[j >> 2] |= (uint32_t)tile[(kb + j) * 68 + cc] << (8 * (j & 3));
+            int8_t* dst = out + d.offset + (((int64_t)c * d.T + t) * d.U + u) * K + k0 + kb;
+            if (k0 + kb + 16 <= K && (((uintptr_t)dst) & 15) == 0) {
+                *(uint4*)dst = make_uint4(v[0], v[1], v[2], v[3]);
+            } else {
+                for (int j = 0; j < 16 && k0 + kb + j < K; j++) dst[j] = (int8_t)(v[j >> 2] >> (8 * (j & 3)));
+            }
+        }
     }
 }
 
@@ -551,8 +590,11 @@ hipError_t repack_dgrad_run(const int8_t* w, int8_t* out, const DgradClass* cls,
         total = cls[i].offset + (int64_t)C * cls[i].T * cls[i].U * K;
     }
     if (total <= 0) return hipSuccess;
-    hipLaunchKernelGGL(repack_dgrad_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, w, out, cl, K,
-                       R, S, C, sh, sw, total);
+    int taps = 0;
+    for (int i = 0; i < ncls; i++) taps += cls[i].T * cls[i].U;
+    if (taps <= 0) return hipSuccess;
+    hipLaunchKernelGGL(repack_dgrad_tiled_kernel, dim3((unsigned)taps, (unsigned)((C + 63) / 64), (unsigned)((K + 63) / 64)),
+                       dim3(256), 0, s, w, out, cl, K, R, S, C, sh, sw);
     return hipGetLastError();
 }
 
