@@ -467,22 +467,26 @@ __global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t*
     }
 }
 
-// One block per padded pixel row (image, row); threads walk its dwords.
-__global__ void pad_image_kernel(const uint32_t* x, uint32_t* xp, int32_t h, int32_t w, int32_t c4, int32_t hp,
-                                 int32_t wp, int32_t ph, int32_t pw) {
-    const uint32_t rid = blockIdx.x;                       // img * hp + padded row
-    const uint32_t img = rid / (uint32_t)hp;
-    const int row = (int)(rid - img * (uint32_t)hp) - ph;
+// Eight padded pixel rows (image, row) per workgroup; threads walk their dwords.
+__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* x, uint32_t* xp, int32_t h, int32_t w,
+                                                        int32_t c4, int32_t hp, int32_t wp, int32_t ph, int32_t pw,
+                                                        uint32_t rows) {
     const uint32_t len = (uint32_t)wp * (uint32_t)c4;
-    uint32_t* dst = xp + (size_t)rid * len;
-    const bool row_in = row >= 0 && row < h;
-    const uint32_t* src = x + ((size_t)img * h + (row_in ? row : 0)) * (size_t)w * c4;
-    for (uint32_t i = threadIdx.x; i < len; i += blockDim.x) {
-        const uint32_t pc = c4 == 1 ? i : i / (uint32_t)c4;
-        const int col = (int)pc - pw;
-        uint32_t v = 0;
-        if (row_in && col >= 0 && col < w) v = src[(uint32_t)col * (uint32_t)c4 + (i - pc * (uint32_t)c4)];
-        dst[i] = v;
+    for (uint32_t rr = 0; rr < 8; rr++) {
+        const uint32_t rid = blockIdx.x * 8 + rr;   // img * hp + padded row
+        if (rid >= rows) return;
+        const uint32_t img = rid / (uint32_t)hp;
+        const int row = (int)(rid - img * (uint32_t)hp) - ph;
+        uint32_t* dst = xp + (size_t)rid * len;
+        const bool row_in = row >= 0 && row < h;
+        const uint32_t* src = x + ((size_t)img * h + (row_in ? row : 0)) * (size_t)w * c4;
+        for (uint32_t i = threadIdx.x; i < len; i += blockDim.x) {
+            const uint32_t pc = c4 == 1 ? i : i / (uint32_t)c4;
+            const int col = (int)pc - pw;
+            uint32_t v = 0;
+            if (row_in && col >= 0 && col < w) v = src[(uint32_t)col * (uint32_t)c4 + (i - pc * (uint32_t)c4)];
+            dst[i] = v;
+        }
     }
 }
 
@@ -629,9 +633,10 @@ hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int6
                          int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
     const int64_t total = n * hp * wp * (c / 4);
     if (total <= 0) return hipSuccess;
-    hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)(n * hp)), dim3(kThreads), 0, s, (const uint32_t*)x,
+    const uint32_t rows = (uint32_t)(n * hp);
+    hipLaunchKernelGGL(pad_image_kernel, dim3((rows + 7) / 8), dim3(kThreads), 0, s, (const uint32_t*)x,
                        (uint32_t*)xp, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)wp, (int32_t)ph,
-                       (int32_t)pw);
+                       (int32_t)pw, rows);
     return hipGetLastError();
 }
 

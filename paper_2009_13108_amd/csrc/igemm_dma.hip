@@ -48,6 +48,13 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
+// vmcnt <= N and lgkmcnt == 0 (this wave's LDS reads done).
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
+}
+
 template <int BM, int BN, int NS, int WGM, int WGN>
 struct Cfg {
     static constexpr int NWAVES = WGM * WGN;
@@ -335,25 +342,41 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
 #pragma unroll
     for (int s = 0; s < NS - 1; s++) issue();
 
+    // Register double buffer over the two 32-byte halves of a K step: the
+    // second half's fragments are read while the first half's MFMAs run, and
+    // the next stage's first half right after the barrier, before this
+    // stage's second-half MFMAs.  Before each barrier a wave waits for its
+    // own fragment reads (lgkmcnt 0), so once all waves pass it no read of
+    // the stage that the next load overwrites is still in flight.
+    auto read_half = [&](const int8_t* st, int ks, v4i (&fa)[T::FN], v4i (&fb)[T::FM]) {
+        const int kp = (lane >> 5) + 2 * ks;
+#pragma unroll
+        for (int a = 0; a < T::FN; a++) fa[a] = *(const v4i*)(st + a_off[a] + ((kp ^ a_sw[a]) << 4));
+#pragma unroll
+        for (int b = 0; b < T::FM; b++) fb[b] = *(const v4i*)(st + b_off[b] + ((kp ^ b_sw[b]) << 4));
+    };
+    auto mma_half = [&](const v4i (&fa)[T::FN], const v4i (&fb)[T::FM]) {
+#pragma unroll
+        for (int a = 0; a < T::FN; a++)
+#pragma unroll
+            for (int b = 0; b < T::FM; b++)
+                acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    };
+    v4i fa0[T::FN], fb0[T::FM], fa1[T::FN], fb1[T::FM];
+    wait_vm<(NS - 2) * T::IPW>();
+    __builtin_amdgcn_s_barrier();
+    read_half(lds, 0, fa0, fb0);
     for (int kt = 0; kt < nk; kt++) {
-        wait_vm<(NS - 2) * T::IPW>();
-        __builtin_amdgcn_s_barrier();
-        issue();
         const int8_t* st = lds + (kt % NS) * T::STAGE_BYTES;
-#pragma unroll
-        for (int ks = 0; ks < 2; ks++) {
-            const int kp = (lane >> 5) + 2 * ks;
-            v4i fa[T::FN], fb[T::FM];
-#pragma unroll
-            for (int a = 0; a < T::FN; a++) fa[a] = *(const v4i*)(st + a_off[a] + ((kp ^ a_sw[a]) << 4));
-#pragma unroll
-            for (int b = 0; b < T::FM; b++) fb[b] = *(const v4i*)(st + b_off[b] + ((kp ^ b_sw[b]) << 4));
-#pragma unroll
-            for (int a = 0; a < T::FN; a++)
-#pragma unroll
-                for (int b = 0; b < T::FM; b++)
-                    acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
-        }
+        issue();   // into the slot of stage kt - 1, which every wave has finished reading
+        read_half(st, 1, fa1, fb1);
+        mma_half(fa0, fb0);
+        // (after the last step this reads the zero-filled stage loaded past
+        // the end: harmless, and it keeps the loop free of branches)
+        wait_vm_lgkm0<(NS - 2) * T::IPW>();
+        __builtin_amdgcn_s_barrier();
+        read_half(lds + ((kt + 1) % NS) * T::STAGE_BYTES, 0, fa0, fb0);
+        mma_half(fa1, fb1);
     }
     // Drain the loads issued past the end before the ring is reused.
     wait_vm<0>();
