@@ -62,15 +62,16 @@ struct Cfg {
     static constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile: pixels x channels
     static constexpr int FM = WTM / 32, FN = WTN / 32;
     static constexpr int BLOCKS = (BM + BN) / 16;           // 1 KiB blocks per stage
-    static constexpr int IPW = BLOCKS / NWAVES;             // load instructions per wave per stage
     static constexpr int ABLK = BN / 16;                    // blocks holding weight rows
-    static constexpr int IPW_W = ABLK / NWAVES;             // of which weight blocks
-    static constexpr int IPW_A = IPW - IPW_W;               // and activation blocks
-    static_assert(ABLK % NWAVES == 0 && (BLOCKS - ABLK) % NWAVES == 0, "blocks split evenly over waves");
+    // Weight blocks per wave: ABLK / NWAVES each, or (fewer blocks than
+    // waves) one each for waves 0 .. ABLK-1.
+    static constexpr bool W_EVEN = ABLK % NWAVES == 0;
+    static constexpr int IPW_W = W_EVEN ? ABLK / NWAVES : 1;
+    static constexpr int IPW_A = (BLOCKS - ABLK) / NWAVES;  // activation blocks per wave
+    static_assert((BLOCKS - ABLK) % NWAVES == 0 && (W_EVEN || ABLK < NWAVES), "load split over waves");
     static constexpr int STAGE_BYTES = (BM + BN) * KSTEP;
     static constexpr int LDS_BYTES = NS * STAGE_BYTES;
     static constexpr int WGM_ = WGM, BN_ = BN;
-    static_assert(BLOCKS % NWAVES == 0, "blocks per wave");
     static_assert(BM * (BN + 16) <= LDS_BYTES, "output tile fits in the ring");
 };
 
@@ -210,10 +211,12 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     const uint32_t kpo = (uint32_t)(((lane & 3) ^ swz(lrow)) << 4);  // byte offset of this lane's chunk
     uint32_t wb[T::IPW_W], ab[T::IPW_A];
     uint32_t aux[T::IPW_A];   // kConv64: taps (bit r*S+s) outside the image; kWin: filter row of the piece
+    const bool wload = T::W_EVEN || wave < T::ABLK;   // this wave loads weight blocks (uniform)
+    const int wblk0 = T::W_EVEN ? wave * T::IPW_W : wave;
 #pragma unroll
     for (int i = 0; i < T::IPW_W; i++) {
-        const int n = tn * BN + (wave * T::IPW_W + i) * 16 + lrow;
-        wb[i] = n < P.Nout ? (uint32_t)n * (uint32_t)P.Ktot + kpo : kOOB;
+        const int n = tn * BN + (wblk0 + i) * 16 + lrow;
+        wb[i] = (wload && n < P.Nout) ? (uint32_t)n * (uint32_t)P.Ktot + kpo : kOOB;
     }
 #pragma unroll
     for (int i = 0; i < T::IPW_A; i++) {
@@ -260,13 +263,16 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     // whose piece is past K, past R or outside the image get kOOB.
     auto issue = [&]() {
         int8_t* st = lds + (next_kt % NS) * T::STAGE_BYTES;
-        int8_t* wst = st + wave * T::IPW_W * 1024;
+        int8_t* wst = st + wblk0 * 1024;
         int8_t* ast = st + (T::ABLK + wave * T::IPW_A) * 1024;
         if (next_kt >= nk) {
             // loads past the last K step keep the wait counts constant
+            if (wload) {
 #pragma unroll
-            for (int i = 0; i < T::IPW_W; i++)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)kOOB, 0, 0, 0);
+                for (int i = 0; i < T::IPW_W; i++)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)kOOB, 0, 0,
+                                                             0);
+            }
 #pragma unroll
             for (int i = 0; i < T::IPW_A; i++)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)kOOB, 0, 0, 0);
@@ -276,10 +282,12 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
         const uint32_t kb = (uint32_t)next_kt * KSTEP;
         // kGemm: bytes of this K step inside the row (64 except on a partial last step)
         const uint32_t klim = min((uint32_t)P.Ktot - kb, (uint32_t)KSTEP);
+        if (wload) {
 #pragma unroll
-        for (int i = 0; i < T::IPW_W; i++) {
-            const uint32_t v = (MODE == kGemm && kpo >= klim) ? kOOB : wb[i];
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)v, (int)kb, 0, 0);
+            for (int i = 0; i < T::IPW_W; i++) {
+                const uint32_t v = (MODE == kGemm && kpo >= klim) ? kOOB : wb[i];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)v, (int)kb, 0, 0);
+            }
         }
         if (MODE == kGemm) {
 #pragma unroll
@@ -362,8 +370,13 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
             for (int b = 0; b < T::FM; b++)
                 acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
     };
+    // Loads per stage of this wave (uniform): the stage-exact wait counts.
+    constexpr int LW = T::IPW_A + T::IPW_W, LA = T::IPW_A;
     v4i fa0[T::FN], fb0[T::FM], fa1[T::FN], fb1[T::FM];
-    wait_vm<(NS - 2) * T::IPW>();
+    if (wload)
+        wait_vm<(NS - 2) * LW>();
+    else
+        wait_vm<(NS - 2) * LA>();
     __builtin_amdgcn_s_barrier();
     read_half(lds, 0, fa0, fb0);
     for (int kt = 0; kt < nk; kt++) {
@@ -373,7 +386,10 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
         mma_half(fa0, fb0);
         // (after the last step this reads the zero-filled stage loaded past
         // the end: harmless, and it keeps the loop free of branches)
-        wait_vm_lgkm0<(NS - 2) * T::IPW>();
+        if (wload)
+            wait_vm_lgkm0<(NS - 2) * LW>();
+        else
+            wait_vm_lgkm0<(NS - 2) * LA>();
         __builtin_amdgcn_s_barrier();
         read_half(lds + ((kt + 1) % NS) * T::STAGE_BYTES, 0, fa0, fb0);
         mma_half(fa1, fb1);
@@ -501,12 +517,14 @@ hipError_t run_mode(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         maxN = b.p[i].Nout > maxN ? b.p[i].Nout : maxN;
     }
     // The largest tile that still gives most compute units a workgroup.
-    if (maxN <= 64) return launch_dma<256, 64, 4, 4, 1, MODE>(b, ctl, stream);
-    // 128 x 128 fits two workgroups per CU (256 x 128 fits one, by registers).
-    if (maxN <= 128) return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
+    if (maxN <= 64) return launch_dma<256, 64, 4, 8, 1, MODE>(b, ctl, stream);
+    // 128 x 128 with eight 32 x 64 waves: two workgroups per CU (256 x 128
+    // fits one, by registers) and four waves per SIMD to hide each other's
+    // LDS and barrier waits.
+    if (maxN <= 128) return launch_dma<128, 128, 4, 4, 2, MODE>(b, ctl, stream);
     if (work >= (int64_t)200 * 256 * 256) return launch_dma<256, 256, 3, 2, 4, MODE>(b, ctl, stream);
     if (work >= (int64_t)200 * 256 * 128) return launch_dma<256, 128, 4, 2, 2, MODE>(b, ctl, stream);
-    return launch_dma<128, 128, 4, 2, 2, MODE>(b, ctl, stream);
+    return launch_dma<128, 128, 4, 4, 2, MODE>(b, ctl, stream);
 }
 
 }  // namespace
