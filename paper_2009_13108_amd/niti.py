@@ -181,6 +181,44 @@ def _check(st, what):
         raise NitiError(st, what)
 
 
+# Prepared calls: while a recorder list is set, every entry point appends
+# (function, marshalled arguments, name) after checking its arguments and
+# running.  replay() reissues such a list without the Python-side checks,
+# for callers that enqueue the same calls (same tensors, streams, stats)
+# every step.
+_recorder = None
+
+
+def _run(name, *args):
+    f = getattr(lib(), name)
+    if _recorder is not None:
+        _recorder.append((f, args, name))
+    _check(f(*args), name)
+
+
+class recording:
+    """with niti.recording() as calls: ... -> calls lists the entry-point calls made."""
+
+    def __enter__(self):
+        global _recorder
+        self.calls = []
+        _recorder = self.calls
+        return self.calls
+
+    def __exit__(self, *exc):
+        global _recorder
+        _recorder = None
+        return False
+
+
+def replay(calls):
+    """Reissue recorded calls (see recording); raises on the first error."""
+    for f, args, name in calls:
+        st = f(*args)
+        if st != 0:
+            raise NitiError(st, name)
+
+
 def _stats_ptr(stats, index=0):
     torch = _torch()
     _dev(stats, torch.uint8, "stats")
@@ -236,9 +274,9 @@ def gemm_fwd(A, B, C, stats, s_a=None, s_b=None, s_c=None, target_bits=7, relu=F
     if K2 != K or tuple(C.shape) != (M, N):
         raise ValueError("gemm_fwd: shapes %s %s %s" % (tuple(A.shape), tuple(B.shape), tuple(C.shape)))
     _exp3(s_a, s_b, s_c, "gemm_fwd")
-    _check(lib().niti_gemm_fwd(_ptr(A), _ptr(B), _ptr(C), M, N, K, _ptr(s_a), _ptr(s_b), _ptr(s_c),
+    _run("niti_gemm_fwd", _ptr(A), _ptr(B), _ptr(C), M, N, K, _ptr(s_a), _ptr(s_b), _ptr(s_c),
                                int(target_bits), int(bool(relu)), int(mode),
-                               _stats_ptr(stats, stats_index), _stream(stream)), "niti_gemm_fwd")
+                               _stats_ptr(stats, stats_index), _stream(stream))
 
 
 def _conv_check(d: ConvDesc, **tensors):
@@ -261,19 +299,17 @@ def conv_fwd(d: ConvDesc, x, w, y, stats, s_x=None, s_w=None, s_y=None, relu=Fal
     _exp3(s_x, s_w, s_y, "conv_fwd")
     if ws is not None:
         _dev(ws, torch.uint8, "ws")
-    _check(lib().niti_conv_fwd(ctypes.byref(d), _ptr(x), _ptr(w), _ptr(y), _ptr(s_x), _ptr(s_w),
+    _run("niti_conv_fwd", ctypes.byref(d), _ptr(x), _ptr(w), _ptr(y), _ptr(s_x), _ptr(s_w),
                                _ptr(s_y), int(bool(relu)), int(mode), _stats_ptr(stats, stats_index),
-                               _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)),
-           "niti_conv_fwd")
+                               _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
 
 
 def conv_bwd_data(d: ConvDesc, dy, w, dx, stats, ws, relu_src=None, mode=PSR, stats_index=0, stream=None):
     torch = _torch()
     _conv_check(d, dy=dy, w=w, dx=dx, relu_src=relu_src)
     _dev(ws, torch.uint8, "ws")
-    _check(lib().niti_conv_bwd_data(ctypes.byref(d), _ptr(dy), _ptr(w), _ptr(dx), _ptr(relu_src), int(mode),
-                                    _stats_ptr(stats, stats_index), _ptr(ws), ws.numel(), _stream(stream)),
-           "niti_conv_bwd_data")
+    _run("niti_conv_bwd_data", ctypes.byref(d), _ptr(dy), _ptr(w), _ptr(dx), _ptr(relu_src), int(mode),
+                                    _stats_ptr(stats, stats_index), _ptr(ws), ws.numel(), _stream(stream))
 
 
 def conv_bwd_weight(d: ConvDesc, x, dy, w, stats, ws=None, g32_out=None, mu=5, mode=PSR, stats_index=0,
@@ -286,10 +322,9 @@ def conv_bwd_weight(d: ConvDesc, x, dy, w, stats, ws=None, g32_out=None, mu=5, m
             raise ValueError("g32_out shape")
     if ws is not None:
         _dev(ws, torch.uint8, "ws")
-    _check(lib().niti_conv_bwd_weight(ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(w), _ptr(g32_out), int(mu),
+    _run("niti_conv_bwd_weight", ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(w), _ptr(g32_out), int(mu),
                                       int(mode), _stats_ptr(stats, stats_index), _ptr(ws),
-                                      ws.numel() if ws is not None else 0, _stream(stream)),
-           "niti_conv_bwd_weight")
+                                      ws.numel() if ws is not None else 0, _stream(stream))
 
 
 def round_psr(x, y, bp=-1, target_bits=7, stats=None, s_in=None, s_out=None, mode=PSR, stats_index=0,
@@ -300,8 +335,8 @@ def round_psr(x, y, bp=-1, target_bits=7, stats=None, s_in=None, s_out=None, mod
         raise ValueError("round_psr: sizes differ")
     _dev(s_in, torch.int8, "s_in"); _dev(s_out, torch.int8, "s_out")
     sp = _stats_ptr(stats, stats_index) if stats is not None else None
-    _check(lib().niti_round_psr(_ptr(x), _ptr(y), x.numel(), int(bp), int(target_bits), int(mode),
-                                _ptr(s_in), _ptr(s_out), sp, _stream(stream)), "niti_round_psr")
+    _run("niti_round_psr", _ptr(x), _ptr(y), x.numel(), int(bp), int(target_bits), int(mode),
+                                _ptr(s_in), _ptr(s_out), sp, _stream(stream))
 
 
 def int_ce_loss_grad(logits, s_logits, labels, err, stats, ws, mode=PSR, stats_index=0, stream=None):
@@ -311,9 +346,9 @@ def int_ce_loss_grad(logits, s_logits, labels, err, stats, ws, mode=PSR, stats_i
     B, N = logits.shape
     if tuple(err.shape) != (B, N) or tuple(labels.shape) != (B,):
         raise ValueError("int_ce_loss_grad: shapes")
-    _check(lib().niti_int_ce_loss_grad(_ptr(logits), _ptr(s_logits), _ptr(labels), _ptr(err), B, N,
+    _run("niti_int_ce_loss_grad", _ptr(logits), _ptr(s_logits), _ptr(labels), _ptr(err), B, N,
                                        int(mode), _stats_ptr(stats, stats_index), _ptr(ws), ws.numel(),
-                                       _stream(stream)), "niti_int_ce_loss_grad")
+                                       _stream(stream))
 
 
 def sgd_update(w, g32, stats, mu=5, mode=PSR, stats_index=0, stream=None):
@@ -321,8 +356,8 @@ def sgd_update(w, g32, stats, mu=5, mode=PSR, stats_index=0, stream=None):
     _dev(w, torch.int8, "w"); _dev(g32, torch.int32, "g32")
     if w.numel() != g32.numel():
         raise ValueError("sgd_update: sizes differ")
-    _check(lib().niti_sgd_update(_ptr(w), _ptr(g32), w.numel(), int(mu), int(mode),
-                                 _stats_ptr(stats, stats_index), _stream(stream)), "niti_sgd_update")
+    _run("niti_sgd_update", _ptr(w), _ptr(g32), w.numel(), int(mu), int(mode),
+                                 _stats_ptr(stats, stats_index), _stream(stream))
 
 
 # ------------------------------------------------------------------ glue
@@ -333,8 +368,7 @@ def quantize_u8(px, x, stream=None):
     n, c, h, w = px.shape
     if tuple(x.shape[:3]) != (n, h, w) or x.shape[3] < c:
         raise ValueError("quantize_u8: shapes")
-    _check(lib().niti_quantize_u8(_ptr(px), _ptr(x), n, c, h, w, x.shape[3], _stream(stream)),
-           "niti_quantize_u8")
+    _run("niti_quantize_u8", _ptr(px), _ptr(x), n, c, h, w, x.shape[3], _stream(stream))
 
 
 def maxpool2_fwd(x, y, idx, stream=None):
@@ -343,8 +377,7 @@ def maxpool2_fwd(x, y, idx, stream=None):
     n, h, w, c = x.shape
     if tuple(y.shape) != (n, h // 2, w // 2, c) or tuple(idx.shape) != tuple(y.shape):
         raise ValueError("maxpool2_fwd: shapes")
-    _check(lib().niti_maxpool2_fwd(_ptr(x), _ptr(y), _ptr(idx), n, h, w, c, _stream(stream)),
-           "niti_maxpool2_fwd")
+    _run("niti_maxpool2_fwd", _ptr(x), _ptr(y), _ptr(idx), n, h, w, c, _stream(stream))
 
 
 def maxpool2_bwd(dy, idx, dx, stream=None):
@@ -353,8 +386,7 @@ def maxpool2_bwd(dy, idx, dx, stream=None):
     n, h, w, c = dx.shape
     if tuple(dy.shape) != (n, h // 2, w // 2, c) or tuple(idx.shape) != tuple(dy.shape):
         raise ValueError("maxpool2_bwd: shapes")
-    _check(lib().niti_maxpool2_bwd(_ptr(dy), _ptr(idx), _ptr(dx), n, h, w, c, _stream(stream)),
-           "niti_maxpool2_bwd")
+    _run("niti_maxpool2_bwd", _ptr(dy), _ptr(idx), _ptr(dx), n, h, w, c, _stream(stream))
 
 
 def relu_mask(e, a, stream=None):
@@ -362,4 +394,4 @@ def relu_mask(e, a, stream=None):
     _dev(e, torch.int8, "e"); _dev(a, torch.int8, "a")
     if e.numel() != a.numel():
         raise ValueError("relu_mask: sizes differ")
-    _check(lib().niti_relu_mask(_ptr(e), _ptr(a), e.numel(), _stream(stream)), "niti_relu_mask")
+    _run("niti_relu_mask", _ptr(e), _ptr(a), e.numel(), _stream(stream))

@@ -318,3 +318,33 @@ def test_glue_parity():
     niti.relu_mask(ed, dev(act))
     torch.cuda.synchronize()
     assert (host(ed) == e_exp).all()
+
+
+def test_recorded_calls_replay():
+    """Calls recorded once (marshalled arguments) and replayed act like fresh
+    calls: the replay reads the buffers' current contents and updates the
+    block statistics the same way."""
+    import torch
+    say("recorded replay")
+    M, N, K = 300, 200, 784
+    dA = torch.empty((M, K), dtype=torch.int8, device="cuda")
+    dB = dev(I.weights(7, (N, K)))
+    C = torch.empty((M, N), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    sa, sb, sc = _i8(-7), _i8(-9), _i8(0)
+    calls = None
+    for rep, seed in enumerate([11, 12, 13]):
+        A = I.activations(seed, (M, K))
+        dA.copy_(dev(A))
+        C.fill_(99)
+        if calls is None:
+            with niti.recording() as calls:
+                niti.gemm_fwd(dA, dB, C, stats, sa, sb, sc, 7, True)
+            assert len(calls) == 1
+        else:
+            niti.replay(calls)
+        torch.cuda.synchronize()
+        exp_out, _, st = oracle.gemm_fwd(A, I.weights(7, (N, K)), relu=True)
+        g = niti.read_stats(stats)[0]
+        assert (host(C) == exp_out).all(), "rep %d" % rep
+        assert same_stats(g, st) and g["calls"] == rep + 1

@@ -152,3 +152,39 @@ def test_config3_vgg_training_steps(batch, steps):
             assert (kcrs(gw[li])[:, :w_orc[li].shape[1]] == onet.w[li]).all(), "conv %d step %d" % (li, step)
         assert (kcrs(gw[0])[:, 3] == 0).all()
         assert (_gpu_fc_to_orc(gw[6], 256, 4) == onet.w[6]).all(), "fc step %d" % step
+
+
+def test_graph_replay_matches_eager():
+    """A training step captured as a HIP graph and replayed matches eager
+    steps call for call: two nets start from the same weights; each round
+    runs one eager step on one and one replay on the other (with eager work
+    and synchronizations between replays), then compares weights and logits."""
+    import torch
+    batch = 8
+    say("graph replay vgg", batch)
+    px, labels, w_orc, w_gpu, exps = _vgg_setup(batch)
+    eager = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps)
+    graphed = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps)
+    x = torch.empty((batch, 32, 32, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(dev(px), x)
+    lab = dev(labels)
+    s0 = _i8(-7)
+    # one eager step on both (first calls set up kernel attributes and guesses)
+    eager.step(x, s0, lab)
+    graphed.step(x, s0, lab)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=cap):
+        lg, sg = graphed.step(x, s0, lab)
+    torch.cuda.synchronize()
+    for rnd in range(3):
+        le, se = eager.step(x, s0, lab)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert (host(lg) == host(le)).all(), "logits round %d" % rnd
+        assert int(host(sg)[0]) == int(host(se)[0])
+        for a, b in zip(graphed.weights(), eager.weights()):
+            assert (host(a) == host(b)).all(), "weights round %d" % rnd
