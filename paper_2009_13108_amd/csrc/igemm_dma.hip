@@ -199,10 +199,8 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave % WGM, wn = wave / WGM;
 
-    const __amdgpu_buffer_rsrc_t act_rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.act, 0, (int)P.act_bytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t wgt_rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.wgt, 0, (int)P.wgt_bytes, 0x00020000);
+    const u32x4 act_rs = raw_rsrc(P.act, (uint32_t)P.act_bytes);
+    const u32x4 wgt_rs = raw_rsrc(P.wgt, (uint32_t)P.wgt_bytes);
 
     // Per-lane row state for each load instruction: a wave issues IPW_W
     // weight blocks and IPW_A activation blocks per stage; wb / ab is the
@@ -254,75 +252,95 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     }
 
     const int nk = (P.Ktot + KSTEP - 1) / KSTEP;
-    // Uniform position of the next stage to issue: K offset, tap (r, s), channel block.
-    int next_kt = 0, tr = 0, ts = 0, tc = 0;
-
-    // The uniform part of an offset rides in the instruction's SGPR offset
-    // wherever the lane part is a fixed in-bounds position; every lane offset
-    // that is not kOOB stays inside its buffer by construction, and lanes
-    // whose piece is past K, past R or outside the image get kOOB.
-    auto issue = [&]() {
-        int8_t* st = lds + (next_kt % NS) * T::STAGE_BYTES;
-        int8_t* wst = st + wblk0 * 1024;
-        int8_t* ast = st + (T::ABLK + wave * T::IPW_A) * 1024;
-        if (next_kt >= nk) {
-            // loads past the last K step keep the wait counts constant
-            if (wload) {
+    // Scalar instructions issue at about one per cycle per CU, shared by all
+    // waves, so the load side keeps its per-step uniform work small: the
+    // lanes' current offsets cvw / cva change only at events (a filter tap
+    // change, the last K step, the end of K), counted down by ev; between
+    // events a step adds to the two uniform offsets kb (weights, and kGemm
+    // activations) and sa (kConv64: channel offset within the tap; kWin:
+    // window row offset).  The uniform part of an offset rides in the
+    // instruction's SGPR offset; every lane offset that is not kOOB stays
+    // inside its buffer together with it, and lanes whose piece is past K,
+    // past R or outside the image get kOOB (zeros).
+    const uint32_t lds0 = lds_address(lds);
+    const uint32_t wdst = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)wblk0 * 1024u);
+    const uint32_t adst = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(T::ABLK + wave * T::IPW_A) * 1024u);
+    const int cbs = __builtin_amdgcn_readfirstlane(MODE == kConv64 ? P.C / KSTEP : 1);
+    const int ntap = __builtin_amdgcn_readfirstlane(P.R * P.S);
+    const uint32_t da = __builtin_amdgcn_readfirstlane(
+        MODE == kWin ? (uint32_t)(KSTEP / P.L) * (uint32_t)(P.W * P.C) : (uint32_t)KSTEP);
+    const uint32_t klim = __builtin_amdgcn_readfirstlane(
+        MODE == kGemm ? (uint32_t)(P.Ktot - (nk - 1) * KSTEP) : (MODE == kWin ? (uint32_t)(P.R - (nk - 1) * (KSTEP / P.L)) : 0u));
+    uint32_t kb = 0, sa = 0, slot = 0, tapbase = 0;
+    int ev = 0, tap = 0, ts = 0, ph = 0;
+    uint32_t cvw[T::IPW_W], cva[T::IPW_A];
 #pragma unroll
-                for (int i = 0; i < T::IPW_W; i++)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)kOOB, 0, 0,
-                                                             0);
+    for (int i = 0; i < T::IPW_W; i++) cvw[i] = wb[i];
+    auto set_tap = [&]() {
+#pragma unroll
+        for (int i = 0; i < T::IPW_A; i++) cva[i] = (__builtin_amdgcn_ubfe(aux[i], (uint32_t)tap, 1) << 31) | (ab[i] + tapbase);
+    };
+    // last K step (kGemm: pieces past K; kWin: rows past R masked)
+    auto last_step = [&]() {
+        ph = 1;
+        ev = 1;
+#pragma unroll
+        for (int i = 0; i < T::IPW_W; i++) cvw[i] = (MODE == kGemm && kpo >= klim) ? kOOB : wb[i];
+#pragma unroll
+        for (int i = 0; i < T::IPW_A; i++) cva[i] = (MODE == kGemm ? kpo >= klim : aux[i] >= klim) ? kOOB : ab[i];
+    };
+#pragma unroll
+    for (int i = 0; i < T::IPW_A; i++) cva[i] = ab[i];
+    if (nk <= 0) {
+        ph = 2;
+        ev = 1 << 30;
+    } else if (MODE == kConv64) {
+        set_tap();
+        ev = cbs;
+    } else {
+        ev = nk - 1;
+        if (ev == 0) last_step();
+    }
+    // Events are handled at the start of the issue that follows them.
+    auto advance = [&]() {
+        if (MODE == kConv64 && tap + 1 < ntap) {
+            ++tap;
+            if (++ts == P.S) {
+                ts = 0;
+                tapbase += (uint32_t)((P.W - P.S + 1) * P.C);
+            } else {
+                tapbase += (uint32_t)P.C;
             }
-#pragma unroll
-            for (int i = 0; i < T::IPW_A; i++)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)kOOB, 0, 0, 0);
-            next_kt++;
+            set_tap();
+            sa = 0;
+            ev = cbs;
             return;
         }
-        const uint32_t kb = (uint32_t)next_kt * KSTEP;
-        // kGemm: bytes of this K step inside the row (64 except on a partial last step)
-        const uint32_t klim = min((uint32_t)P.Ktot - kb, (uint32_t)KSTEP);
+        if (MODE != kConv64 && ph == 0) {
+            last_step();
+            return;
+        }
+        // Past the end of K the loads go on unchanged (the buffer bounds
+        // keep them harmless): they keep the wait counts constant, and the
+        // stages they fill are never multiplied.
+        tap = 1 << 30;
+        ph = 2;
+        ev = 1 << 30;
+    };
+    auto issue = [&]() {
+        if (ev == 0) advance();
         if (wload) {
 #pragma unroll
-            for (int i = 0; i < T::IPW_W; i++) {
-                const uint32_t v = (MODE == kGemm && kpo >= klim) ? kOOB : wb[i];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(wgt_rs, (lds_void*)(wst + i * 1024), 16, (int)v, (int)kb, 0, 0);
-            }
+            for (int i = 0; i < T::IPW_W; i++) lds_dma16(wgt_rs, wdst + slot + (uint32_t)(i * 1024), cvw[i], kb);
         }
-        if (MODE == kGemm) {
 #pragma unroll
-            for (int i = 0; i < T::IPW_A; i++) {
-                const uint32_t v = kpo >= klim ? kOOB : ab[i];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, (int)kb, 0, 0);
-            }
-        } else if (MODE == kWin) {
-            const int rps = KSTEP / P.L;                      // filter rows per step (uniform)
-            const int rlim = P.R - next_kt * rps;             // pieces at row rr >= rlim are past R
-            const uint32_t soff = (uint32_t)(next_kt * rps) * (uint32_t)(P.W * P.C);
-#pragma unroll
-            for (int i = 0; i < T::IPW_A; i++) {
-                const uint32_t v = (int)aux[i] >= rlim ? kOOB : ab[i];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, (int)soff, 0, 0);
-            }
-        } else {
-            const uint32_t tap_off = (uint32_t)((tr * P.W + ts) * P.C + tc);
-            const int tap = tr * P.S + ts;
-#pragma unroll
-            for (int i = 0; i < T::IPW_A; i++) {
-                // bit 31 set for a tap outside the image: past any buffer size
-                const uint32_t v = (__builtin_amdgcn_ubfe(aux[i], tap, 1) << 31) | (ab[i] + tap_off);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(act_rs, (lds_void*)(ast + i * 1024), 16, (int)v, 0, 0, 0);
-            }
-            tc += KSTEP;
-            if (tc == P.C) {
-                tc = 0;
-                if (++ts == P.S) {
-                    ts = 0;
-                    ++tr;
-                }
-            }
-        }
-        next_kt++;
+        for (int i = 0; i < T::IPW_A; i++)
+            lds_dma16(act_rs, adst + slot + (uint32_t)(i * 1024), cva[i], MODE == kGemm ? kb : sa);
+        kb += KSTEP;
+        sa += da;
+        ev = __builtin_amdgcn_readfirstlane(ev - 1);
+        slot = __builtin_amdgcn_readfirstlane(slot == (uint32_t)((NS - 1) * T::STAGE_BYTES) ? 0u
+                                                                                             : slot + (uint32_t)T::STAGE_BYTES);
     };
 
     v16i acc[T::FN][T::FM];
@@ -384,8 +402,8 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
         issue();   // into the slot of stage kt - 1, which every wave has finished reading
         read_half(st, 1, fa1, fb1);
         mma_half(fa0, fb0);
-        // (after the last step this reads the zero-filled stage loaded past
-        // the end: harmless, and it keeps the loop free of branches)
+        // (after the last step this reads a stage loaded past the end of K,
+        // which no MFMA uses: it keeps the loop free of branches)
         if (wload)
             wait_vm_lgkm0<(NS - 2) * LW>();
         else
