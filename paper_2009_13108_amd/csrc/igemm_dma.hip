@@ -263,15 +263,19 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     // inside its buffer together with it, and lanes whose piece is past K,
     // past R or outside the image get kOOB (zeros).
     const uint32_t lds0 = lds_address(lds);
-    const uint32_t wdst = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)wblk0 * 1024u);
-    const uint32_t adst = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(T::ABLK + wave * T::IPW_A) * 1024u);
+    uint32_t wdst[T::IPW_W], adst[T::IPW_A];   // this wave's blocks in stage 0
+#pragma unroll
+    for (int i = 0; i < T::IPW_W; i++) wdst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(wblk0 + i) * 1024u);
+#pragma unroll
+    for (int i = 0; i < T::IPW_A; i++)
+        adst[i] = __builtin_amdgcn_readfirstlane(lds0 + (uint32_t)(T::ABLK + wave * T::IPW_A + i) * 1024u);
     const int cbs = __builtin_amdgcn_readfirstlane(MODE == kConv64 ? P.C / KSTEP : 1);
     const int ntap = __builtin_amdgcn_readfirstlane(P.R * P.S);
     const uint32_t da = __builtin_amdgcn_readfirstlane(
         MODE == kWin ? (uint32_t)(KSTEP / P.L) * (uint32_t)(P.W * P.C) : (uint32_t)KSTEP);
     const uint32_t klim = __builtin_amdgcn_readfirstlane(
         MODE == kGemm ? (uint32_t)(P.Ktot - (nk - 1) * KSTEP) : (MODE == kWin ? (uint32_t)(P.R - (nk - 1) * (KSTEP / P.L)) : 0u));
-    uint32_t kb = 0, sa = 0, slot = 0, tapbase = 0;
+    uint32_t kb = 0, sa = 0, tapbase = 0;
     int ev = 0, tap = 0, ts = 0, ph = 0;
     uint32_t cvw[T::IPW_W], cva[T::IPW_A];
 #pragma unroll
@@ -327,20 +331,19 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
         ph = 2;
         ev = 1 << 30;
     };
-    auto issue = [&]() {
+    // issue(j): load K step j (ring slot j % NS)
+    auto issue = [&](int j) {
         if (ev == 0) advance();
+        const uint32_t slot = (uint32_t)(j % NS) * (uint32_t)T::STAGE_BYTES;
         if (wload) {
 #pragma unroll
-            for (int i = 0; i < T::IPW_W; i++) lds_dma16(wgt_rs, wdst + slot + (uint32_t)(i * 1024), cvw[i], kb);
+            for (int i = 0; i < T::IPW_W; i++) lds_dma16_at(wgt_rs, wdst[i], slot, cvw[i], kb);
         }
 #pragma unroll
-        for (int i = 0; i < T::IPW_A; i++)
-            lds_dma16(act_rs, adst + slot + (uint32_t)(i * 1024), cva[i], MODE == kGemm ? kb : sa);
+        for (int i = 0; i < T::IPW_A; i++) lds_dma16_at(act_rs, adst[i], slot, cva[i], MODE == kGemm ? kb : sa);
         kb += KSTEP;
         sa += da;
         ev = __builtin_amdgcn_readfirstlane(ev - 1);
-        slot = __builtin_amdgcn_readfirstlane(slot == (uint32_t)((NS - 1) * T::STAGE_BYTES) ? 0u
-                                                                                             : slot + (uint32_t)T::STAGE_BYTES);
     };
 
     v16i acc[T::FN][T::FM];
@@ -366,7 +369,7 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     }
 
 #pragma unroll
-    for (int s = 0; s < NS - 1; s++) issue();
+    for (int s = 0; s < NS - 1; s++) issue(s);
 
     // Register double buffer over the two 32-byte halves of a K step: the
     // second half's fragments are read while the first half's MFMAs run, and
@@ -399,7 +402,7 @@ __device__ __forceinline__ void dma_tile(const IgemmProblem& P, int tm, int tn, 
     read_half(lds, 0, fa0, fb0);
     for (int kt = 0; kt < nk; kt++) {
         const int8_t* st = lds + (kt % NS) * T::STAGE_BYTES;
-        issue();   // into the slot of stage kt - 1, which every wave has finished reading
+        issue(kt + NS - 1);   // into the slot of stage kt - 1, which every wave has finished reading
         read_half(st, 1, fa1, fb1);
         mma_half(fa0, fb0);
         // (after the last step this reads a stage loaded past the end of K,

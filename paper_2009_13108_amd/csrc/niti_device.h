@@ -171,6 +171,16 @@ __device__ __forceinline__ void lds_dma16(u32x4 rs, uint32_t m0, uint32_t voff, 
                  : "memory", "m0");
 }
 
+// The same with the LDS address given as the sum of two uniform values,
+// formed directly in m0.
+__device__ __forceinline__ void lds_dma16_at(u32x4 rs, uint32_t base, uint32_t off, uint32_t voff, uint32_t soff) {
+    asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(base)), "s"(__builtin_amdgcn_readfirstlane(off)), "v"(voff),
+                   "s"(rs), "s"(soff)
+                 : "memory", "m0", "scc");
+}
+
 // Wave maximum of a 32-bit value with row-local DPP steps and four lane
 // reads; the result is uniform.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
