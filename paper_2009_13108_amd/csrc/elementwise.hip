@@ -467,25 +467,34 @@ __global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t*
     }
 }
 
-// Eight padded pixel rows (image, row) per workgroup; threads walk their dwords.
-__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* x, uint32_t* xp, int32_t h, int32_t w,
-                                                        int32_t c4, int32_t hp, int32_t wp, int32_t ph, int32_t pw,
-                                                        uint32_t rows) {
-    const uint32_t len = (uint32_t)wp * (uint32_t)c4;
-    for (uint32_t rr = 0; rr < 8; rr++) {
-        const uint32_t rid = blockIdx.x * 8 + rr;   // img * hp + padded row
-        if (rid >= rows) return;
-        const uint32_t img = rid / (uint32_t)hp;
-        const int row = (int)(rid - img * (uint32_t)hp) - ph;
-        uint32_t* dst = xp + (size_t)rid * len;
-        const bool row_in = row >= 0 && row < h;
-        const uint32_t* src = x + ((size_t)img * h + (row_in ? row : 0)) * (size_t)w * c4;
-        for (uint32_t i = threadIdx.x; i < len; i += blockDim.x) {
-            const uint32_t pc = c4 == 1 ? i : i / (uint32_t)c4;
+// Zero-padded copy, 16 output bytes per thread over the flat output (the
+// output rows need not be 16-byte multiples, so a piece may straddle two
+// rows): four independent dword loads, one 16-byte store.
+__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* x, uint32_t* xp, FastDiv div_len,
+                                                        FastDiv div_hp, FastDiv div_c4, uint32_t len, int32_t h,
+                                                        int32_t w, int32_t c4, int32_t hp, int32_t ph, int32_t pw,
+                                                        uint32_t total) {
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t t = blockIdx.x * blockDim.x + threadIdx.x; 4 * t < total; t += stride) {
+        uint32_t v[4];
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const uint32_t j = 4 * t + (uint32_t)q;   // output dword
+            v[q] = 0;
+            if (j >= total) continue;
+            const uint32_t rid = fdiv(j, div_len);     // img * hp + padded row
+            const uint32_t cw = j - rid * len;
+            const uint32_t img = fdiv(rid, div_hp);
+            const int row = (int)(rid - img * (uint32_t)hp) - ph;
+            const uint32_t pc = c4 == 1 ? cw : fdiv(cw, div_c4);
             const int col = (int)pc - pw;
-            uint32_t v = 0;
-            if (row_in && col >= 0 && col < w) v = src[(uint32_t)col * (uint32_t)c4 + (i - pc * (uint32_t)c4)];
-            dst[i] = v;
+            if (row >= 0 && row < h && col >= 0 && col < w)
+                v[q] = x[(((size_t)img * h + row) * w + col) * c4 + (cw - pc * (uint32_t)c4)];
+        }
+        if (4 * t + 3 < total) {
+            *(uint4*)(xp + 4 * t) = make_uint4(v[0], v[1], v[2], v[3]);
+        } else {
+            for (int q = 0; q < 4 && 4 * t + q < total; q++) xp[4 * t + q] = v[q];
         }
     }
 }
@@ -633,10 +642,15 @@ hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int6
                          int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
     const int64_t total = n * hp * wp * (c / 4);
     if (total <= 0) return hipSuccess;
-    const uint32_t rows = (uint32_t)(n * hp);
-    hipLaunchKernelGGL(pad_image_kernel, dim3((rows + 7) / 8), dim3(kThreads), 0, s, (const uint32_t*)x,
-                       (uint32_t*)xp, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)wp, (int32_t)ph,
-                       (int32_t)pw, rows);
+    if (total >= ((int64_t)1 << 32) - 4) return hipErrorInvalidValue;
+    const uint32_t len = (uint32_t)(wp * (c / 4));
+    const int64_t threads = (total + 3) / 4;
+    int64_t grid = (threads + kThreads - 1) / kThreads;
+    if (grid > 65536) grid = 65536;
+    hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, s, (const uint32_t*)x,
+                       (uint32_t*)xp, make_fastdiv(len), make_fastdiv((uint32_t)hp), make_fastdiv((uint32_t)(c / 4)),
+                       len, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)ph, (int32_t)pw,
+                       (uint32_t)total);
     return hipGetLastError();
 }
 

@@ -155,7 +155,8 @@ WgradSetup wgrad_setup(const niti_conv_desc* d, int64_t P, int64_t Q) {
         p.ncol_w = 0;
     }
     r.tap = !r.win && wgrad_tap_eligible(p);
-    r.plan = r.tap ? wgrad_tap_plan(d->k, d->c, npix) : wgrad_plan(d->k, r.win ? p.ncol_w : p.ncol, npix);
+    r.plan = r.tap ? wgrad_tap_plan(d->k, d->c, npix)
+                   : wgrad_plan(d->k, r.win ? p.ncol_w : p.ncol, npix, wgrad_dma_eligible(p) ? 768 : 256);
     return r;
 }
 

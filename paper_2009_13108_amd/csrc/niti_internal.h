@@ -77,7 +77,9 @@ struct WgradPlan {
     int32_t chunk;   // pixels per range
 };
 
-WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix);
+// groups: workgroups to aim for (256: one per CU for the general kernel;
+// the DMA kernel keeps three per CU busy).
+WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix, int64_t groups);
 hipError_t wgrad_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);
 bool wgrad_dma_eligible(const WgradProblem& p);
 hipError_t wgrad_dma_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream);

@@ -228,14 +228,14 @@ hipError_t launch_wgrad(const WgradProblem& p, const WgradPlan& plan, hipStream_
 
 }  // namespace
 
-// Split of the pixel reduction: enough workgroups to give every compute
-// unit one tile, but at least 8 steps of 64 pixels per workgroup.
-WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix) {
+// Split of the pixel reduction: about `groups` workgroups in all, but at
+// least 8 steps of 64 pixels per workgroup.
+WgradPlan wgrad_plan(int64_t K, int64_t ncol, int64_t npix, int64_t groups) {
     WgradPlan pl;
     pl.tbk = K <= 64 ? 64 : 128;
     const int64_t tiles = ((K + pl.tbk - 1) / pl.tbk) * ((ncol + 127) / 128);
     const int64_t steps = (npix + BKP - 1) / BKP;
-    int64_t splits = (256 + tiles - 1) / tiles;
+    int64_t splits = (groups + tiles - 1) / tiles;
     const int64_t max_splits = steps / 8 > 1 ? steps / 8 : 1;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
