@@ -52,6 +52,10 @@ int timing_begin(int family, hipStream_t s);
 void timing_end(int idx, hipStream_t s);
 bool igemm_dma_eligible(const IgemmBatch& b);
 hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
+// Weight operand resident in LDS (igemm_wres.hip): one problem, at most 128
+// output channels, a short reduction.
+bool igemm_wres_eligible(const IgemmBatch& b);
+hipError_t igemm_wres_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 
 // Weight-gradient contraction.  The pixel reduction is split into `splits`
 // ranges; split z stores its partial sums to part + z*K*ncol (with one split
