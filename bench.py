@@ -374,7 +374,7 @@ def summarize_kernel_trace(path):
     for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
         if "niti::" in name:
             print("%-58s %7d %11.1f %9.2f" % (name[:58], len(v), sum(v), sum(v) / len(v)))
-    fam = {"igemm": (r"niti::igemm_(dma_)?(main|fixup)<", r"niti::igemm_(dma_)?main<"),
+    fam = {"igemm": (r"niti::igemm_(dma_|wres_)?(main|fixup)<", r"niti::igemm_(dma_|wres_)?main<"),
            "wgrad": (r"niti::wgrad_\w*kernel<", r"niti::wgrad_\w*kernel<")}
     for f, (member, counter) in fam.items():
         tot = sum(sum(v) for n, v in per.items() if re.search(member, n))
@@ -398,7 +398,7 @@ def summarize_counters(path):
         per[r["Counter_Name"]][name] += float(r["Counter_Value"])
         disp[name].add(r["Dispatch_Id"])
     calls = {n: len(d) for n, d in disp.items()}
-    fam = {"igemm": (r"niti::\(anonymous namespace\)::igemm_(dma_)?(main|fixup)<", r"igemm_(dma_)?main<"),
+    fam = {"igemm": (r"niti::\(anonymous namespace\)::igemm_(dma_|wres_)?(main|fixup)<", r"igemm_(dma_|wres_)?main<"),
            "wgrad": (r"niti::\(anonymous namespace\)::wgrad_\w*kernel<", r"wgrad_\w*kernel<")}
     for cname, vals in per.items():
         for f, (member, counter) in fam.items():
