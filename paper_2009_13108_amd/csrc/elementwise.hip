@@ -145,40 +145,46 @@ __global__ __launch_bounds__(256) void reduce_max_flat_kernel(const int32_t* par
     block_publish_max32(st, slot, (uint32_t)m, red, snap);  // magnitudes <= 2^31
 }
 
-// The same sum for many splits (n % 4 == 0).  A workgroup takes 256
-// consecutive elements at a time: each wave reads them as one 1 KiB row piece
-// per split (lane l holds elements 4l .. 4l+3), wave w adds splits w, w + 4,
-// ... with eight 16-byte loads in flight, and the four wave sums are added in
-// LDS.  At most one workgroup per CU strides over the tensor, so one atomic
-// per CU folds the maximum in.
+// The same sum for many splits (n % 4 == 0).  A workgroup of four waves works
+// in groups of G waves; a group takes 256 consecutive elements at a time:
+// each of its waves reads them as one 1 KiB row piece per split (lane l holds
+// elements 4l .. 4l+3), member w adds splits w, w + G, ... with a batch of
+// 16-byte loads in flight (sixteen for G = 1, eight for G = 4), and the G
+// sums are added in LDS.  G is one below 32 splits (a wave holds a whole
+// column of them in one batch of loads) and four above.  At most one workgroup per CU strides over the tensor, so the
+// maximum costs one atomic per CU.
+template <int G>
 __global__ __launch_bounds__(256) void reduce_max_many_kernel(const int32_t* part, int splits, int32_t* g32,
                                                               int64_t n, niti_stats* st) {
+    constexpr int NG = 4 / G;   // element groups per pass
     __shared__ uint4 sums[4][64];
     __shared__ uint32_t red[4];
     const int slot = call_slot(st);
     const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int gi = wv / G, wm = wv - gi * G;
     uint32_t m = 0;
-    for (int64_t i0 = (int64_t)blockIdx.x * 256; i0 < n; i0 += (int64_t)gridDim.x * 256) {
+    for (int64_t i0 = ((int64_t)blockIdx.x * NG + gi) * 256; i0 - gi * 256 < n; i0 += (int64_t)gridDim.x * NG * 256) {
         const int64_t i = i0 + 4 * lane;
         uint4 a = make_uint4(0, 0, 0, 0);
         if (i < n) {
             const int32_t* src = part + i;
-            int z = wv;
-            for (; z + 28 < splits; z += 32) {
-                uint4 v[8];
+            constexpr int B = G == 1 ? 16 : 8;   // loads per batch
+            int z = wm;
+            for (; z + (B - 1) * G < splits; z += B * G) {
+                uint4 v[B];
 #pragma unroll
-                for (int u = 0; u < 8; u++) v[u] = *(const uint4*)(src + (int64_t)(z + 4 * u) * n);
+                for (int u = 0; u < B; u++) v[u] = *(const uint4*)(src + (int64_t)(z + G * u) * n);
 #pragma unroll
-                for (int u = 0; u < 8; u++) {
+                for (int u = 0; u < B; u++) {
                     a.x += v[u].x;
                     a.y += v[u].y;
                     a.z += v[u].z;
                     a.w += v[u].w;
                 }
             }
-            for (; z < splits; z += 4) {
+            for (; z < splits; z += G) {
                 const uint4 v = *(const uint4*)(src + (int64_t)z * n);
                 a.x += v.x;
                 a.y += v.y;
@@ -186,23 +192,27 @@ __global__ __launch_bounds__(256) void reduce_max_many_kernel(const int32_t* par
                 a.w += v.w;
             }
         }
-        sums[wv][lane] = a;
-        __syncthreads();
-        if (wv == 0 && i < n) {
+        if (G > 1) {
+            sums[wv][lane] = a;
+            __syncthreads();
+            if (wm == 0) {
 #pragma unroll
-            for (int h = 1; h < 4; h++) {
-                const uint4 v = sums[h][lane];
-                a.x += v.x;
-                a.y += v.y;
-                a.z += v.z;
-                a.w += v.w;
+                for (int h = 1; h < G; h++) {
+                    const uint4 v = sums[wv + h][lane];
+                    a.x += v.x;
+                    a.y += v.y;
+                    a.z += v.z;
+                    a.w += v.w;
+                }
             }
+        }
+        if (wm == 0 && i < n) {
             *(uint4*)(g32 + i) = a;
             const uint32_t mq =
                 max(max(mag32((int32_t)a.x), mag32((int32_t)a.y)), max(mag32((int32_t)a.z), mag32((int32_t)a.w)));
             m = max(m, mq);
         }
-        __syncthreads();   // sums is rewritten by the next pass
+        if (G > 1) __syncthreads();   // sums is rewritten by the next pass
     }
     block_publish_max32(st, slot, m, red, snap);  // magnitudes <= 2^31
 }
@@ -560,9 +570,20 @@ hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t
         return hipGetLastError();
     }
     if (n > 0 && n % 4 == 0 && splits > 8) {
-        int64_t blocks = (n + 255) / 256;
-        if (blocks > 256) blocks = 256;
-        hipLaunchKernelGGL(reduce_max_many_kernel, dim3((unsigned)blocks), dim3(256), 0, s, part, splits, g32, n, st);
+        // waves per 256 elements: one below 32 splits, else four
+        const int g = splits < 32 ? 1 : 4;
+        const int64_t passes = (n + 256 * (4 / g) - 1) / (256 * (4 / g));
+        const int64_t blocks = passes < 256 ? passes : 256;
+#define NITI_MANY(G)                                                                                              \
+    case G:                                                                                                       \
+        hipLaunchKernelGGL(reduce_max_many_kernel<G>, dim3((unsigned)blocks), dim3(256), 0, s, part, splits, g32,  \
+                           n, st);                                                                                \
+        break;
+        switch (g) {
+            NITI_MANY(1)
+            NITI_MANY(4)
+        }
+#undef NITI_MANY
         return hipGetLastError();
     }
     const int64_t blocks = (n + 255) / 256;
