@@ -369,6 +369,12 @@ hipError_t igemm_dispatch(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         maxM = b.p[i].M > maxM ? b.p[i].M : maxM;
         maxN = b.p[i].Nout > maxN ? b.p[i].Nout : maxN;
     }
+    // Small problems (a classifier head's back-propagation) get 64 x 64
+    // tiles, so that more than a handful of CUs take part.
+    int64_t tiles128 = 0;
+    for (int i = 0; i < b.nprob; i++)
+        tiles128 += (int64_t)((b.p[i].M + 127) / 128) * ((b.p[i].Nout + 127) / 128);
+    if (tiles128 < 64) return launch_igemm<64, 64>(b, ctl, stream);
     (void)maxM;
     if (maxN <= 64) return launch_igemm<256, 64>(b, ctl, stream);
     return launch_igemm<128, 128>(b, ctl, stream);
