@@ -242,6 +242,7 @@ __device__ __forceinline__ void run_tile(const IgemmProblem& P, int tm, int tn, 
         const int m = tm * TBM + wm * WTM + b * 32 + (lane & 31);
         const bool mvalid = m < P.M;
         int64_t ooff = 0;
+        uint32_t zs = 0;
         if (mvalid) {
             const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
             const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
@@ -250,6 +251,7 @@ __device__ __forceinline__ void run_tile(const IgemmProblem& P, int tm, int tn, 
             const int oh = (int)i0 * P.os + P.oa;
             const int ow = (int)j0 * P.os + P.ob;
             ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
+            if (P.zsib) zs = zero_siblings(P, oh, ow);
         }
 #pragma unroll
         for (int a = 0; a < FN; a++) {
@@ -292,6 +294,13 @@ __device__ __forceinline__ void run_tile(const IgemmProblem& P, int tm, int tn, 
                     }
                 }
             }
+        }
+        if (do_store && zs) {
+            for (int a = 0; a < FN; a++)
+                for (int jj = 0; jj < 4; jj++) {
+                    const int n0 = tn * TBN + wn * WTN + a * 32 + 8 * jj + 4 * (lane >> 5);
+                    if (n0 < P.Nout) store_zero_siblings(P, ooff + n0, zs, min(4, P.Nout - n0));
+                }
         }
     }
 }

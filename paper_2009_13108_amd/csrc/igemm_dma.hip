@@ -143,6 +143,7 @@ __device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn
         const int n0 = tn * BN + pc * 16;
         if (m >= P.M || n0 >= P.Nout) continue;
         int64_t ooff;
+        const int nv = min(16, P.Nout - n0);
         if (dense) {
             ooff = (int64_t)m * P.ldo + n0;   // the output grid is the pixel grid
         } else {
@@ -153,9 +154,9 @@ __device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn
             const int oh = (int)i0 * P.os + P.oa;
             const int ow = (int)j0 * P.os + P.ob;
             ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo + n0;
+            if (P.zsib) store_zero_siblings(P, ooff, zero_siblings(P, oh, ow), nv);
         }
         uint4 v = *(const uint4*)(lds + row * PITCH + pc * 16);
-        const int nv = min(16, P.Nout - n0);
         int8_t* dst = P.out + ooff;
         const bool full = nv == 16 && (((uintptr_t)dst) & 15) == 0;
         if (P.mask) {

@@ -113,11 +113,11 @@ __device__ __forceinline__ void wr_store16(const IgemmProblem& P, int64_t off, u
     }
 }
 
-template <int NF>
+template <int NF, int D>
 struct WrCfg {
     static constexpr int NROWS = 32 * NF;   // weight rows staged (channels, zero past Nout)
     // waves per SIMD the register budget is set for: two workgroups per CU
-    // for two channel fragments, one for four
+    // for two channel fragments or a one-step lead, else one
     static constexpr int MINW = NF <= 2 ? 4 : 2;
 };
 
@@ -144,7 +144,7 @@ template <int NF, int MODE, int D>
 __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList tl, int8_t* lds, const RoundK& rk,
                                            int relu, int do_store, int do_max, uint32_t& tmax, niti_stats* snap_st,
                                            int snap_slot, uint64_t& snap) {
-    using T = WrCfg<NF>;
+    using T = WrCfg<NF, D>;
     const int lane = threadIdx.x & 63;
     const int hi = lane >> 5;   // which 16 bytes of a 32-byte half this lane feeds
     const int nk = (P.Ktot + KSTEP - 1) / KSTEP;
@@ -303,10 +303,30 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
         }
         if (do_max) tmax = mx > tmax ? mx : tmax;
     }
+    // Zero siblings of the tasks' pixels (stride-2 classes without taps),
+    // in a pass of their own so that they cost no registers in the main loop.
+    if (do_store && P.zsib) {
+        for (int t = tl.first; t < tl.end; t += tl.step) {
+            const int m = t * 32 + (lane & 31);
+            if (m >= P.M) continue;
+            const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
+            const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
+            const uint32_t i0 = fdiv(rem, P.div_ow);
+            const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
+            const int oh = (int)i0 * P.os + P.oa;
+            const int ow = (int)j0 * P.os + P.ob;
+            const int64_t ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
+            const uint32_t zs = zero_siblings(P, oh, ow);
+            for (int a = 0; a < NF; a++) {
+                const int n0 = a * 32 + 16 * hi;
+                if (n0 < P.Nout) store_zero_siblings(P, ooff + n0, zs, min(16, P.Nout - n0));
+            }
+        }
+    }
 }
 
 template <int NF, int MODE, int D>
-__global__ __launch_bounds__(NT, WrCfg<NF>::MINW) void igemm_wres_main(IgemmBatch batch, IgemmCtl ctl, int tasks) {
+__global__ __launch_bounds__(NT, (WrCfg<NF, D>::MINW)) void igemm_wres_main(IgemmBatch batch, IgemmCtl ctl, int tasks) {
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
     const int slot = call_slot(st);
@@ -326,7 +346,7 @@ __global__ __launch_bounds__(NT, WrCfg<NF>::MINW) void igemm_wres_main(IgemmBatc
 }
 
 template <int NF, int MODE, int D>
-__global__ __launch_bounds__(NT, WrCfg<NF>::MINW) void igemm_wres_fixup(IgemmBatch batch, IgemmCtl ctl, int tasks) {
+__global__ __launch_bounds__(NT, (WrCfg<NF, D>::MINW)) void igemm_wres_fixup(IgemmBatch batch, IgemmCtl ctl, int tasks) {
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
     const int cur = st->cur & 1;
@@ -348,7 +368,7 @@ hipError_t launch_wres(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     static bool attr_done = false;
     static int resident = 0;
     const IgemmProblem& p = b.p[0];
-    const int lds = WrCfg<NF>::NROWS * (p.Ktot + 16);
+    const int lds = WrCfg<NF, D>::NROWS * (p.Ktot + 16);
     if (!attr_done) {
         constexpr int kMaxLds = 160 * 1024;
         hipError_t e = hipFuncSetAttribute((const void*)igemm_wres_main<NF, MODE, D>,
@@ -366,8 +386,8 @@ hipError_t launch_wres(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         attr_done = true;
     }
     // workgroups per CU: two when two weight copies fit the LDS and the
-    // registers allow (two channel fragments), else one
-    const int per_cu = (NF <= 2 && 2 * lds <= 160 * 1024) ? 2 : 1;
+    // registers allow, else one
+    const int per_cu = (WrCfg<NF, D>::MINW >= 4 && 2 * lds <= 160 * 1024) ? 2 : 1;
     const int tasks = (p.M + 31) / 32;
     int grid = (tasks + NWAVES - 1) / NWAVES;
     if (grid > per_cu * resident) grid = per_cu * resident;

@@ -384,6 +384,12 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
             p.wgt_bytes = (int64_t)C * c.T * c.U * K;
         }
     }
+    // A 1 x 1 stride-2 filter: only class (0, 0) has taps, and its kernel
+    // writes the zeros of the other three classes beside its own pixels.
+    if (st == 2 && b.nprob == 1 && b.p[0].oa == 0 && b.p[0].ob == 0 && zero_mask == 0xEu) {
+        b.p[0].zsib = 7;
+        zero_mask = 0;
+    }
     hipError_t e = repack_dgrad_run(w, (int8_t*)ws, cls, ncls, K, R, S, C, st, st, as_stream(stream));
     if (e != hipSuccess) return NITI_ERR_HIP;
     e = zero_classes_run(dx, d->n, d->h, d->w, d->c, st, zero_mask, as_stream(stream));

@@ -28,7 +28,36 @@ struct IgemmProblem {
     int64_t act_bytes;   // extent of act (bytes), for buffer bounds
     int64_t wgt_bytes;   // extent of wgt (bytes)
     int32_t win;         // act is a zero-padded image read in filter-row windows of L bytes
+    // Stride-2 class (0, 0) whose three sibling classes have no filter taps:
+    // with each stored piece the kernels also write zeros at the same
+    // channels of pixel (oh, ow + 1) (bit 0), (oh + 1, ow) (bit 1) and
+    // (oh + 1, ow + 1) (bit 2), inside the output tensor.
+    int32_t zsib;
 };
+
+// Which zero siblings of output pixel (oh, ow) lie inside the tensor
+// (bits as in IgemmProblem::zsib).
+__device__ __forceinline__ uint32_t zero_siblings(const IgemmProblem& P, int oh, int ow) {
+    const uint32_t c = ow + 1 < P.OW ? 1u : 0u, r = oh + 1 < P.OH ? 1u : 0u;
+    return (uint32_t)P.zsib & (c | (r << 1) | ((r & c) << 2));
+}
+// Zeros over nv bytes at dst.
+__device__ __forceinline__ void store_zero_bytes(int8_t* dst, int nv) {
+    if (nv == 16 && (((uintptr_t)dst) & 15) == 0) {
+        *(uint4*)dst = make_uint4(0, 0, 0, 0);
+    } else if (nv == 4 && (((uintptr_t)dst) & 3) == 0) {
+        *(uint32_t*)dst = 0u;
+    } else {
+        for (int e = 0; e < nv; e++) dst[e] = 0;
+    }
+}
+// Zeros at the siblings in bits of the piece at output offset off.
+__device__ __forceinline__ void store_zero_siblings(const IgemmProblem& P, int64_t off, uint32_t bits, int nv) {
+    const int64_t row = (int64_t)P.OW * P.ldo;
+    if (bits & 1u) store_zero_bytes(P.out + off + P.ldo, nv);
+    if (bits & 2u) store_zero_bytes(P.out + off + row, nv);
+    if (bits & 4u) store_zero_bytes(P.out + off + row + P.ldo, nv);
+}
 
 struct IgemmBatch {
     IgemmProblem p[kMaxProblems];

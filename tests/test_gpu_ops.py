@@ -112,6 +112,8 @@ CONV_CASES = [
     (2, 16, 7, 7, 32, 2, 2, 1, 0, False),
     # strided 1x1: three of four sub-pixel classes have no taps
     (2, 64, 14, 14, 128, 1, 1, 2, 0, True),
+    (2, 64, 7, 9, 256, 1, 1, 2, 0, False),
+    (2, 256, 9, 7, 128, 1, 1, 2, 0, True),
     # 1x1 over padding only: no class has taps, dx is all zeros
     (1, 4, 1, 1, 8, 1, 1, 2, 1, False),
 ]
