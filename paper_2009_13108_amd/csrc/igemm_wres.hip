@@ -30,6 +30,13 @@ constexpr int kWinW = 2;    // zero-padded image read in filter-row windows of L
 constexpr int NWAVES = 8;
 constexpr int NT = 64 * NWAVES;
 
+// Wait until this wave's vector memory operations (LDS DMA included) are done.
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// LDS bytes of the staged weights: NROWS rows of pitch Ktot + 16, in whole
+// 1 KB blocks (the staging DMA writes 64 slots of 16 bytes at a time).
+__host__ __device__ constexpr int wres_lds_bytes(int nrows, int ktot) { return (nrows * (ktot + 16) + 1023) / 1024 * 1024; }
+
 // Round one accumulator (Algorithm 3, or nearest) with the call's uniform
 // shift; RELU: v is already non-negative.  Returns the int8 in the low byte.
 template <bool RELU, bool RTN>
@@ -225,21 +232,39 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
         tapbase = 0;
     };
 
-    // ---- weights: rows [n][Ktot] into LDS with pitch kp (zero rows past Nout)
-    {
-        const int cpr = P.Ktot / 16;   // 16-byte chunks per row
-        for (int idx = threadIdx.x; idx < T::NROWS * cpr; idx += NT) {
-            const int n = idx / cpr, c = idx - n * cpr;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (n < P.Nout) v = *(const uint4*)(P.wgt + (int64_t)n * P.Ktot + c * 16);
-            *(uint4*)(lds + n * kp + c * 16) = v;
-        }
-    }
-
+    // ---- the first task's first D steps go out before the weights, so that
+    // both latencies overlap
     v4i bq[D][2];
     next_task_cursor(tl.first);
 #pragma unroll
     for (int u = 0; u < D; u++) load_step(bq[u]);
+
+    // ---- weights: rows [n][Ktot] into LDS with pitch kp, by DMA straight
+    // from memory.  LDS 16-byte slot s is chunk s % spr of row s / spr
+    // (spr = Ktot / 16 + 1: the last slot of a row is its pad); pad slots and
+    // rows past Nout read past the buffer end, which loads zeros.  Each wave
+    // instruction fills 64 consecutive slots.
+    {
+        const u32x4 wrs = raw_rsrc(P.wgt, (uint32_t)P.wgt_bytes);
+        const uint32_t spr = (uint32_t)(P.Ktot / 16 + 1);
+        const uint32_t nslots = (uint32_t)T::NROWS * spr;
+        const uint32_t lds0 = lds_address(lds);
+        const uint32_t step = (uint32_t)NT;   // slots per pass of the workgroup
+        const uint32_t dn = step / spr, dc = step - dn * spr;
+        uint32_t s0 = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x & ~63);
+        uint32_t n = (s0 + lane) / spr, c = (s0 + lane) - n * spr;
+        for (; s0 < nslots; s0 += step) {
+            const bool data = n < (uint32_t)P.Nout && c + 1 < spr;
+            lds_dma16_at(wrs, lds0, s0 * 16u, data ? n * (uint32_t)P.Ktot + c * 16u : kOOB, 0u);
+            n += dn;
+            c += dc;
+            if (c >= spr) {
+                c -= spr;
+                ++n;
+            }
+        }
+        wait_vm0();
+    }
     __syncthreads();   // weights staged
 
     // fragment reads: channel row (a * 32 + lane % 32), K bytes 32 h + 16 hi of step j
@@ -368,7 +393,7 @@ hipError_t launch_wres(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     static bool attr_done = false;
     static int resident = 0;
     const IgemmProblem& p = b.p[0];
-    const int lds = WrCfg<NF, D>::NROWS * (p.Ktot + 16);
+    const int lds = wres_lds_bytes(WrCfg<NF, D>::NROWS, p.Ktot);
     if (!attr_done) {
         constexpr int kMaxLds = 160 * 1024;
         hipError_t e = hipFuncSetAttribute((const void*)igemm_wres_main<NF, MODE, D>,
@@ -443,8 +468,10 @@ bool igemm_wres_eligible(const IgemmBatch& b) {
         if (p.C % KSTEP != 0 || p.L != p.S * p.C || p.Lpad != p.L || p.Ktot != p.R * p.L || p.R * p.S > 32)
             return false;
     }
+    if (p.wgt_bytes < (int64_t)p.Nout * p.Ktot || p.wgt_bytes >= ((int64_t)1 << 31)) return false;
     const int nf = p.Nout <= 64 ? 2 : 4;
-    const int64_t lds = (int64_t)32 * nf * (p.Ktot + 16);
+    if (p.Ktot > 8192) return false;
+    const int lds = wres_lds_bytes(32 * nf, p.Ktot);
     return nf == 2 ? lds <= 80 * 1024 : lds <= 152 * 1024;
 }
 
