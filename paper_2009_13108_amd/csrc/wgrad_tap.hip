@@ -45,6 +45,9 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
+// Wait until this wave's LDS reads are done (lgkmcnt 0, other counters free).
+__device__ __forceinline__ void wait_lds0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
 // Chunk swizzle of 64-byte pixel rows: conflict-free transpose reads over 8
 // consecutive pixels.
 __device__ __forceinline__ int swz(int pix) { return (pix >> 1) & 3; }
@@ -157,23 +160,54 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
 #pragma unroll
         for (int e = 0; e < 16; e++) acc[t][e] = 0;
 
-#pragma unroll
-    for (int s = 0; s < NS - 1; s++) issue();
-    for (int it = 0; it < nsteps; it++) {
-        wait_vm<(NS - 2) * (NTAP + 1)>();
-        __builtin_amdgcn_s_barrier();
-        issue();
-        const uint32_t st = lds0 + (uint32_t)((it % NS) * STAGE);
+    // Fragments of one stage: per 32-pixel half, the error fragment and the
+    // nine input fragments.  A stage's fragments are read during the previous
+    // stage's MFMAs, so the LDS latency is hidden behind them.
+    struct Frags {
+        v4i d[2];
+        v4i x[2][NTAP];
+    };
+    auto read_stage = [&](int j, Frags& F) {
+        const uint32_t st = lds0 + (uint32_t)((j % NS) * STAGE);
 #pragma unroll
         for (int ks = 0; ks < 2; ks++) {
-            const v4i fd = tr_frag<REG>(st + fo_d[ks].lo, st + fo_d[ks].hi, NTAP);
+            F.d[ks] = tr_frag<REG>(st + fo_d[ks].lo, st + fo_d[ks].hi, NTAP);
 #pragma unroll
-            for (int t = 0; t < NTAP; t++) {
-                const v4i fx = tr_frag<REG>(st + fo_x[ks].lo, st + fo_x[ks].hi, t);
-                acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fx, fd, acc[t], 0, 0, 0);
-            }
+            for (int t = 0; t < NTAP; t++) F.x[ks][t] = tr_frag<REG>(st + fo_x[ks].lo, st + fo_x[ks].hi, t);
         }
+    };
+    auto mfma_stage = [&](const Frags& F) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ks++)
+#pragma unroll
+            for (int t = 0; t < NTAP; t++)
+                acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.x[ks][t], F.d[ks], acc[t], 0, 0, 0);
+    };
+    // Stage it: stage it + 1 has landed (every wave's loads, hence the
+    // barrier) and every wave has its stage-it fragments in registers, so
+    // stage it's slot takes stage it + NS; then stage it + 1 is read while
+    // stage it's MFMAs run.
+    auto step = [&](int it, const Frags& cur, Frags& nxt) {
+        wait_vm<(NS - 2) * (NTAP + 1)>();
+        wait_lds0();
+        __builtin_amdgcn_s_barrier();
+        issue();
+        read_stage(it + 1, nxt);
+        mfma_stage(cur);
+    };
+
+#pragma unroll
+    for (int s = 0; s < NS; s++) issue();
+    wait_vm<(NS - 1) * (NTAP + 1)>();
+    __builtin_amdgcn_s_barrier();
+    Frags f0, f1;
+    read_stage(0, f0);
+    int it = 0;
+    for (; it + 1 < nsteps; it += 2) {
+        step(it, f0, f1);
+        step(it + 1, f1, f0);
     }
+    if (it < nsteps) step(it, f0, f1);
     wait_vm<0>();
 
     // acc[t] element 4*jj + i: channel c0 + 32*wc + 8*jj + 4*(lane/32) + i of
