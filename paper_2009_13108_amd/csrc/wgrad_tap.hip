@@ -118,9 +118,15 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     const uint32_t cbyte = (uint32_t)((((lane & 3) ^ swz(prow))) << 4);
     const uint32_t WC = (uint32_t)P.W * (uint32_t)P.C;
 
+    // Addresses of one stage's loads: LDS base of this wave's block, input
+    // offset of the lane's pixel, the taps outside the image, error offset.
+    struct Issue {
+        uint32_t st, base, outside, dv;
+    };
     int next = 0;
-    auto issue = [&]() {
-        const uint32_t st = lds0 + (uint32_t)((next % NS) * STAGE + wave * 1024);
+    auto prep = [&]() {
+        Issue q;
+        q.st = lds0 + (uint32_t)((next % NS) * STAGE + wave * 1024);
         const int pix = pbeg + next * PIX + prow;
         const bool ok = next < nsteps && pix < pend;
         const uint32_t pp = ok ? (uint32_t)pix : 0u;
@@ -136,19 +142,28 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
 #pragma unroll
         for (int s = 0; s < 3; s++) cols |= (uint32_t)((unsigned)(w0 + s) < (unsigned)P.W) << s;
         // bit r*3+s set: tap (r, s) outside the image (all taps for a pixel past the range)
-        uint32_t outside = ok ? ~((((rows & 1u) ? cols : 0u)) | (((rows & 2u) ? cols : 0u) << 3) |
-                                  (((rows & 4u) ? cols : 0u) << 6))
-                              : ~0u;
-        const uint32_t base = (uint32_t)(((int)n * P.H + h0) * P.W + w0) * (uint32_t)P.C + (uint32_t)c0 + cbyte;
-#pragma unroll
-        for (int t = 0; t < NTAP; t++) {
-            const uint32_t tap_off = (uint32_t)(t / 3) * WC + (uint32_t)(t % 3) * (uint32_t)P.C;
-            const uint32_t v = (__builtin_amdgcn_ubfe(outside, t, 1) << 31) | (base + tap_off);
-            lds_dma16(xrs, st + t * REG, v, 0);
-        }
-        const uint32_t dv = ok ? pp * (uint32_t)P.K + (uint32_t)k0 + cbyte : kOOB;
-        lds_dma16(drs, st + NTAP * REG, dv, 0);
+        q.outside = ok ? ~((((rows & 1u) ? cols : 0u)) | (((rows & 2u) ? cols : 0u) << 3) |
+                           (((rows & 4u) ? cols : 0u) << 6))
+                       : ~0u;
+        q.base = (uint32_t)(((int)n * P.H + h0) * P.W + w0) * (uint32_t)P.C + (uint32_t)c0 + cbyte;
+        q.dv = ok ? pp * (uint32_t)P.K + (uint32_t)k0 + cbyte : kOOB;
         next++;
+        return q;
+    };
+    // Load g of a stage: regions 0..8 the nine shifted input slices, 9 the error slice.
+    auto load = [&](const Issue& q, int g) {
+        if (g < NTAP) {
+            const uint32_t tap_off = (uint32_t)(g / 3) * WC + (uint32_t)(g % 3) * (uint32_t)P.C;
+            const uint32_t v = (__builtin_amdgcn_ubfe(q.outside, (uint32_t)g, 1) << 31) | (q.base + tap_off);
+            lds_dma16(xrs, q.st + g * REG, v, 0);
+        } else {
+            lds_dma16(drs, q.st + NTAP * REG, q.dv, 0);
+        }
+    };
+    auto issue = [&]() {
+        const Issue q = prep();
+#pragma unroll
+        for (int g = 0; g <= NTAP; g++) load(q, g);
     };
 
     const FragOff fo_x[2] = {frag_off(0, 32 * wc, lane), frag_off(32, 32 * wc, lane)};
@@ -187,13 +202,34 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     // barrier) and every wave has its stage-it fragments in registers, so
     // stage it's slot takes stage it + NS; then stage it + 1 is read while
     // stage it's MFMAs run.
+    // The ten loads, twenty fragment reads and eighteen MFMAs of a step are
+    // issued interleaved (scheduling barriers keep the order), so a load
+    // waiting for the memory pipeline holds up no MFMA.
     auto step = [&](int it, const Frags& cur, Frags& nxt) {
         wait_vm<(NS - 2) * (NTAP + 1)>();
         wait_lds0();
         __builtin_amdgcn_s_barrier();
-        issue();
-        read_stage(it + 1, nxt);
-        mfma_stage(cur);
+        const Issue q = prep();
+        const uint32_t st1 = lds0 + (uint32_t)(((it + 1) % NS) * STAGE);
+#pragma unroll
+        for (int g = 0; g <= NTAP; g++) {
+            load(q, g);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int f = 2 * g; f < 2 * g + 2; f++) {
+                const int ks = f / (NTAP + 1), i = f % (NTAP + 1);
+                if (i == 0)
+                    nxt.d[ks] = tr_frag<REG>(st1 + fo_d[ks].lo, st1 + fo_d[ks].hi, NTAP);
+                else
+                    nxt.x[ks][i - 1] = tr_frag<REG>(st1 + fo_x[ks].lo, st1 + fo_x[ks].hi, i - 1);
+            }
+#pragma unroll
+            for (int m = 2 * g; m < 2 * g + 2 && m < 2 * NTAP; m++) {
+                const int ks = m / NTAP, t = m % NTAP;
+                acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(cur.x[ks][t], cur.d[ks], acc[t], 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
 
 #pragma unroll
