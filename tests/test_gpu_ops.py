@@ -105,6 +105,10 @@ CONV_CASES = [
     (2, 32, 16, 16, 96, 1, 1, 2, 0, True),
     (1, 4, 32, 32, 64, 7, 7, 2, 3, True),
     (4, 128, 7, 7, 130, 3, 3, 1, 1, False),
+    # 64 input channels, stride 1: weights in registers, rows staged per block
+    (3, 64, 9, 7, 48, 3, 3, 1, 1, False),
+    (1, 64, 5, 5, 64, 3, 3, 1, 0, True),
+    (5, 64, 13, 11, 64, 3, 3, 1, 1, True),
     # few channels: padded-copy window path (s*c <= 64), windows of 16/32/64 bytes
     (2, 12, 9, 9, 16, 3, 3, 1, 1, True),
     (2, 8, 10, 10, 32, 3, 3, 2, 1, False),
