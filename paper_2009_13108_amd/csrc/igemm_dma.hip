@@ -75,22 +75,21 @@ struct Cfg {
     static_assert(BM * (BN + 16) <= LDS_BYTES, "output tile fits in the ring");
 };
 
-// Round one accumulator (Algorithm 3, or nearest) with the tile's uniform
-// shift; RELU: v is already non-negative.  Returns the int8 in the low byte.
+// Round one accumulator (Algorithm 3 in the closed form of niti_device.h,
+// or nearest) with the tile's uniform shift; RELU: v is already
+// non-negative.  Magnitudes are at most 2^31, so the 32-bit maximum is
+// exact.  Returns the int8 in the low byte.
 template <bool RELU, bool RTN>
-__device__ __forceinline__ uint32_t round_acc(int32_t v, const RoundK& k, uint64_t& tmax) {
+__device__ __forceinline__ uint32_t round_acc(int32_t v, const RoundK& k, uint32_t& tmax) {
     const uint32_t x = RELU ? (uint32_t)v : (v < 0 ? 0u - (uint32_t)v : (uint32_t)v);
-    tmax = (uint64_t)x > tmax ? (uint64_t)x : tmax;
-    uint32_t q = x >> k.bp;
-    uint32_t up;
+    tmax = x > tmax ? x : tmax;
+    uint32_t q;
     if (RTN) {
-        up = k.bp ? __builtin_amdgcn_ubfe(x, k.bp - 1, 1) : 0u;
+        q = x >> k.bp;
+        q = min(q + (k.bp ? __builtin_amdgcn_ubfe(x, k.bp - 1, 1) : 0u), 127u);
     } else {
-        const uint32_t thi = __builtin_amdgcn_ubfe(x, k.odd + k.h, k.h);
-        const uint32_t rlo = __builtin_amdgcn_ubfe(x, k.odd, k.h);
-        up = thi > rlo ? 1u : 0u;
+        q = round_psr_mag_fast(x, k);
     }
-    q = min(q + up, 127u);
     if (RELU) return q;
     const uint32_t sgn = (uint32_t)(v >> 31);
     return ((q ^ sgn) - sgn) & 0xFFu;
@@ -105,7 +104,7 @@ __device__ __forceinline__ void epilogue_regs(v16i (&acc)[T::FN][T::FM], int8_t*
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave % T::WGM_, wn = wave / T::WGM_;
     constexpr int PITCH = T::BN_ + 16;
-    uint64_t mx = 0;
+    uint32_t mx = 0;
 #pragma unroll
     for (int b = 0; b < T::FM; b++) {
         const int row = wm * T::WTM + b * 32 + (lane & 31);
@@ -126,7 +125,7 @@ __device__ __forceinline__ void epilogue_regs(v16i (&acc)[T::FN][T::FM], int8_t*
                 }
             }
     }
-    if (do_max) tmax = mx > tmax ? mx : tmax;
+    if (do_max) tmax = (uint64_t)mx > tmax ? (uint64_t)mx : tmax;
 }
 
 // Out-of-tile accumulators are zero (their operand rows were zero-filled),

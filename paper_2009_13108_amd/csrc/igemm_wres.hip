@@ -38,21 +38,27 @@ __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70);
 __host__ __device__ constexpr int wres_lds_bytes(int nrows, int ktot) { return (nrows * (ktot + 16) + 1023) / 1024 * 1024; }
 
 // Round one accumulator (Algorithm 3, or nearest) with the call's uniform
-// shift; RELU: v is already non-negative.  Returns the int8 in the low byte.
-template <bool RELU, bool RTN>
+// shift; RELU: the backward mask is applied later, the forward ReLU here.
+// FAST: the closed form of niti_device.h.  Returns the int8 in the low
+// byte.
+template <bool RELU, bool RTN, bool FAST>
 __device__ __forceinline__ uint32_t wr_round(int32_t v, const RoundK& k, uint32_t& tmax) {
+    if (RELU) v = v < 0 ? 0 : v;
     const uint32_t x = RELU ? (uint32_t)v : (v < 0 ? 0u - (uint32_t)v : (uint32_t)v);
     tmax = x > tmax ? x : tmax;
-    uint32_t q = x >> k.bp;
-    uint32_t up;
+    uint32_t q;
     if (RTN) {
-        up = k.bp ? __builtin_amdgcn_ubfe(x, k.bp - 1, 1) : 0u;
+        q = x >> k.bp;
+        q += k.bp ? __builtin_amdgcn_ubfe(x, k.bp - 1, 1) : 0u;
+        q = min(q, 127u);
+    } else if (FAST) {
+        q = round_psr_mag_fast(x, k);
     } else {
+        q = x >> k.bp;
         const uint32_t thi = __builtin_amdgcn_ubfe(x, k.odd + k.h, k.h);
         const uint32_t rlo = __builtin_amdgcn_ubfe(x, k.odd, k.h);
-        up = thi > rlo ? 1u : 0u;
+        q = min(q + (thi > rlo ? 1u : 0u), 127u);
     }
-    q = min(q + up, 127u);
     if (RELU) return q;
     const uint32_t sgn = (uint32_t)(v >> 31);
     return ((q ^ sgn) - sgn) & 0xFFu;
@@ -65,18 +71,14 @@ __device__ __forceinline__ uint32_t wr_round(int32_t v, const RoundK& k, uint32_
 // channels 8jj+4..8jj+7.  Two half-wave swaps (lanes 32..63 of the first
 // operand with lanes 0..31 of the second) leave lanes 0..31 with channels
 // 0..15 and lanes 32..63 with channels 16..31, as words (w0, w2, w1, w3).
-template <bool RELU, bool RTN>
+template <bool RELU, bool RTN, bool FAST>
 __device__ __forceinline__ uint4 wr_round_fragment(const v16i& acc, const RoundK& rk, uint32_t& mx) {
     uint32_t w[4];
 #pragma unroll
     for (int jj = 0; jj < 4; jj++) {
         uint32_t packed = 0;
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            int32_t v = acc[4 * jj + i];
-            if (RELU) v = v < 0 ? 0 : v;
-            packed |= wr_round<RELU, RTN>(v, rk, mx) << (8 * i);
-        }
+        for (int i = 0; i < 4; i++) packed |= wr_round<RELU, RTN, FAST>(acc[4 * jj + i], rk, mx) << (8 * i);
         w[jj] = packed;
     }
     const auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
@@ -318,10 +320,10 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
         for (int a = 0; a < NF; a++) {
             uint4 v;
             switch (mode_sel) {
-                case 0: v = wr_round_fragment<false, false>(acc[a], rk, mx); break;
-                case 1: v = wr_round_fragment<true, false>(acc[a], rk, mx); break;
-                case 2: v = wr_round_fragment<false, true>(acc[a], rk, mx); break;
-                default: v = wr_round_fragment<true, true>(acc[a], rk, mx); break;
+                case 0: v = wr_round_fragment<false, false, true>(acc[a], rk, mx); break;
+                case 1: v = wr_round_fragment<true, false, true>(acc[a], rk, mx); break;
+                case 2: v = wr_round_fragment<false, true, false>(acc[a], rk, mx); break;
+                default: v = wr_round_fragment<true, true, false>(acc[a], rk, mx); break;
             }
             const int n0 = a * 32 + 16 * hi;
             if (do_store && ooff >= 0 && n0 < P.Nout) wr_store16(P, ooff + n0, v, min(16, P.Nout - n0));

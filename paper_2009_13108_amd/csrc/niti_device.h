@@ -42,6 +42,10 @@ struct RoundK {
     uint64_t fmask;  // bp low bits
     uint64_t hmask;  // h low bits
     int rtn;         // 1: round to nearest instead
+    // Closed form of the 32-bit rounding (round_psr_mag_fast): with
+    // r = (x >> odd) & hmask, the rounded value is (x + r * k1 + c0) >> bp.
+    int32_t k1;      // -(2^h + 1) * 2^odd
+    int32_t c0;      // (2^2h - 2^h) * 2^odd
 };
 
 __host__ __device__ inline RoundK make_round(int bp, int mode) {
@@ -52,7 +56,20 @@ __host__ __device__ inline RoundK make_round(int bp, int mode) {
     k.fmask = bp >= 64 ? ~0ull : ((1ull << bp) - 1ull);
     k.hmask = (1ull << k.h) - 1ull;
     k.rtn = mode == NITI_ROUND_RTN;
+    k.k1 = k.h < 16 ? -(int32_t)(((1u << k.h) + 1u) << k.odd) : 0;
+    k.c0 = k.h < 16 ? (int32_t)((((1u << (2 * k.h)) - (1u << k.h))) << k.odd) : 0;
     return k;
+}
+
+// Algorithm 3 in closed form for 32-bit data.  Write the fraction (odd
+// bit dropped) as thi * 2^h + rlo.  Adding (2^2h - 2^h - rlo (2^h + 1))
+// 2^odd to x raises the integer part by one exactly when thi > rlo and
+// leaves it otherwise, so q + up = (x + rlo * k1 + c0) >> bp.
+// Magnitude form (x = |v| <= 2^31): exact for every bp <= 31.
+__device__ __forceinline__ uint32_t round_psr_mag_fast(uint32_t x, const RoundK& k) {
+    const uint32_t rlo = __builtin_amdgcn_ubfe(x, k.odd, k.h);
+    const uint32_t z = (uint32_t)(__mul24((int32_t)rlo, k.k1) + k.c0);
+    return min((x + z) >> k.bp, 127u);
 }
 
 // Pseudo stochastic rounding of an unsigned 32-bit magnitude (Algorithm 3):
@@ -60,15 +77,9 @@ __host__ __device__ inline RoundK make_round(int bp, int mode) {
 // bit dropped); q is bumped when the upper half of f exceeds the lower half,
 // the lower half standing in for a random draw.  Held at 127.
 __device__ __forceinline__ uint32_t round_mag32(uint32_t x, const RoundK& k) {
+    if (!k.rtn) return round_psr_mag_fast(x, k);
     uint32_t q = x >> k.bp;
-    if (k.rtn) {
-        q += k.bp ? ((x >> (k.bp - 1)) & 1u) : 0u;
-    } else {
-        uint32_t f = (x & (uint32_t)k.fmask) >> k.odd;
-        uint32_t thi = f >> k.h;
-        uint32_t rlo = f & (uint32_t)k.hmask;
-        q += thi > rlo ? 1u : 0u;
-    }
+    q += k.bp ? ((x >> (k.bp - 1)) & 1u) : 0u;
     return q < 127u ? q : 127u;
 }
 

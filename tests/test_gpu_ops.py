@@ -228,6 +228,33 @@ def test_round_psr_parity(n):
         assert (host(y) == oracle.round_fixed(x, bp, oracle.RTN)).all()
 
 
+def test_round_psr_every_shift():
+    """Every binary point 0..31, both parities of the fraction split, on the
+    full int32 range and on values at the rounding decision (upper half of
+    the fraction equal to the lower half, one above, one below)."""
+    import torch
+    say("round_psr every shift")
+    rng = np.random.default_rng(77)
+    for bp in range(32):
+        odd, h = bp & 1, (bp - (bp & 1)) // 2
+        vals = [0, 1, -1, 2 ** 31 - 1, -(2 ** 31), 2 ** 31 - 2, -(2 ** 31) + 1]
+        q = rng.integers(0, 128, 64)
+        for lo in rng.integers(0, 1 << h, 8) if h else [0]:
+            for d in (-1, 0, 1):
+                hi_ = min(max(int(lo) + d, 0), (1 << h) - 1) if h else 0
+                f = ((hi_ << h) | int(lo)) << odd
+                for qq in q[:8]:
+                    v = (int(qq) << bp) + f
+                    if v < 2 ** 31:
+                        vals += [v, -v]
+        vals += list(rng.integers(-(2 ** 31), 2 ** 31, 2000))
+        x = np.array(vals, dtype=np.int64).astype(np.int32)
+        y = torch.empty(x.size, dtype=torch.int8, device="cuda")
+        niti.round_psr(dev(x), y, bp, 7, None)
+        torch.cuda.synchronize()
+        assert (host(y) == oracle.round_fixed(x, bp)).all(), bp
+
+
 def test_round_psr_worked_examples():
     import json, os, torch
     g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "psr_examples.json")))
