@@ -114,6 +114,10 @@ CONV_CASES = [
     (2, 8, 10, 10, 32, 3, 3, 2, 1, False),
     (3, 4, 13, 12, 48, 5, 5, 2, 2, True),
     (2, 16, 7, 7, 32, 2, 2, 1, 0, False),
+    # strided 3x3 back-propagation over 64 error channels (odd sizes: sub-pixel
+    # classes of unequal size)
+    (2, 32, 9, 11, 64, 3, 3, 2, 1, True),
+    (1, 64, 8, 8, 128, 3, 3, 2, 1, False),
     # strided 1x1: three of four sub-pixel classes have no taps
     (2, 64, 14, 14, 128, 1, 1, 2, 0, True),
     (2, 64, 7, 9, 256, 1, 1, 2, 0, False),
