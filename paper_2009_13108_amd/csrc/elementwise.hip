@@ -256,12 +256,41 @@ __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_
 
 // Discrete update, the finishing launch of its call:
 // g = round(g32, max(0, B(g32) - mu)); w <- clamp(w - g).
-__global__ void update_kernel(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode, niti_stats* st,
-                              uint32_t static_flags) {
+__global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict__ g32, int64_t n, int mu, int mode,
+                              niti_stats* st, uint32_t static_flags) {
     const int bp = block_bp(load_acc(st, st->cur & 1), mu);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // Groups of four weights (one 4-byte word of w, 16 bytes of g32), two
+    // groups per thread and pass with both loads issued before any store.
+    const bool vec = ((((uintptr_t)w) | ((uintptr_t)g32)) & 15) == 0;
+    const int64_t nq = vec ? n >> 2 : 0;
+    for (int64_t q0 = tid; q0 < nq; q0 += 2 * stride) {
+        int4 g[2];
+        uint32_t wv[2];
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            const int64_t q = q0 + j * stride;
+            g[j] = q < nq ? ((const int4*)g32)[q] : make_int4(0, 0, 0, 0);
+            wv[j] = q < nq ? ((const uint32_t*)w)[q] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            const int64_t q = q0 + j * stride;
+            if (q >= nq) continue;
+            const int32_t gv[4] = {g[j].x, g[j].y, g[j].z, g[j].w};
+            uint32_t out = 0;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                int v = (int)(int8_t)(wv[j] >> (8 * e)) - (int)round_i32(gv[e], rk);
+                v = v > 127 ? 127 : (v < -127 ? -127 : v);
+                out |= (uint32_t)(uint8_t)v << (8 * e);
+            }
+            ((uint32_t*)w)[q] = out;
+        }
+    }
+    for (int64_t i = 4 * nq + tid; i < n; i += stride) {
         int v = (int)w[i] - (int)round_i32(g32[i], rk);
         v = v > 127 ? 127 : (v < -127 ? -127 : v);
         w[i] = (int8_t)v;
@@ -282,8 +311,14 @@ __device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
     return prod * 2;
 }
 
-__global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
-                            int64_t* e64, int64_t batch, int64_t classes, niti_stats* st) {
+// One wave per sample.  NPL > 0: every lane keeps its NPL entries (lane,
+// lane + 64, ...) in registers, so the logits are read once and e64 is only
+// written (classes <= 64 * NPL); NPL == 0 streams any number of classes
+// through e64.
+template <int NPL>
+__global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __restrict__ s_logits,
+                            const int32_t* __restrict__ labels, int64_t* __restrict__ e64, int64_t batch,
+                            int64_t classes, niti_stats* st) {
     const int slot = call_slot(st);
     const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
@@ -299,40 +334,90 @@ __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const 
     if (sample < batch) {
         const int8_t* a = logits + sample * classes;
         int64_t* e = e64 + sample * classes;
-        int64_t C = 0;
-        if (s_a <= -7) {
-            const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
-            for (int64_t i = lane; i < classes; i += 64) {
-                const int64_t ai = a[i];
-                const int64_t t = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
-                e[i] = t;
-                C += t;
+        const int32_t y = labels[sample];
+        const bool taylor = s_a <= -7;
+        const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
+        if constexpr (NPL > 0) {
+            int av[NPL];
+#pragma unroll
+            for (int j = 0; j < NPL; j++) {
+                const int i = lane + 64 * j;
+                av[j] = i < classes ? (int)a[i] : 0;
+            }
+            int64_t t[NPL];
+            int64_t C = 0;
+            if (taylor) {
+#pragma unroll
+                for (int j = 0; j < NPL; j++) {
+                    const int64_t ai = av[j];
+                    t[j] = lane + 64 * j < classes ? ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai : 0;
+                    C += t[j];
+                }
+            } else {
+                int64_t mx = INT64_MIN;
+#pragma unroll
+                for (int j = 0; j < NPL; j++)
+                    if (lane + 64 * j < classes) {
+                        const int64_t xh = loss_xhat(av[j], s_a);
+                        mx = xh > mx ? xh : mx;
+                    }
+                const int64_t p = wave_max_i64(mx) - 10;
+#pragma unroll
+                for (int j = 0; j < NPL; j++) {
+                    int64_t xt = loss_xhat(av[j], s_a) - p;
+                    xt = xt < 0 ? 0 : xt;
+                    t[j] = lane + 64 * j < classes ? (int64_t)1 << xt : 0;
+                    C += t[j];
+                }
+            }
+            C = wave_sum_i64(C);
+            // The owner of the label's entry subtracts C (a label outside
+            // [0, classes) contributes no term).
+            const bool own = y >= 0 && y < classes && (y & 63) == lane;
+#pragma unroll
+            for (int j = 0; j < NPL; j++) {
+                const int i = lane + 64 * j;
+                if (own && (y >> 6) == j) t[j] -= C;
+                if (i < classes) {
+                    e[i] = t[j];
+                    const uint64_t mg = t[j] < 0 ? 0ull - (uint64_t)t[j] : (uint64_t)t[j];
+                    m = mg > m ? mg : m;
+                }
             }
         } else {
-            int64_t mx = INT64_MIN;
-            for (int64_t i = lane; i < classes; i += 64) {
-                const int64_t xh = loss_xhat(a[i], s_a);
-                mx = xh > mx ? xh : mx;
+            int64_t C = 0;
+            if (taylor) {
+                for (int64_t i = lane; i < classes; i += 64) {
+                    const int64_t ai = a[i];
+                    const int64_t t = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
+                    e[i] = t;
+                    C += t;
+                }
+            } else {
+                int64_t mx = INT64_MIN;
+                for (int64_t i = lane; i < classes; i += 64) {
+                    const int64_t xh = loss_xhat(a[i], s_a);
+                    mx = xh > mx ? xh : mx;
+                }
+                mx = wave_max_i64(mx);
+                const int64_t p = mx - 10;
+                for (int64_t i = lane; i < classes; i += 64) {
+                    int64_t xt = loss_xhat(a[i], s_a) - p;
+                    xt = xt < 0 ? 0 : xt;
+                    const int64_t t = (int64_t)1 << xt;
+                    e[i] = t;
+                    C += t;
+                }
             }
-            mx = wave_max_i64(mx);
-            const int64_t p = mx - 10;
+            C = wave_sum_i64(C);
+            // Lane i owns entries i, i+64, ...; the owner of the label's entry
+            // subtracts C (a label outside [0, classes) contributes no term).
+            if (y >= 0 && y < classes && (y & 63) == lane) e[y] -= C;
             for (int64_t i = lane; i < classes; i += 64) {
-                int64_t xt = loss_xhat(a[i], s_a) - p;
-                xt = xt < 0 ? 0 : xt;
-                const int64_t t = (int64_t)1 << xt;
-                e[i] = t;
-                C += t;
+                const int64_t v = e[i];
+                const uint64_t mg = v < 0 ? 0ull - (uint64_t)v : (uint64_t)v;
+                m = mg > m ? mg : m;
             }
-        }
-        C = wave_sum_i64(C);
-        const int32_t y = labels[sample];
-        // Lane i owns entries i, i+64, ...; the owner of the label's entry
-        // subtracts C (a label outside [0, classes) contributes no term).
-        if (y >= 0 && y < classes && (y & 63) == lane) e[y] -= C;
-        for (int64_t i = lane; i < classes; i += 64) {
-            const int64_t v = e[i];
-            const uint64_t mg = v < 0 ? 0ull - (uint64_t)v : (uint64_t)v;
-            m = mg > m ? mg : m;
         }
     }
     if (flag_sa && threadIdx.x == 0 && blockIdx.x == 0)
@@ -340,12 +425,22 @@ __global__ void loss_kernel(const int8_t* logits, const int8_t* s_logits, const 
     block_publish_max(st, slot, m, snap);
 }
 
-__global__ void loss_round_kernel(const int64_t* e64, int8_t* err, int64_t n, int mode, niti_stats* st) {
+// Rounds e64 with the call's block binary point (finishing launch); each
+// thread issues its LR loads before any store.
+constexpr int LR = 4;
+__global__ void loss_round_kernel(const int64_t* __restrict__ e64, int8_t* __restrict__ err, int64_t n, int mode,
+                                  niti_stats* st) {
     const int bp = block_bp(load_acc(st, st->cur & 1), 7);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        err[i] = round_i64(e64[i], rk);
+    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += LR * stride) {
+        int64_t v[LR];
+#pragma unroll
+        for (int j = 0; j < LR; j++) v[j] = i0 + j * stride < n ? e64[i0 + j * stride] : 0;
+#pragma unroll
+        for (int j = 0; j < LR; j++)
+            if (i0 + j * stride < n) err[i0 + j * stride] = round_i64(v[j], rk);
+    }
     if (is_finisher()) finish_call(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0);
 }
 
@@ -604,12 +699,17 @@ hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t*
                     hipStream_t s) {
     const int per_block = kThreads / 64;
     const int64_t blocks = (batch + per_block - 1) / per_block;
-    hipLaunchKernelGGL(loss_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(kThreads), 0, s,
-                       logits, s_logits, labels, e64, batch, classes, st);
+    const dim3 grid((unsigned)(blocks > 0 ? blocks : 1));
+    if (classes <= 64 * 16)
+        hipLaunchKernelGGL(loss_kernel<16>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e64, batch,
+                           classes, st);
+    else
+        hipLaunchKernelGGL(loss_kernel<0>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e64, batch,
+                           classes, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = batch * classes;
-    hipLaunchKernelGGL(loss_round_kernel, dim3(grid_for(n, 8)), dim3(kThreads), 0, s, e64, err, n, mode,
+    hipLaunchKernelGGL(loss_round_kernel, dim3(grid_for(n, LR)), dim3(kThreads), 0, s, e64, err, n, mode,
                        st);
     return hipGetLastError();
 }

@@ -370,6 +370,7 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
 namespace {
 
 hipError_t igemm_dispatch(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
+    if (igemm_small_eligible(b)) return igemm_small_run(b, ctl, stream);
     if (igemm_wres_eligible(b)) return igemm_wres_run(b, ctl, stream);
     if (igemm_dma_eligible(b)) return igemm_dma_run(b, ctl, stream);
     // All problems of a batch share the tile shape; pick it from the largest.

@@ -79,6 +79,10 @@ hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 // timing is off; end closes that record on the same stream.
 int timing_begin(int family, hipStream_t s);
 void timing_end(int idx, hipStream_t s);
+// Few outputs, long reduction (igemm_small.hip): a single plain matrix
+// product of at most 1024 rows.
+bool igemm_small_eligible(const IgemmBatch& b);
+hipError_t igemm_small_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 bool igemm_dma_eligible(const IgemmBatch& b);
 hipError_t igemm_dma_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 // Weight operand resident in LDS (igemm_wres.hip): one problem, at most 128

@@ -44,6 +44,12 @@ GEMM_CASES = [
     (70001, 100, 64, True, oracle.PSR, "w"),      # 256x128 tiles, ragged M
     (4100, 4096, 272, False, oracle.PSR, "w"),    # 256x256 tiles, ragged M and K
     (2000, 300, 512, False, oracle.RTN, "e5"),    # 128x128 tiles
+    # few outputs, long reduction: reduction split over the waves of a tile
+    (128, 1000, 512, False, oracle.PSR, "w"),     # classifier head forward
+    (128, 512, 1000, True, oracle.PSR, "e5"),     # rows of 1000 bytes (8-byte aligned)
+    (96, 40, 5000, False, oracle.RTN, "w"),       # several load batches per wave
+    (1024, 66, 77, True, oracle.PSR, "w"),        # largest row count of that path
+    (1025, 30, 200, False, oracle.PSR, "w"),      # one row more: tiled kernels
 ]
 
 
@@ -124,6 +130,8 @@ CONV_CASES = [
     (2, 256, 9, 7, 128, 1, 1, 2, 0, True),
     # 1x1 over padding only: no class has taps, dx is all zeros
     (1, 4, 1, 1, 8, 1, 1, 2, 1, False),
+    # classifier head as a 1x1 convolution: 512 features, 1000 classes
+    (128, 512, 1, 1, 1000, 1, 1, 1, 0, True),
 ]
 
 
@@ -278,7 +286,7 @@ def test_round_psr_worked_examples():
 
 
 @pytest.mark.parametrize("s_a", [-40, -22, -13, -9, -7, -6, -3, 0, 5, 15, 16, 100])
-@pytest.mark.parametrize("shape", [(256, 10), (128, 1000), (3, 65)])
+@pytest.mark.parametrize("shape", [(256, 10), (128, 1000), (3, 65), (5, 1024), (4, 1500)])
 def test_int_ce_loss_grad_parity(s_a, shape):
     import torch
     say("loss", s_a, shape)
