@@ -3,38 +3,49 @@
 //
 //   g32[k][(r*3 + s)*C + c] = sum over pixels pix of dy[pix][k] * x[n][oh*sh - ph + r][ow*sw - pw + s][c]
 //
-// The nine taps of one 64-channel chunk read the same input pixels, shifted.
+// The nine taps of one channel chunk read the same input pixels, shifted.
 // A workgroup therefore owns an output tile of 64 output channels x (all nine
-// taps of a 64-channel chunk) and, per stage of 64 output pixels, loads the
-// nine shifted 64-pixel x 64-byte slices and the 64 x 64-byte error slice.
+// taps of a 32-channel chunk) and, per stage of 128 output pixels, loads the
+// nine shifted 128-pixel x 32-byte slices and the 128 x 64-byte error slice.
 // The nine slices of one stage touch the same few input rows at nearly the
 // same time, so they meet in L2 instead of re-reading memory past it, which
 // is what bounds a kernel that tiles the im2col columns independently.
 //
-// Layout of a stage in LDS: nine x regions [64 pixels][64 bytes] (one per tap)
-// and one dy region [64 pixels][64 bytes], 16-byte chunks XOR-swizzled by
-// pixel; the MFMA operands come out of them with transpose reads (the same
-// fragment reader as wgrad_dma.hip).  Wave (wk, wc) of four computes output
-// channels k0 + 32*wk .. +31 x channels c0 + 32*wc .. +31 for all nine taps:
-// per 32 pixels one error fragment and nine input fragments feed nine MFMAs.
+// The pixel reduction is split over about one workgroup per CU and every
+// workgroup writes its partial tile, which the split-sum pass reads back:
+// that traffic is the workgroup count times the tile size.  A 32-channel
+// chunk halves it against a 64-channel one, for 10% more operand loads per
+// multiply-add (the error slice is shared by fewer taps' columns).
 //
-// Loads.  Wave w fills pixels 16w .. 16w+15 of every region of a stage (ten
-// direct-to-LDS loads of 1 KiB, issued as inline assembly so the compiler
-// does not wait for the whole ring before each transpose read); a lane keeps
-// the input offset of its pixel
-// and a 9-bit mask of the taps that fall outside the image, so each tap's
-// load is one add and one bit test.  Each workgroup stores its partial tile
-// to its own slice; the split-sum pass adds the slices.
+// Layout of a stage in LDS: nine x regions [128 pixels][32 bytes] (one per
+// tap; eight consecutive rows are 256 contiguous bytes, so transpose reads
+// need no swizzle) and one dy region [128 pixels][64 bytes] (16-byte chunks
+// XOR-swizzled by pixel).  The MFMA operands come out of them with transpose
+// reads (the same fragment reader as wgrad_dma.hip).  Wave (wk, ph) of four
+// computes output channels k0 + 32*wk .. +31 x the 32 channels for all nine
+// taps over pixel half ph of each stage: per 32 pixels one error fragment and
+// nine input fragments feed nine MFMAs.  The two pixel halves' sums meet in
+// LDS at the end.
+//
+// Loads.  Wave w fills pixels 32w .. 32w+31 of the nine x regions and pixels
+// 32w .. 32w+31 of the dy region (eleven direct-to-LDS loads of 1 KiB,
+// issued as inline assembly so the compiler does not wait for the whole ring
+// before each transpose read); a lane keeps the input offset of its pixel and
+// a 9-bit mask of the taps that fall outside the image, so each tap's load is
+// one add and one bit test.
 #include "niti_internal.h"
 
 namespace niti {
 
 namespace {
 
-constexpr int PIX = 64;                 // output pixels per stage
+constexpr int PIX = 128;                  // output pixels per stage
 constexpr int NTAP = 9;
-constexpr int REG = PIX * 64;           // bytes of one [64 pixels][64 bytes] region
-constexpr int STAGE = (NTAP + 1) * REG; // nine tap regions and the error region
+constexpr int CW = 32;                    // channels per tile
+constexpr int XREG = PIX * CW;            // bytes of one [128 pixels][32 bytes] x region
+constexpr int DOFF = NTAP * XREG;         // dy region [128 pixels][64 bytes]
+constexpr int STAGE = DOFF + PIX * 64;
+constexpr int LOADS = NTAP + 2;           // loads per wave and stage
 constexpr uint32_t kOOB = 0x80000000u;
 
 typedef __attribute__((address_space(3))) v2i lds_v2i;
@@ -52,15 +63,16 @@ __device__ __forceinline__ void wait_lds0() { __builtin_amdgcn_s_waitcnt(0xC07F)
 // consecutive pixels.
 __device__ __forceinline__ int swz(int pix) { return (pix >> 1) & 3; }
 
-// Lane byte offsets, within a [pixel][64 bytes] region, of the two transpose
-// reads that give a 32 x 32-pixel fragment: the lane gets 16 pixel bytes
-// (pixels p0 + 16*(lane/32) ...) of column cbase + lane%32.  They depend on
-// the lane, p0 and cbase only, so a workgroup computes them once.
+// Lane byte offsets, within a region, of the two transpose reads that give a
+// 32 x 32-pixel fragment: the lane gets 16 pixel bytes (pixels p0 +
+// 16*(lane/32) ...) of column cbase + lane%32.  They depend on the lane, p0
+// and cbase only, so a workgroup computes them once.
 struct FragOff {
     int lo, hi;
 };
 
-__device__ __forceinline__ FragOff frag_off(int p0, int cbase, int lane) {
+// 64-byte rows (dy), swizzled.
+__device__ __forceinline__ FragOff frag_off64(int p0, int cbase, int lane) {
     const int g = lane >> 4, j = lane & 15;
     const int chunk = (cbase >> 4) + (g & 1);
     const int prow = p0 + 16 * (g >> 1) + (j >> 1);
@@ -71,14 +83,24 @@ __device__ __forceinline__ FragOff frag_off(int p0, int cbase, int lane) {
     return f;
 }
 
-// Fragment of region `reg` (a compile-time region index, folded into the
-// instructions' offset field) from LDS byte addresses lo / hi of region 0.
-template <int REG_BYTES>
-__device__ __forceinline__ v4i tr_frag(uint32_t lo_addr, uint32_t hi_addr, int reg) {
+// 32-byte rows (x), all 32 columns, unswizzled.
+__device__ __forceinline__ FragOff frag_off32(int p0, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int prow = p0 + 16 * (g >> 1) + (j >> 1);
+    const int col = ((g & 1) << 4) + (j & 1) * 8;
+    FragOff f;
+    f.lo = prow * 32 + col;
+    f.hi = (prow + 8) * 32 + col;
+    return f;
+}
+
+// Fragment at LDS byte addresses lo / hi plus off (a constant after
+// unrolling, folded into the instructions' offset field).
+__device__ __forceinline__ v4i tr_frag(uint32_t lo_addr, uint32_t hi_addr, int off) {
     const lds_v2i* lo = (const lds_v2i*)(uintptr_t)lo_addr;
     const lds_v2i* hi = (const lds_v2i*)(uintptr_t)hi_addr;
-    const v2i a = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(lo + reg * (REG_BYTES / 8)));
-    const v2i b = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(hi + reg * (REG_BYTES / 8)));
+    const v2i a = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(lo + off / 8));
+    const v2i b = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(hi + off / 8));
     v4i r;
     r[0] = a[0];
     r[1] = a[1];
@@ -95,14 +117,14 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int wk = wave & 1, wc = wave >> 1;
+    const int wk = wave & 1, ph = wave >> 1;
     const int ntiles = tiles_c * tiles_k;
     const int per_xcd = (ntiles * splits + 7) / 8;
     const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
     if ((blockIdx.x >> 3) >= per_xcd || item >= ntiles * splits) return;
     const int split = item / ntiles;
     const int tile = item - split * ntiles;
-    const int c0 = (tile % tiles_c) * 64;
+    const int c0 = (tile % tiles_c) * CW;
     const int k0 = (tile / tiles_c) * 64;
     const int pbeg = split * P.chunk;
     const int pend = min(P.npix, pbeg + P.chunk);
@@ -112,22 +134,31 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     const u32x4 drs = raw_rsrc(P.dy, (uint32_t)P.dy_bytes);
     const uint32_t lds0 = lds_address(lds);
 
-    // This lane's pixel row in every region and the chunk it fetches so that
-    // it lands in its fixed slot (lane l -> row l/4, slot l%4).
-    const int prow = 16 * wave + (lane >> 2);
-    const uint32_t cbyte = (uint32_t)((((lane & 3) ^ swz(prow))) << 4);
+    // This lane's rows: x pixel 32*wave + lane/2 (chunk lane%2; a 1 KiB block
+    // of an x region is 32 rows of 32 bytes) and dy pixels 32*wave + 16*u +
+    // lane/4 (chunk lane%4, swizzled; a block of the dy region is 16 rows).
+    const int xrow = 32 * wave + (lane >> 1);
+    const uint32_t xbyte = (uint32_t)((lane & 1) << 4);
+    int drow[2];
+    uint32_t dbyte[2];
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        drow[u] = 32 * wave + 16 * u + (lane >> 2);
+        dbyte[u] = (uint32_t)(((lane & 3) ^ swz(drow[u])) << 4);
+    }
     const uint32_t WC = (uint32_t)P.W * (uint32_t)P.C;
 
-    // Addresses of one stage's loads: LDS base of this wave's block, input
-    // offset of the lane's pixel, the taps outside the image, error offset.
+    // Addresses of one stage's loads: LDS stage base, input offset of the
+    // lane's x pixel, the taps outside the image, error offsets.
     struct Issue {
-        uint32_t st, base, outside, dv;
+        uint32_t st, base, outside, dv[2];
     };
     int next = 0;
     auto prep = [&]() {
         Issue q;
-        q.st = lds0 + (uint32_t)((next % NS) * STAGE + wave * 1024);
-        const int pix = pbeg + next * PIX + prow;
+        q.st = lds0 + (uint32_t)((next % NS) * STAGE);
+        const int pb = pbeg + next * PIX;
+        const int pix = pb + xrow;
         const bool ok = next < nsteps && pix < pend;
         const uint32_t pp = ok ? (uint32_t)pix : 0u;
         const uint32_t n = fdiv(pp, P.div_pq);
@@ -145,29 +176,36 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
         q.outside = ok ? ~((((rows & 1u) ? cols : 0u)) | (((rows & 2u) ? cols : 0u) << 3) |
                            (((rows & 4u) ? cols : 0u) << 6))
                        : ~0u;
-        q.base = (uint32_t)(((int)n * P.H + h0) * P.W + w0) * (uint32_t)P.C + (uint32_t)c0 + cbyte;
-        q.dv = ok ? pp * (uint32_t)P.K + (uint32_t)k0 + cbyte : kOOB;
+        q.base = (uint32_t)(((int)n * P.H + h0) * P.W + w0) * (uint32_t)P.C + (uint32_t)c0 + xbyte;
+#pragma unroll
+        for (int u = 0; u < 2; u++) {
+            const int dp = pb + drow[u];
+            q.dv[u] = next < nsteps && dp < pend ? (uint32_t)dp * (uint32_t)P.K + (uint32_t)k0 + dbyte[u] : kOOB;
+        }
         next++;
         return q;
     };
-    // Load g of a stage: regions 0..8 the nine shifted input slices, 9 the error slice.
+    // Load g of a stage: 0..8 this wave's block of the nine shifted input
+    // slices, 9 and 10 its two blocks of the error slice.
     auto load = [&](const Issue& q, int g) {
         if (g < NTAP) {
             const uint32_t tap_off = (uint32_t)(g / 3) * WC + (uint32_t)(g % 3) * (uint32_t)P.C;
             const uint32_t v = (__builtin_amdgcn_ubfe(q.outside, (uint32_t)g, 1) << 31) | (q.base + tap_off);
-            lds_dma16(xrs, q.st + g * REG, v, 0);
+            lds_dma16(xrs, q.st + g * XREG + wave * 1024, v, 0);
         } else {
-            lds_dma16(drs, q.st + NTAP * REG, q.dv, 0);
+            const int u = g - NTAP;
+            lds_dma16(drs, q.st + DOFF + (2 * wave + u) * 1024, q.dv[u], 0);
         }
     };
     auto issue = [&]() {
         const Issue q = prep();
 #pragma unroll
-        for (int g = 0; g <= NTAP; g++) load(q, g);
+        for (int g = 0; g < LOADS; g++) load(q, g);
     };
 
-    const FragOff fo_x[2] = {frag_off(0, 32 * wc, lane), frag_off(32, 32 * wc, lane)};
-    const FragOff fo_d[2] = {frag_off(0, 32 * wk, lane), frag_off(32, 32 * wk, lane)};
+    // Fragment offsets of this wave's two 32-pixel quarters (2*ph, 2*ph + 1).
+    const FragOff fo_x[2] = {frag_off32(64 * ph, lane), frag_off32(64 * ph + 32, lane)};
+    const FragOff fo_d[2] = {frag_off64(64 * ph, 32 * wk, lane), frag_off64(64 * ph + 32, 32 * wk, lane)};
 
     v16i acc[NTAP];
 #pragma unroll
@@ -175,56 +213,43 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
 #pragma unroll
         for (int e = 0; e < 16; e++) acc[t][e] = 0;
 
-    // Fragments of one stage: per 32-pixel half, the error fragment and the
-    // nine input fragments.  A stage's fragments are read during the previous
-    // stage's MFMAs, so the LDS latency is hidden behind them.
+    // Fragments of one stage: per 32-pixel quarter, the error fragment and
+    // the nine input fragments.  A stage's fragments are read during the
+    // previous stage's MFMAs, so the LDS latency is hidden behind them.
     struct Frags {
         v4i d[2];
         v4i x[2][NTAP];
     };
-    auto read_stage = [&](int j, Frags& F) {
-        const uint32_t st = lds0 + (uint32_t)((j % NS) * STAGE);
-#pragma unroll
-        for (int ks = 0; ks < 2; ks++) {
-            F.d[ks] = tr_frag<REG>(st + fo_d[ks].lo, st + fo_d[ks].hi, NTAP);
-#pragma unroll
-            for (int t = 0; t < NTAP; t++) F.x[ks][t] = tr_frag<REG>(st + fo_x[ks].lo, st + fo_x[ks].hi, t);
-        }
-    };
-    auto mfma_stage = [&](const Frags& F) {
-#pragma unroll
-        for (int ks = 0; ks < 2; ks++)
-#pragma unroll
-            for (int t = 0; t < NTAP; t++)
-                acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.x[ks][t], F.d[ks], acc[t], 0, 0, 0);
+    // Fragment read f (0..19) of the stage at LDS address st: per quarter
+    // ks, the error fragment, then the nine taps.
+    auto read_one = [&](uint32_t st, int f, Frags& F) {
+        const int ks = f / (NTAP + 1), i = f % (NTAP + 1);
+        if (i == 0)
+            F.d[ks] = tr_frag(st + fo_d[ks].lo, st + fo_d[ks].hi, DOFF);
+        else
+            F.x[ks][i - 1] = tr_frag(st + fo_x[ks].lo, st + fo_x[ks].hi, (i - 1) * XREG);
     };
     // Stage it: stage it + 1 has landed (every wave's loads, hence the
     // barrier) and every wave has its stage-it fragments in registers, so
     // stage it's slot takes stage it + NS; then stage it + 1 is read while
-    // stage it's MFMAs run.
-    // The ten loads, twenty fragment reads and eighteen MFMAs of a step are
-    // issued interleaved (scheduling barriers keep the order), so a load
-    // waiting for the memory pipeline holds up no MFMA.
+    // stage it's MFMAs run.  The eleven loads, twenty fragment reads and
+    // eighteen MFMAs of a step are issued interleaved (scheduling barriers
+    // keep the order), so a load waiting for the memory pipeline holds up no
+    // MFMA.
     auto step = [&](int it, const Frags& cur, Frags& nxt) {
-        wait_vm<(NS - 2) * (NTAP + 1)>();
+        wait_vm<(NS - 2) * LOADS>();
         wait_lds0();
         __builtin_amdgcn_s_barrier();
         const Issue q = prep();
         const uint32_t st1 = lds0 + (uint32_t)(((it + 1) % NS) * STAGE);
 #pragma unroll
-        for (int g = 0; g <= NTAP; g++) {
+        for (int g = 0; g < LOADS; g++) {
             load(q, g);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int f = 2 * g; f < 2 * g + 2; f++) {
-                const int ks = f / (NTAP + 1), i = f % (NTAP + 1);
-                if (i == 0)
-                    nxt.d[ks] = tr_frag<REG>(st1 + fo_d[ks].lo, st1 + fo_d[ks].hi, NTAP);
-                else
-                    nxt.x[ks][i - 1] = tr_frag<REG>(st1 + fo_x[ks].lo, st1 + fo_x[ks].hi, i - 1);
-            }
+            for (int f = (g * 20) / LOADS; f < ((g + 1) * 20) / LOADS; f++) read_one(st1, f, nxt);
 #pragma unroll
-            for (int m = 2 * g; m < 2 * g + 2 && m < 2 * NTAP; m++) {
+            for (int m = (g * 18) / LOADS; m < ((g + 1) * 18) / LOADS; m++) {
                 const int ks = m / NTAP, t = m % NTAP;
                 acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(cur.x[ks][t], cur.d[ks], acc[t], 0, 0, 0);
             }
@@ -234,10 +259,11 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
 
 #pragma unroll
     for (int s = 0; s < NS; s++) issue();
-    wait_vm<(NS - 1) * (NTAP + 1)>();
+    wait_vm<(NS - 1) * LOADS>();
     __builtin_amdgcn_s_barrier();
     Frags f0, f1;
-    read_stage(0, f0);
+#pragma unroll
+    for (int f = 0; f < 20; f++) read_one(lds0, f, f0);
     int it = 0;
     for (; it + 1 < nsteps; it += 2) {
         step(it, f0, f1);
@@ -245,18 +271,41 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     }
     if (it < nsteps) step(it, f0, f1);
     wait_vm<0>();
+    wait_lds0();
+    __syncthreads();   // the ring is free
 
-    // acc[t] element 4*jj + i: channel c0 + 32*wc + 8*jj + 4*(lane/32) + i of
-    // tap t, output channel k0 + 32*wk + lane%32: four consecutive columns per store.
+    // The two pixel halves: wave (wk, ph) stores taps 0..4 (ph 0) or 5..8
+    // (ph 1); it hands the sums of the other taps to its partner (wk, 1 - ph)
+    // through LDS, slot [wk][t][jj][lane] of 16 bytes.
+    v4i* xch = (v4i*)lds;
+    const bool mine0 = ph == 0;
+#pragma unroll
+    for (int t = 0; t < NTAP; t++)
+        if ((t < 5) != mine0)
+#pragma unroll
+            for (int jj = 0; jj < 4; jj++) {
+                v4i q;
+                q[0] = acc[t][4 * jj];
+                q[1] = acc[t][4 * jj + 1];
+                q[2] = acc[t][4 * jj + 2];
+                q[3] = acc[t][4 * jj + 3];
+                xch[((wk * NTAP + t) * 4 + jj) * 64 + lane] = q;
+            }
+    __syncthreads();
+
+    // acc[t] element 4*jj + i: channel c0 + 8*jj + 4*(lane/32) + i of tap t,
+    // output channel k0 + 32*wk + lane%32: four consecutive columns per store.
     int32_t* out = P.part + (int64_t)split * P.K * P.ncol + (int64_t)(k0 + 32 * wk + (lane & 31)) * P.ncol;
 #pragma unroll
     for (int t = 0; t < NTAP; t++)
+        if ((t < 5) == mine0)
 #pragma unroll
-        for (int jj = 0; jj < 4; jj++) {
-            const int col = t * P.C + c0 + 32 * wc + 8 * jj + 4 * (lane >> 5);
-            *(int4*)(out + col) =
-                make_int4(acc[t][4 * jj], acc[t][4 * jj + 1], acc[t][4 * jj + 2], acc[t][4 * jj + 3]);
-        }
+            for (int jj = 0; jj < 4; jj++) {
+                const v4i o = xch[((wk * NTAP + t) * 4 + jj) * 64 + lane];
+                const int col = t * P.C + c0 + 8 * jj + 4 * (lane >> 5);
+                *(int4*)(out + col) = make_int4(acc[t][4 * jj] + o[0], acc[t][4 * jj + 1] + o[1],
+                                                acc[t][4 * jj + 2] + o[2], acc[t][4 * jj + 3] + o[3]);
+            }
 }
 
 }  // namespace
@@ -269,11 +318,11 @@ bool wgrad_tap_eligible(const WgradProblem& p) {
 WgradPlan wgrad_tap_plan(int64_t K, int64_t C, int64_t npix) {
     WgradPlan pl;
     pl.tbk = 64;
-    const int64_t tiles = (K / 64) * (C / 64);
+    const int64_t tiles = (K / 64) * (C / CW);
     const int64_t steps = (npix + PIX - 1) / PIX;
-    // about one workgroup per CU, at least four stages each
+    // about one workgroup per CU, at least two stages each
     int64_t splits = (256 + tiles - 1) / tiles;
-    const int64_t max_splits = steps / 4 > 1 ? steps / 4 : 1;
+    const int64_t max_splits = steps / 2 > 1 ? steps / 2 : 1;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     const int64_t chunk_steps = (steps + splits - 1) / splits;
@@ -286,6 +335,7 @@ WgradPlan wgrad_tap_plan(int64_t K, int64_t C, int64_t npix) {
 hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {
     constexpr int NS = 3;
     constexpr int LDS = NS * STAGE;
+    static_assert(LDS >= 2 * NTAP * 4 * 64 * 16, "exchange area");
     static bool attr_done = false;
     if (!attr_done) {
         hipError_t e = hipFuncSetAttribute((const void*)wgrad_tap_kernel<NS>,
@@ -294,7 +344,7 @@ hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t str
         attr_done = true;
     }
     p.chunk = plan.chunk;
-    const int tc = p.C / 64, tk = p.K / 64;
+    const int tc = p.C / CW, tk = p.K / 64;
     const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
     hipLaunchKernelGGL((wgrad_tap_kernel<NS>), dim3((unsigned)grid), dim3(256), LDS, stream, p, tc, tk, plan.splits);
     return hipGetLastError();
