@@ -269,8 +269,17 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
     }
     __syncthreads();   // weights staged
 
-    // fragment reads: channel row (a * 32 + lane % 32), K bytes 32 h + 16 hi of step j
+    // fragment reads: channel row (a * 32 + lane % 32), K bytes 32 h + 16 hi of
+    // the step at K byte kk.  The weights of a half step are read one half
+    // step ahead (they are the same for every task: after a task's last step
+    // come the first step's), so no MFMA waits for LDS.
     const int8_t* wrow = lds + (lane & 31) * kp + 16 * hi;
+    auto read_wh = [&](int kk, int h, v4i (&w)[NF]) {
+#pragma unroll
+        for (int a = 0; a < NF; a++) w[a] = *(const v4i*)(wrow + a * 32 * (int)kp + kk + 32 * h);
+    };
+    v4i wn[NF];
+    read_wh(0, 0, wn);
     v16i acc[NF];
     const int mode_sel = (relu ? 1 : 0) | (rk.rtn ? 2 : 0);
     const bool dense = P.os == 1 && P.OHc == P.OH && P.OWc == P.OW;
@@ -285,16 +294,22 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
 #pragma unroll
             for (int u = 0; u < D; u++) {
                 const int kk = (g * D + u) * KSTEP;
-                v4i wa[2][NF];
+                int kn = kk + KSTEP;
+                if (kn == P.Ktot) kn = 0;
 #pragma unroll
-                for (int h = 0; h < 2; h++)
+                for (int h = 0; h < 2; h++) {
+                    v4i wa[NF];
 #pragma unroll
-                    for (int a = 0; a < NF; a++) wa[h][a] = *(const v4i*)(wrow + a * 32 * (int)kp + kk + 32 * h);
-#pragma unroll
-                for (int h = 0; h < 2; h++)
+                    for (int a = 0; a < NF; a++) wa[a] = wn[a];
+                    if (h == 0)
+                        read_wh(kk, 1, wn);
+                    else
+                        read_wh(kn, 0, wn);
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int a = 0; a < NF; a++)
-                        acc[a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wa[h][a], bq[u][h], acc[a], 0, 0, 0);
+                        acc[a] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wa[a], bq[u][h], acc[a], 0, 0, 0);
+                }
                 load_step(bq[u]);
             }
         }

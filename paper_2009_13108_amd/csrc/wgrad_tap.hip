@@ -21,18 +21,24 @@
 // tap; eight consecutive rows are 256 contiguous bytes, so transpose reads
 // need no swizzle) and one dy region [128 pixels][64 bytes] (16-byte chunks
 // XOR-swizzled by pixel).  The MFMA operands come out of them with transpose
-// reads (the same fragment reader as wgrad_dma.hip).  Wave (wk, ph) of four
-// computes output channels k0 + 32*wk .. +31 x the 32 channels for all nine
-// taps over pixel half ph of each stage: per 32 pixels one error fragment and
-// nine input fragments feed nine MFMAs.  The two pixel halves' sums meet in
-// LDS at the end.
+// reads (the same fragment reader as wgrad_dma.hip).  Eight waves, two per
+// SIMD: wave w computes output channels k0 + 32*wk .. +31 x the 32 channels
+// over pixel half ph of each stage ((wk, ph) from w % 4) for taps 0..4
+// (w < 4) or 5..8 (w >= 4): per 32 pixels one error fragment and five or
+// four input fragments feed as many MFMAs.  The two pixel halves' sums meet
+// in LDS at the end.
 //
-// Loads.  Wave w fills pixels 32w .. 32w+31 of the nine x regions and pixels
-// 32w .. 32w+31 of the dy region (eleven direct-to-LDS loads of 1 KiB,
-// issued as inline assembly so the compiler does not wait for the whole ring
-// before each transpose read); a lane keeps the input offset of its pixel and
-// a 9-bit mask of the taps that fall outside the image, so each tap's load is
-// one add and one bit test.
+// Issue cost.  Every instruction a wave issues besides its MFMAs holds the
+// SIMD's MFMA pipe for a few cycles (about three and a half with one wave
+// per SIMD, about two with two waves), so the kernel keeps the instruction
+// count per MFMA low: two waves per SIMD, and only waves 0..3 load.
+//
+// Loads.  Wave w < 4 fills pixels 32w .. 32w+31 of the nine x regions and
+// of the dy region (eleven direct-to-LDS loads of 1 KiB, issued as inline
+// assembly so the compiler does not wait for the whole ring before each
+// transpose read); a lane keeps the input offset of its pixel and a 9-bit
+// mask of the taps that fall outside the image, so each tap's load is one
+// add and one bit test.
 #include "niti_internal.h"
 
 namespace niti {
@@ -109,41 +115,43 @@ __device__ __forceinline__ v4i tr_frag(uint32_t lo_addr, uint32_t hi_addr, int o
     return r;
 }
 
-// Work items (split, tile), tile fastest, cut into eight equal consecutive
-// runs, one per XCD (workgroup L runs on XCD L % 8), so the tiles of one pixel
-// range share an XCD and its L2.
-template <int NS>
-__global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int tiles_c, int tiles_k, int splits) {
-    extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
+// Taps of a wave: wave w of eight runs on SIMD w % 4; waves w and w + 4 take
+// taps 0..4 and 5..8 of the same output block and pixel half, so the two
+// waves of a SIMD share its MFMA pipe, one issuing while the other waits.
+// Only waves 0..3 load, so the loads' address work is not duplicated.
+template <int TH>
+struct TapHalf {
+    static constexpr int T0 = TH ? 5 : 0;   // first tap
+    static constexpr int N = TH ? 4 : 5;    // taps
+};
+constexpr int NTHREADS = 512;
+
+template <int NS, int TH>
+__device__ __forceinline__ void tap_body(const WgradProblem& P, int8_t* lds, int split, int c0, int k0, int pbeg,
+                                         int pend, int nsteps) {
+    constexpr int T0 = TapHalf<TH>::T0, NTW = TapHalf<TH>::N;
+    constexpr bool LOADER = TH == 0;
+    constexpr int NR = 2 * (NTW + 1);      // fragment reads per stage
+    constexpr int NM = 2 * NTW;            // MFMAs per stage
+    constexpr int NG = LOADER ? LOADS : NTW + 1;   // issue groups per step
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int wk = wave & 1, ph = wave >> 1;
-    const int ntiles = tiles_c * tiles_k;
-    const int per_xcd = (ntiles * splits + 7) / 8;
-    const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-    if ((blockIdx.x >> 3) >= per_xcd || item >= ntiles * splits) return;
-    const int split = item / ntiles;
-    const int tile = item - split * ntiles;
-    const int c0 = (tile % tiles_c) * CW;
-    const int k0 = (tile / tiles_c) * 64;
-    const int pbeg = split * P.chunk;
-    const int pend = min(P.npix, pbeg + P.chunk);
-    const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
+    const int sub = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 3);
+    const int wk = sub & 1, ph = sub >> 1;
 
     const u32x4 xrs = raw_rsrc(P.x, (uint32_t)P.x_bytes);
     const u32x4 drs = raw_rsrc(P.dy, (uint32_t)P.dy_bytes);
     const uint32_t lds0 = lds_address(lds);
 
-    // This lane's rows: x pixel 32*wave + lane/2 (chunk lane%2; a 1 KiB block
-    // of an x region is 32 rows of 32 bytes) and dy pixels 32*wave + 16*u +
+    // Loader lanes' rows: x pixel 32*sub + lane/2 (chunk lane%2; a 1 KiB block
+    // of an x region is 32 rows of 32 bytes) and dy pixels 32*sub + 16*u +
     // lane/4 (chunk lane%4, swizzled; a block of the dy region is 16 rows).
-    const int xrow = 32 * wave + (lane >> 1);
+    const int xrow = 32 * sub + (lane >> 1);
     const uint32_t xbyte = (uint32_t)((lane & 1) << 4);
     int drow[2];
     uint32_t dbyte[2];
 #pragma unroll
     for (int u = 0; u < 2; u++) {
-        drow[u] = 32 * wave + 16 * u + (lane >> 2);
+        drow[u] = 32 * sub + 16 * u + (lane >> 2);
         dbyte[u] = (uint32_t)(((lane & 3) ^ swz(drow[u])) << 4);
     }
     const uint32_t WC = (uint32_t)P.W * (uint32_t)P.C;
@@ -191,10 +199,10 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
         if (g < NTAP) {
             const uint32_t tap_off = (uint32_t)(g / 3) * WC + (uint32_t)(g % 3) * (uint32_t)P.C;
             const uint32_t v = (__builtin_amdgcn_ubfe(q.outside, (uint32_t)g, 1) << 31) | (q.base + tap_off);
-            lds_dma16(xrs, q.st + g * XREG + wave * 1024, v, 0);
+            lds_dma16_at(xrs, q.st, (uint32_t)(g * XREG + sub * 1024), v, 0);
         } else {
             const int u = g - NTAP;
-            lds_dma16(drs, q.st + DOFF + (2 * wave + u) * 1024, q.dv[u], 0);
+            lds_dma16_at(drs, q.st, (uint32_t)(DOFF + (2 * sub + u) * 1024), q.dv[u], 0);
         }
     };
     auto issue = [&]() {
@@ -207,63 +215,66 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     const FragOff fo_x[2] = {frag_off32(64 * ph, lane), frag_off32(64 * ph + 32, lane)};
     const FragOff fo_d[2] = {frag_off64(64 * ph, 32 * wk, lane), frag_off64(64 * ph + 32, 32 * wk, lane)};
 
-    v16i acc[NTAP];
+    v16i acc[NTW];
 #pragma unroll
-    for (int t = 0; t < NTAP; t++)
+    for (int t = 0; t < NTW; t++)
 #pragma unroll
         for (int e = 0; e < 16; e++) acc[t][e] = 0;
 
     // Fragments of one stage: per 32-pixel quarter, the error fragment and
-    // the nine input fragments.  A stage's fragments are read during the
-    // previous stage's MFMAs, so the LDS latency is hidden behind them.
+    // the input fragments of this wave's taps.  A stage's fragments are read
+    // during the previous stage's MFMAs, so the LDS latency is hidden behind
+    // them.
     struct Frags {
         v4i d[2];
-        v4i x[2][NTAP];
+        v4i x[2][NTW];
     };
-    // Fragment read f (0..19) of the stage at LDS address st: per quarter
-    // ks, the error fragment, then the nine taps.
+    // Fragment read f of the stage at LDS address st: per quarter ks, the
+    // error fragment, then the taps.
     auto read_one = [&](uint32_t st, int f, Frags& F) {
-        const int ks = f / (NTAP + 1), i = f % (NTAP + 1);
+        const int ks = f / (NTW + 1), i = f % (NTW + 1);
         if (i == 0)
             F.d[ks] = tr_frag(st + fo_d[ks].lo, st + fo_d[ks].hi, DOFF);
         else
-            F.x[ks][i - 1] = tr_frag(st + fo_x[ks].lo, st + fo_x[ks].hi, (i - 1) * XREG);
+            F.x[ks][i - 1] = tr_frag(st + fo_x[ks].lo, st + fo_x[ks].hi, (T0 + i - 1) * XREG);
     };
-    // Stage it: stage it + 1 has landed (every wave's loads, hence the
+    // Stage it: stage it + 1 has landed (every loader's loads, hence the
     // barrier) and every wave has its stage-it fragments in registers, so
     // stage it's slot takes stage it + NS; then stage it + 1 is read while
-    // stage it's MFMAs run.  The eleven loads, twenty fragment reads and
-    // eighteen MFMAs of a step are issued interleaved (scheduling barriers
-    // keep the order), so a load waiting for the memory pipeline holds up no
-    // MFMA.
+    // stage it's MFMAs run.  Loads, fragment reads and MFMAs of a step are
+    // issued interleaved (scheduling barriers keep the order), so a load
+    // waiting for the memory pipeline holds up no MFMA.
     auto step = [&](int it, const Frags& cur, Frags& nxt) {
-        wait_vm<(NS - 2) * LOADS>();
+        if (LOADER) wait_vm<(NS - 2) * LOADS>();
         wait_lds0();
         __builtin_amdgcn_s_barrier();
-        const Issue q = prep();
+        Issue q;
+        if (LOADER) q = prep();
         const uint32_t st1 = lds0 + (uint32_t)(((it + 1) % NS) * STAGE);
 #pragma unroll
-        for (int g = 0; g < LOADS; g++) {
-            load(q, g);
+        for (int g = 0; g < NG; g++) {
+            if (LOADER) load(q, g);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int f = (g * 20) / LOADS; f < ((g + 1) * 20) / LOADS; f++) read_one(st1, f, nxt);
+            for (int f = (g * NR) / NG; f < ((g + 1) * NR) / NG; f++) read_one(st1, f, nxt);
 #pragma unroll
-            for (int m = (g * 18) / LOADS; m < ((g + 1) * 18) / LOADS; m++) {
-                const int ks = m / NTAP, t = m % NTAP;
+            for (int m = (g * NM) / NG; m < ((g + 1) * NM) / NG; m++) {
+                const int ks = m / NTW, t = m % NTW;
                 acc[t] = __builtin_amdgcn_mfma_i32_32x32x32_i8(cur.x[ks][t], cur.d[ks], acc[t], 0, 0, 0);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
     };
 
+    if (LOADER) {
 #pragma unroll
-    for (int s = 0; s < NS; s++) issue();
-    wait_vm<(NS - 1) * LOADS>();
+        for (int s = 0; s < NS; s++) issue();
+        wait_vm<(NS - 1) * LOADS>();
+    }
     __builtin_amdgcn_s_barrier();
     Frags f0, f1;
 #pragma unroll
-    for (int f = 0; f < 20; f++) read_one(lds0, f, f0);
+    for (int f = 0; f < NR; f++) read_one(lds0, f, f0);
     int it = 0;
     for (; it + 1 < nsteps; it += 2) {
         step(it, f0, f1);
@@ -274,14 +285,13 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
     wait_lds0();
     __syncthreads();   // the ring is free
 
-    // The two pixel halves: wave (wk, ph) stores taps 0..4 (ph 0) or 5..8
-    // (ph 1); it hands the sums of the other taps to its partner (wk, 1 - ph)
-    // through LDS, slot [wk][t][jj][lane] of 16 bytes.
+    // The two pixel halves: wave (wk, 1, TH) hands its sums to wave
+    // (wk, 0, TH) through LDS, slot [wk][tap][jj][lane] of 16 bytes, which
+    // adds them to its own and stores.
     v4i* xch = (v4i*)lds;
-    const bool mine0 = ph == 0;
+    if (ph == 1) {
 #pragma unroll
-    for (int t = 0; t < NTAP; t++)
-        if ((t < 5) != mine0)
+        for (int t = 0; t < NTW; t++)
 #pragma unroll
             for (int jj = 0; jj < 4; jj++) {
                 v4i q;
@@ -289,23 +299,48 @@ __global__ __launch_bounds__(256, 1) void wgrad_tap_kernel(WgradProblem P, int t
                 q[1] = acc[t][4 * jj + 1];
                 q[2] = acc[t][4 * jj + 2];
                 q[3] = acc[t][4 * jj + 3];
-                xch[((wk * NTAP + t) * 4 + jj) * 64 + lane] = q;
+                xch[((wk * NTAP + T0 + t) * 4 + jj) * 64 + lane] = q;
             }
+    }
     __syncthreads();
+    if (ph == 1) return;
 
-    // acc[t] element 4*jj + i: channel c0 + 8*jj + 4*(lane/32) + i of tap t,
-    // output channel k0 + 32*wk + lane%32: four consecutive columns per store.
+    // acc[t] element 4*jj + i: channel c0 + 8*jj + 4*(lane/32) + i of tap
+    // T0 + t, output channel k0 + 32*wk + lane%32: four consecutive columns
+    // per store.
     int32_t* out = P.part + (int64_t)split * P.K * P.ncol + (int64_t)(k0 + 32 * wk + (lane & 31)) * P.ncol;
 #pragma unroll
-    for (int t = 0; t < NTAP; t++)
-        if ((t < 5) == mine0)
+    for (int t = 0; t < NTW; t++)
 #pragma unroll
-            for (int jj = 0; jj < 4; jj++) {
-                const v4i o = xch[((wk * NTAP + t) * 4 + jj) * 64 + lane];
-                const int col = t * P.C + c0 + 8 * jj + 4 * (lane >> 5);
-                *(int4*)(out + col) = make_int4(acc[t][4 * jj] + o[0], acc[t][4 * jj + 1] + o[1],
-                                                acc[t][4 * jj + 2] + o[2], acc[t][4 * jj + 3] + o[3]);
-            }
+        for (int jj = 0; jj < 4; jj++) {
+            const v4i o = xch[((wk * NTAP + T0 + t) * 4 + jj) * 64 + lane];
+            const int col = (T0 + t) * P.C + c0 + 8 * jj + 4 * (lane >> 5);
+            *(int4*)(out + col) = make_int4(acc[t][4 * jj] + o[0], acc[t][4 * jj + 1] + o[1],
+                                            acc[t][4 * jj + 2] + o[2], acc[t][4 * jj + 3] + o[3]);
+        }
+}
+
+// Work items (split, tile), tile fastest, cut into eight equal consecutive
+// runs, one per XCD (workgroup L runs on XCD L % 8), so the tiles of one pixel
+// range share an XCD and its L2.
+template <int NS>
+__global__ __launch_bounds__(NTHREADS, 1) void wgrad_tap_kernel(WgradProblem P, int tiles_c, int tiles_k, int splits) {
+    extern __shared__ __attribute__((aligned(1024))) int8_t lds[];
+    const int ntiles = tiles_c * tiles_k;
+    const int per_xcd = (ntiles * splits + 7) / 8;
+    const int item = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if ((blockIdx.x >> 3) >= per_xcd || item >= ntiles * splits) return;
+    const int split = item / ntiles;
+    const int tile = item - split * ntiles;
+    const int c0 = (tile % tiles_c) * CW;
+    const int k0 = (tile / tiles_c) * 64;
+    const int pbeg = split * P.chunk;
+    const int pend = min(P.npix, pbeg + P.chunk);
+    const int nsteps = pend > pbeg ? (pend - pbeg + PIX - 1) / PIX : 0;
+    if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 8) == 0)
+        tap_body<NS, 0>(P, lds, split, c0, k0, pbeg, pend, nsteps);
+    else
+        tap_body<NS, 1>(P, lds, split, c0, k0, pbeg, pend, nsteps);
 }
 
 }  // namespace
@@ -346,7 +381,7 @@ hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t str
     p.chunk = plan.chunk;
     const int tc = p.C / CW, tk = p.K / 64;
     const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
-    hipLaunchKernelGGL((wgrad_tap_kernel<NS>), dim3((unsigned)grid), dim3(256), LDS, stream, p, tc, tk, plan.splits);
+    hipLaunchKernelGGL((wgrad_tap_kernel<NS>), dim3((unsigned)grid), dim3(NTHREADS), LDS, stream, p, tc, tk, plan.splits);
     return hipGetLastError();
 }
 
