@@ -104,7 +104,8 @@ class ResNetStep:
         # Two streams, as in a training step: A runs the forward pass and the
         # back-propagation chain; B runs each layer's weight gradient + update
         # as soon as that layer's back-propagation is enqueued, overlapping the
-        # next layer's back-propagation.  B's update of w(l) follows A's
+        # next layer's back-propagation (the image layer's, which has no
+        # back-propagation, runs on A after the chain).  B's update of w(l) follows A's
         # back-propagation of layer l (which reads w(l)), and the next step's
         # forward pass follows all of B's updates.
         self.sA = torch.cuda.Stream()
@@ -196,9 +197,15 @@ class ResNetStep:
             for c in reversed(range(L["count"])):
                 w = L["w"][c]
                 s0 = L["stats"] + 3 * c
-                if L["bwd_data"]:
-                    seg(A, lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
-                                                      relu_src=L["x"], stats_index=s0 + 1))
+                if not L["bwd_data"]:
+                    # The image layer has no back-propagation: stream A,
+                    # idle from here on, takes its weight gradient, which
+                    # then overlaps B's remaining queue instead of ending it.
+                    seg(A, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu,
+                                                        stats_index=s0 + 2))
+                    continue
+                seg(A, lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
+                                                  relu_src=L["x"], stats_index=s0 + 1))
                 ev += 1
                 rec(self.ev_bwd[ev], A)
                 wait(B, self.ev_bwd[ev])
