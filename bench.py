@@ -111,6 +111,7 @@ class ResNetStep:
         self.sA = torch.cuda.Stream()
         self.sB = torch.cuda.Stream()
         self.ev_bwd = [torch.cuda.Event() for _ in range(sum(L["count"] for L in self.layers) + 1)]
+        self.ev_fwd = [torch.cuda.Event() for _ in range(8)]
         self.ev_upd = torch.cuda.Event()
         self.ev_upd.record(self.sB)
         self.fam_ops = {"igemm": 0, "wgrad": 0}
@@ -171,11 +172,11 @@ class ResNetStep:
             if plan is not None:
                 plan.append(("wait", stream, ev))
 
+        def conv_fwd(L, c, ws):
+            niti.conv_fwd(L["desc"], L["x"], L["w"][c], L["y"], self.stats, relu=True,
+                          stats_index=L["stats"] + 3 * c, ws=ws)
+
         def head():
-            for L in self.layers:
-                for c in range(L["count"]):
-                    niti.conv_fwd(L["desc"], L["x"], L["w"][c], L["y"], self.stats, relu=True,
-                                  stats_index=L["stats"] + 3 * c, ws=self.ws)
             niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc, self.s_logits, 7,
                           False, stats_index=s)
             niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats, self.ws,
@@ -185,6 +186,27 @@ class ResNetStep:
                                relu_src=self.feat.view(Bsz, 1, 1, fin), stats_index=s + 2)
 
         wait(A, self.ev_upd)             # the previous step's weight updates
+        # Forward.  A downsampling block's 1x1 projection reads the block input,
+        # as its first 3x3 convolution does, and its output is needed only when
+        # the block's two branches are added, before the next block: it runs on
+        # stream B (idle in the forward pass) beside the two 3x3 convolutions.
+        blk = 0
+        pending = None
+        for L in self.layers:
+            if L["name"].endswith("_1x1s2"):
+                seg(B, lambda: conv_fwd(L, 0, self.ws_b))
+                pending = self.ev_fwd[2 * blk + 1]
+                rec(pending, B)
+                blk += 1
+                continue
+            for c in range(L["count"]):
+                if L["name"].endswith("3x3s2"):
+                    rec(self.ev_fwd[2 * blk], A)      # the block input is ready
+                    wait(B, self.ev_fwd[2 * blk])
+                if pending is not None and c == 1:
+                    wait(A, pending)                  # both branches done before the next block
+                    pending = None
+                seg(A, lambda: conv_fwd(L, c, self.ws))
         seg(A, head)
         ev = 0
         rec(self.ev_bwd[ev], A)
