@@ -572,34 +572,35 @@ __global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t*
     }
 }
 
-// Zero-padded copy, 16 output bytes per thread over the flat output (the
-// output rows need not be 16-byte multiples, so a piece may straddle two
-// rows): four independent dword loads, one 16-byte store.
-__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* x, uint32_t* xp, FastDiv div_len,
-                                                        FastDiv div_hp, FastDiv div_c4, uint32_t len, int32_t h,
-                                                        int32_t w, int32_t c4, int32_t hp, int32_t ph, int32_t pw,
-                                                        uint32_t total) {
-    const uint32_t stride = gridDim.x * blockDim.x;
-    for (uint32_t t = blockIdx.x * blockDim.x + threadIdx.x; 4 * t < total; t += stride) {
-        uint32_t v[4];
+// Zero-padded copy, one wave per padded row (image * hp + row): the lanes
+// take the row's dwords 64 apart, each issuing all its loads before its
+// stores; columns and rows outside the image are zeros.
+constexpr int kPadU = 4;   // dwords per lane and pass
+__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* __restrict__ x, uint32_t* __restrict__ xp,
+                                                        uint32_t len, int32_t h, int32_t w, int32_t c4, int32_t hp,
+                                                        int32_t ph, int32_t pw, uint32_t rows) {
+    const uint32_t r = blockIdx.x * 4u + (threadIdx.x >> 6);
+    if (r >= rows) return;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t img = r / (uint32_t)hp;
+    const int row = (int)(r - img * (uint32_t)hp) - ph;
+    const bool rowok = row >= 0 && row < h;
+    // dword index in x of padded column 0 of this row (negative values are
+    // never used: only in-image columns are read)
+    const int64_t base = (((int64_t)img * h + row) * w - pw) * c4;
+    const uint32_t lo = (uint32_t)(pw * c4), hi = (uint32_t)((pw + w) * c4);
+    uint32_t* dst = xp + (size_t)r * len;
+    for (uint32_t j0 = lane; j0 < len; j0 += 64u * kPadU) {
+        uint32_t v[kPadU];
 #pragma unroll
-        for (int q = 0; q < 4; q++) {
-            const uint32_t j = 4 * t + (uint32_t)q;   // output dword
-            v[q] = 0;
-            if (j >= total) continue;
-            const uint32_t rid = fdiv(j, div_len);     // img * hp + padded row
-            const uint32_t cw = j - rid * len;
-            const uint32_t img = fdiv(rid, div_hp);
-            const int row = (int)(rid - img * (uint32_t)hp) - ph;
-            const uint32_t pc = c4 == 1 ? cw : fdiv(cw, div_c4);
-            const int col = (int)pc - pw;
-            if (row >= 0 && row < h && col >= 0 && col < w)
-                v[q] = x[(((size_t)img * h + row) * w + col) * c4 + (cw - pc * (uint32_t)c4)];
+        for (int u = 0; u < kPadU; u++) {
+            const uint32_t j = j0 + 64u * u;
+            v[u] = (rowok && j >= lo && j < hi) ? x[base + j] : 0u;
         }
-        if (4 * t + 3 < total) {
-            *(uint4*)(xp + 4 * t) = make_uint4(v[0], v[1], v[2], v[3]);
-        } else {
-            for (int q = 0; q < 4 && 4 * t + q < total; q++) xp[4 * t + q] = v[q];
+#pragma unroll
+        for (int u = 0; u < kPadU; u++) {
+            const uint32_t j = j0 + 64u * u;
+            if (j < len) dst[j] = v[u];
         }
     }
 }
@@ -761,17 +762,14 @@ hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int
 
 hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
                          int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
-    const int64_t total = n * hp * wp * (c / 4);
-    if (total <= 0) return hipSuccess;
-    if (total >= ((int64_t)1 << 32) - 4) return hipErrorInvalidValue;
-    const uint32_t len = (uint32_t)(wp * (c / 4));
-    const int64_t threads = (total + 3) / 4;
-    int64_t grid = (threads + kThreads - 1) / kThreads;
-    if (grid > 65536) grid = 65536;
+    const int64_t rows = n * hp;
+    const int64_t len = wp * (c / 4);
+    if (rows <= 0 || len <= 0) return hipSuccess;
+    if (rows * len >= ((int64_t)1 << 32) || rows >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    const int64_t grid = (rows + 3) / 4;
     hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, s, (const uint32_t*)x,
-                       (uint32_t*)xp, make_fastdiv(len), make_fastdiv((uint32_t)hp), make_fastdiv((uint32_t)(c / 4)),
-                       len, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp, (int32_t)ph, (int32_t)pw,
-                       (uint32_t)total);
+                       (uint32_t*)xp, (uint32_t)len, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp,
+                       (int32_t)ph, (int32_t)pw, (uint32_t)rows);
     return hipGetLastError();
 }
 
