@@ -331,9 +331,8 @@ template <int TBM, int TBN>
 __global__ __launch_bounds__(NTHREADS) void igemm_fixup(IgemmBatch batch, IgemmCtl ctl) {
     __shared__ Smem<TBM, TBN> sm;
     niti_stats* st = ctl.stats;
-    const int cur = st->cur & 1;
     const int hint = st->hint_used;
-    const int bp = block_bp(load_acc(st, cur), ctl.target);
+    const int bp = block_bp(load_cur_acc(st), ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         for (int tt = blockIdx.x; tt < batch.total_tiles; tt += gridDim.x) {

@@ -167,9 +167,8 @@ __global__ __launch_bounds__(ST) void igemm_small_main(IgemmProblem P, IgemmCtl 
 __global__ __launch_bounds__(ST) void igemm_small_fixup(IgemmProblem P, IgemmCtl ctl, int ntiles) {
     __shared__ __attribute__((aligned(16))) int32_t red[SW * 32 * RP];
     niti_stats* st = ctl.stats;
-    const int cur = st->cur & 1;
     const int hint = st->hint_used;
-    const int bp = block_bp(load_acc(st, cur), ctl.target);
+    const int bp = block_bp(load_cur_acc(st), ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         uint32_t dummy = 0;

@@ -391,9 +391,8 @@ template <int NF, int MODE, int D>
 __global__ __launch_bounds__(NT, (WrCfg<NF, D>::MINW)) void igemm_wres_fixup(IgemmBatch batch, IgemmCtl ctl, int tasks) {
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
-    const int cur = st->cur & 1;
     const int hint = st->hint_used;
-    const int bp = block_bp(load_acc(st, cur), ctl.target);
+    const int bp = block_bp(load_cur_acc(st), ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         uint32_t dummy = 0;

@@ -235,6 +235,14 @@ __device__ __forceinline__ uint64_t load_acc(niti_stats* st, int slot) {
     return __hip_atomic_load(&st->acc_max[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The maximum of the call in progress: both slots and the slot index are
+// read at once (one memory round trip instead of two dependent ones) and
+// the current slot's value is selected.
+__device__ __forceinline__ uint64_t load_cur_acc(niti_stats* st) {
+    const uint64_t a0 = load_acc(st, 0), a1 = load_acc(st, 1);
+    return (st->cur & 1) ? a1 : a0;
+}
+
 // Snapshot of the tensor maximum taken when a workgroup starts (by thread 0,
 // the one that publishes).  The maximum only grows, so a workgroup maximum
 // not above the snapshot can be skipped without a fresh read at the end.
@@ -305,21 +313,29 @@ struct ExpArgs {
 // maximum, form the output exponent (Algorithm 2: s_q = s_q32 + bp), record
 // the statistics, make bp the next call's first guess, clear the other
 // slot and count the call.
+// Every value it reads is loaded before any is used (one memory round trip).
 __device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint32_t static_flags,
                                    int hinted) {
+    const uint64_t a0 = load_acc(st, 0), a1 = load_acc(st, 1);
+    const uint32_t f0 = __hip_atomic_load(&st->wflags[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t f1 = __hip_atomic_load(&st->wflags[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int cur = st->cur & 1;
-    const uint64_t mx = load_acc(st, cur);
-    const uint32_t wf = __hip_atomic_load(&st->wflags[cur], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int hint_used = st->hint_used;
+    const uint32_t misses = st->misses, calls = st->calls;
+    const int sa = ex.s_out && ex.s_a ? (int)*ex.s_a : 0;
+    const int sb = ex.s_out && ex.s_b ? (int)*ex.s_b : 0;
+    const uint64_t mx = cur ? a1 : a0;
+    const uint32_t wf = cur ? f1 : f0;
     const int b = bitlen64(mx);
     const int bp = block_bp(mx, target);
     uint32_t fl = wf | static_flags;
-    if (hinted && bp != st->hint_used) {
+    if (hinted && bp != hint_used) {
         fl |= NITI_FLAG_HINT_MISS;
-        st->misses += 1;
+        st->misses = misses + 1;
     }
     int s = 0;
     if (ex.s_out) {
-        s = (ex.s_a ? (int)*ex.s_a : 0) + (ex.s_b ? (int)*ex.s_b : 0) + bp;
+        s = sa + sb + bp;
         if (s > 127) { s = 127; fl |= NITI_FLAG_EXP_RANGE; }
         if (s < -128) { s = -128; fl |= NITI_FLAG_EXP_RANGE; }
         *ex.s_out = (int8_t)s;
@@ -332,7 +348,7 @@ __device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint3
     st->bp_hint = bp;
     st->acc_max[cur ^ 1] = 0;
     st->wflags[cur ^ 1] = 0;
-    st->calls += 1;
+    st->calls = calls + 1;
 }
 
 __device__ __forceinline__ bool is_finisher() {
