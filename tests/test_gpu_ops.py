@@ -318,7 +318,9 @@ def test_int_ce_loss_worked_examples():
         assert host(err).tolist() == c["err"], c["why"]
 
 
-@pytest.mark.parametrize("n,mu", [(1, 5), (1000, 5), (36864, 3), (2359296, 1), (7, 8)])
+@pytest.mark.parametrize("n,mu", [(1, 5), (1000, 5), (36864, 3), (2359296, 1), (7, 8),
+                                  (1003, 6),        # groups of four plus a 3-weight tail
+                                  (4194309, 4)])    # more groups than one pass of the grid covers
 def test_sgd_update_parity(n, mu):
     import torch
     say("sgd_update", n, mu)
