@@ -170,15 +170,7 @@ __device__ __forceinline__ void store_tile(const IgemmProblem& P, int tm, int tn
             }
             uint32_t vw[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                uint32_t keep = 0;
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int8_t mb = (int8_t)(mw[q] >> (8 * e));
-                    keep |= (mb > 0 ? 0xFFu : 0u) << (8 * e);
-                }
-                vw[q] &= keep;
-            }
+            for (int q = 0; q < 4; q++) vw[q] &= positive_bytes(mw[q]);
             v = make_uint4(vw[0], vw[1], vw[2], vw[3]);
         }
         if (full) {

@@ -351,6 +351,16 @@ __device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint3
     st->calls = calls + 1;
 }
 
+// 0xFF in every byte of m that is positive as an int8, 0x00 elsewhere (the
+// backward ReLU mask of four packed bytes), without per-byte compares: the
+// low seven bits plus 0x7F carry into bit 7 exactly when they are not all
+// zero, and no byte carries into the next.
+__device__ __forceinline__ uint32_t positive_bytes(uint32_t m) {
+    const uint32_t nz = (m & 0x7F7F7F7Fu) + 0x7F7F7F7Fu;
+    const uint32_t pos = nz & ~m & 0x80808080u;
+    return pos | (pos - (pos >> 7));
+}
+
 __device__ __forceinline__ bool is_finisher() {
     return blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0;
 }
