@@ -576,10 +576,19 @@ __global__ void maxpool_bwd_kernel(const int8_t* dy, const uint8_t* idx, int8_t*
 // take the row's dwords 64 apart, each issuing all its loads before its
 // stores; columns and rows outside the image are zeros.
 constexpr int kPadU = 4;   // dwords per lane and pass
-__global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* __restrict__ x, uint32_t* __restrict__ xp,
-                                                        uint32_t len, int32_t h, int32_t w, int32_t c4, int32_t hp,
-                                                        int32_t ph, int32_t pw, uint32_t rows) {
-    const uint32_t r = blockIdx.x * 4u + (threadIdx.x >> 6);
+struct PadArgs {
+    const uint32_t* x;
+    uint32_t* xp;
+    uint32_t len, rows;
+    int32_t h, w, c4, hp, ph, pw;
+};
+
+__device__ __forceinline__ void pad_rows(const PadArgs& a, uint32_t blk) {
+    const uint32_t* __restrict__ x = a.x;
+    uint32_t* __restrict__ xp = a.xp;
+    const uint32_t len = a.len, rows = a.rows;
+    const int32_t h = a.h, w = a.w, c4 = a.c4, hp = a.hp, ph = a.ph, pw = a.pw;
+    const uint32_t r = blk * 4u + (threadIdx.x >> 6);
     if (r >= rows) return;
     const uint32_t lane = threadIdx.x & 63;
     const uint32_t img = r / (uint32_t)hp;
@@ -605,16 +614,36 @@ __global__ __launch_bounds__(256) void pad_image_kernel(const uint32_t* __restri
     }
 }
 
-__global__ void repack_window_kernel(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
-                                     int64_t ktot) {
-    const int64_t total = k * ktot;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-        const int64_t kk = i / ktot, t = i - kk * ktot;
-        const int64_t row = t / lw, j = t - row * lw;
-        wr[i] = (row < r && j < sc) ? w[(kk * r + row) * sc + j] : (int8_t)0;
+__global__ __launch_bounds__(256) void pad_image_kernel(PadArgs a) { pad_rows(a, blockIdx.x); }
+
+// Window filter of few-channel layers: w [k][r][s*c] -> wr [k][ktot], each
+// filter row r at r*lw (zero past s*c and past the r rows).
+struct WinArgs {
+    const int8_t* w;
+    int8_t* wr;
+    int64_t k, r, sc, lw, ktot;
+};
+
+__device__ __forceinline__ void repack_window(const WinArgs& a, int64_t first, int64_t stride) {
+    const int64_t total = a.k * a.ktot;
+    for (int64_t i = first; i < total; i += stride) {
+        const int64_t kk = i / a.ktot, t = i - kk * a.ktot;
+        const int64_t row = t / a.lw, j = t - row * a.lw;
+        a.wr[i] = (row < a.r && j < a.sc) ? a.w[(kk * a.r + row) * a.sc + j] : (int8_t)0;
     }
 }
+
+// Both preparations of a few-channel convolution in one launch: workgroups
+// below pad_blocks copy the padded image, the others repack the filter.
+__global__ __launch_bounds__(256) void pad_repack_kernel(PadArgs pa, WinArgs wa, uint32_t pad_blocks) {
+    if (blockIdx.x < pad_blocks) {
+        pad_rows(pa, blockIdx.x);
+    } else {
+        const int64_t b = blockIdx.x - pad_blocks;
+        repack_window(wa, b * blockDim.x + threadIdx.x, (int64_t)(gridDim.x - pad_blocks) * blockDim.x);
+    }
+}
+
 
 __global__ void relu_mask_kernel(int8_t* e, const int8_t* a, int64_t n) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -760,16 +789,48 @@ hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int
     return hipGetLastError();
 }
 
-hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
-                         int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
+namespace {
+hipError_t pad_args(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp, int64_t wp,
+                    int64_t ph, int64_t pw, PadArgs& a) {
     const int64_t rows = n * hp;
     const int64_t len = wp * (c / 4);
-    if (rows <= 0 || len <= 0) return hipSuccess;
     if (rows * len >= ((int64_t)1 << 32) || rows >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
-    const int64_t grid = (rows + 3) / 4;
-    hipLaunchKernelGGL(pad_image_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, s, (const uint32_t*)x,
-                       (uint32_t*)xp, (uint32_t)len, (int32_t)h, (int32_t)w, (int32_t)(c / 4), (int32_t)hp,
-                       (int32_t)ph, (int32_t)pw, (uint32_t)rows);
+    a.x = (const uint32_t*)x;
+    a.xp = (uint32_t*)xp;
+    a.len = (uint32_t)(len > 0 ? len : 0);
+    a.rows = (uint32_t)(rows > 0 && len > 0 ? rows : 0);
+    a.h = (int32_t)h;
+    a.w = (int32_t)w;
+    a.c4 = (int32_t)(c / 4);
+    a.hp = (int32_t)hp;
+    a.ph = (int32_t)ph;
+    a.pw = (int32_t)pw;
+    return hipSuccess;
+}
+}  // namespace
+
+hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
+                         int64_t wp, int64_t ph, int64_t pw, hipStream_t s) {
+    PadArgs a;
+    hipError_t e = pad_args(x, xp, n, h, w, c, hp, wp, ph, pw, a);
+    if (e != hipSuccess) return e;
+    if (a.rows == 0) return hipSuccess;
+    hipLaunchKernelGGL(pad_image_kernel, dim3((a.rows + 3) / 4), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t pad_repack_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
+                          int64_t wp, int64_t ph, int64_t pw, const int8_t* wt, int8_t* wr, int64_t k, int64_t r,
+                          int64_t sc, int64_t lw, int64_t ktot, hipStream_t s) {
+    PadArgs a;
+    hipError_t e = pad_args(x, xp, n, h, w, c, hp, wp, ph, pw, a);
+    if (e != hipSuccess) return e;
+    const WinArgs wa{wt, wr, k, r, sc, lw, ktot};
+    const uint32_t pad_blocks = (a.rows + 3) / 4;
+    const int64_t total = k * ktot;
+    const uint32_t rep_blocks = total > 0 ? (uint32_t)grid_for(total, 4) : 0u;
+    if (pad_blocks + rep_blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(pad_repack_kernel, dim3(pad_blocks + rep_blocks), dim3(kThreads), 0, s, a, wa, pad_blocks);
     return hipGetLastError();
 }
 
@@ -781,14 +842,6 @@ hipError_t zero_classes_run(int8_t* out, int64_t n, int64_t h, int64_t w, int64_
     return hipGetLastError();
 }
 
-hipError_t repack_window_run(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
-                             int64_t ktot, hipStream_t s) {
-    const int64_t total = k * ktot;
-    if (total <= 0) return hipSuccess;
-    hipLaunchKernelGGL(repack_window_kernel, dim3(grid_for(total, 4)), dim3(kThreads), 0, s, w, wr, k, r, sc, lw,
-                       ktot);
-    return hipGetLastError();
-}
 
 hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;

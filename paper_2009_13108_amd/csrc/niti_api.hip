@@ -296,9 +296,8 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
         p.wgt_bytes = d->k * wp.ktot;
         p.win = 1;
         if (igemm_dma_eligible(b)) {
-            hipError_t e = pad_image_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, strm);
-            if (e != hipSuccess) return NITI_ERR_HIP;
-            e = repack_window_run(w, wr, d->k, d->r, d->s * d->c, wp.lw, wp.ktot, strm);
+            hipError_t e = pad_repack_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, w, wr,
+                                          d->k, d->r, d->s * d->c, wp.lw, wp.ktot, strm);
             if (e != hipSuccess) return NITI_ERR_HIP;
             return hip_status(igemm_run(b, ctl, strm));
         }

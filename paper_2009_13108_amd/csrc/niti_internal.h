@@ -164,7 +164,10 @@ hipError_t pad_image_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int6
                          int64_t wp, int64_t ph, int64_t pw, hipStream_t s);
 // Filter rows as zero-extended windows: wr[k][t], t < ktot: row t / lw, byte
 // t % lw of w[k][row][S*C] (zero past S*C and past R rows).
-hipError_t repack_window_run(const int8_t* w, int8_t* wr, int64_t k, int64_t r, int64_t sc, int64_t lw,
-                             int64_t ktot, hipStream_t s);
+// Padded image copy and window filter repack of a few-channel convolution in
+// one launch.
+hipError_t pad_repack_run(const int8_t* x, int8_t* xp, int64_t n, int64_t h, int64_t w, int64_t c, int64_t hp,
+                          int64_t wp, int64_t ph, int64_t pw, const int8_t* wt, int8_t* wr, int64_t k, int64_t r,
+                          int64_t sc, int64_t lw, int64_t ktot, hipStream_t s);
 
 }  // namespace niti
