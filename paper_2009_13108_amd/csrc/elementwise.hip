@@ -338,12 +338,14 @@ __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __r
         const bool taylor = s_a <= -7;
         const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
         if constexpr (NPL > 0) {
+            // All NPL loads in flight at once: entries past the row read its
+            // last entry (in bounds, unconditional) and are zeroed after.
             int av[NPL];
 #pragma unroll
-            for (int j = 0; j < NPL; j++) {
-                const int i = lane + 64 * j;
-                av[j] = i < classes ? (int)a[i] : 0;
-            }
+            for (int j = 0; j < NPL; j++) av[j] = (int)a[min((int64_t)(lane + 64 * j), classes - 1)];
+#pragma unroll
+            for (int j = 0; j < NPL; j++)
+                if (lane + 64 * j >= classes) av[j] = 0;
             int64_t t[NPL];
             int64_t C = 0;
             if (taylor) {
