@@ -75,6 +75,7 @@ class ResNetStep:
                  "y": torch.empty(d.y_shape(), dtype=torch.int8, device=dev),
                  "dx": torch.empty(d.x_shape(), dtype=torch.int8, device=dev),
                  "stats": nst, "bwd_data": not name.startswith("stem"),
+                 "packed": [niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, d)) for _ in range(count)],
                  "macs": conv_macs(batch, c_real, hw, hw, cout, k, k, st, pd)}
             nst += 3 * count
             ws = max(ws, niti.workspace_bytes(niti.OP_CONV_FWD, d),
@@ -92,6 +93,7 @@ class ResNetStep:
         self.s_feat = torch.tensor([-9], dtype=torch.int8, device=dev)
         self.s_wfc = torch.tensor([-11], dtype=torch.int8, device=dev)
         self.s_logits = torch.zeros(1, dtype=torch.int8, device=dev)
+        self.fc_packed = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, self.fc_desc))
         self.fc_stats = nst
         nst += 4
         self.fc_macs = batch * fin * fout
@@ -113,6 +115,7 @@ class ResNetStep:
         self.ev_bwd = [torch.cuda.Event() for _ in range(sum(L["count"] for L in self.layers) + 1)]
         self.ev_fwd = [torch.cuda.Event() for _ in range(8)]
         self.ev_upd = torch.cuda.Event()
+        self.ev_pack = torch.cuda.Event()
         self.ev_upd.record(self.sB)
         self.fam_ops = {"igemm": 0, "wgrad": 0}
         for L in self.layers:
@@ -181,11 +184,23 @@ class ResNetStep:
                           False, stats_index=s)
             niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats, self.ws,
                                   stats_index=s + 1)
-            niti.conv_bwd_data(fd, self.err.view(Bsz, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
-                               self.dfeat.view(Bsz, 1, 1, fin), self.stats, self.ws,
-                               relu_src=self.feat.view(Bsz, 1, 1, fin), stats_index=s + 2)
+            niti.conv_bwd_data_packed(fd, self.err.view(Bsz, 1, 1, fout), self.fc_packed,
+                                      self.dfeat.view(Bsz, 1, 1, fin), self.stats,
+                                      relu_src=self.feat.view(Bsz, 1, 1, fin), stats_index=s + 2)
+
+        def pack_filters():
+            for L in self.layers:
+                if L["bwd_data"]:
+                    for c in range(L["count"]):
+                        niti.conv_pack_bwd_data(L["desc"], L["w"][c], L["packed"][c])
+            niti.conv_pack_bwd_data(fd, self.wfc.view(fout, 1, 1, fin), self.fc_packed)
 
         wait(A, self.ev_upd)             # the previous step's weight updates
+        # The filters rearranged for the back-propagation, on stream B (in
+        # order after the previous step's updates, and nearly idle in the
+        # forward pass); A waits for them before the back-propagation.
+        seg(B, pack_filters)
+        rec(self.ev_pack, B)
         # Forward.  A downsampling block's 1x1 projection reads the block input,
         # as its first 3x3 convolution does, and its output is needed only when
         # the block's two branches are added, before the next block: it runs on
@@ -207,6 +222,7 @@ class ResNetStep:
                     wait(A, pending)                  # both branches done before the next block
                     pending = None
                 seg(A, lambda: conv_fwd(L, c, self.ws))
+        wait(A, self.ev_pack)
         seg(A, head)
         ev = 0
         rec(self.ev_bwd[ev], A)
@@ -226,8 +242,9 @@ class ResNetStep:
                     seg(A, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu,
                                                         stats_index=s0 + 2))
                     continue
-                seg(A, lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws,
-                                                  relu_src=L["x"], stats_index=s0 + 1))
+                pk = L["packed"][c]
+                seg(A, lambda: niti.conv_bwd_data_packed(d, L["dy"], pk, L["dx"], self.stats,
+                                                         relu_src=L["x"], stats_index=s0 + 1))
                 ev += 1
                 rec(self.ev_bwd[ev], A)
                 wait(B, self.ev_bwd[ev])

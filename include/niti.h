@@ -154,6 +154,24 @@ niti_status niti_conv_bwd_data(const niti_conv_desc *d, const int8_t *dy, const 
                                int8_t *dx, const int8_t *relu_src, niti_round_mode mode,
                                niti_stats *stats, void *ws, size_t ws_bytes, void *stream);
 
+/* niti_conv_bwd_data in two parts, for callers that take the filter
+ * rearrangement off the back-propagation's critical path (Algorithm 1: the
+ * filter w of layer l is fixed from its forward use until its update, so
+ * it can be rearranged any time in between).  niti_conv_pack_bwd_data
+ * writes the filter w (KRSC, device) rearranged per sub-pixel class into
+ * packed (device, caller-owned, 16-byte aligned, at least
+ * niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, ...) bytes); it stays
+ * valid until w changes.  niti_conv_bwd_data_packed then computes what
+ * niti_conv_bwd_data computes for that w, from packed and without a
+ * workspace; packed_bytes is checked as above.  Same errors as
+ * niti_conv_bwd_data (NITI_ERR_WORKSPACE for a short packed buffer). */
+niti_status niti_conv_pack_bwd_data(const niti_conv_desc *d, const int8_t *w, void *packed,
+                                    size_t packed_bytes, void *stream);
+niti_status niti_conv_bwd_data_packed(const niti_conv_desc *d, const int8_t *dy,
+                                      const void *packed, int8_t *dx, const int8_t *relu_src,
+                                      niti_round_mode mode, niti_stats *stats,
+                                      size_t packed_bytes, void *stream);
+
 /* Weight gradient and discrete update (Algorithm 1, g(l) = a(l-1) (x) e(l)
  * then w <- w - g; Section 3.3).  g32 = sum over n, p, q of dy x x, exact
  * mod 2^32; b = B(g32); g = round(g32, max(0, b - mu)); w <- w - g held to

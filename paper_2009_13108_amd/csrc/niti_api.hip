@@ -317,24 +317,30 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
     return hip_status(igemm_run(b, ctl, strm));
 }
 
-niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const int8_t* w, int8_t* dx,
-                               const int8_t* relu_src, niti_round_mode mode, niti_stats* stats, void* ws,
-                               size_t ws_bytes, void* stream) {
-    int64_t P, Q;
-    if (!d) return NITI_ERR_NULL;
-    if (!dy || !w || !dx || !stats) return NITI_ERR_NULL;
-    if (mis16(dy) || mis16(w) || mis16(dx) || mis16(relu_src) || mis16(ws)) return NITI_ERR_ARG;
-    if (!valid_mode(mode)) return NITI_ERR_ARG;
-    niti_status s = check_conv(d, &P, &Q);
-    if (s != NITI_OK) return s;
-    const size_t need = niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0);
-    if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
+namespace {
+
+// The sub-pixel classes of a back-propagation (Algorithm 1's e(l-1) = w (x)
+// e(l) over a strided filter: one implicit-GEMM problem per class of output
+// pixels that sees the same filter taps) over the class filters packed at
+// `packed`.
+struct DgradPlan {
+    DgradClass cls[kMaxProblems];
+    int ncls = 0;
+    IgemmBatch b{};
+    uint32_t zero_mask = 0;  // classes without taps: exact zeros, written apart
+    int8_t* dx = nullptr;
+};
+
+void plan_dgrad(const niti_conv_desc* d, int64_t P, int64_t Q, const int8_t* dy, const int8_t* packed, int8_t* dx,
+                const int8_t* relu_src, DgradPlan& pl) {
     const int st = d->stride_h;
     const int K = (int)d->k, R = (int)d->r, S = (int)d->s, C = (int)d->c;
-    DgradClass cls[kMaxProblems];
-    IgemmBatch b{};
-    int ncls = 0;
-    uint32_t zero_mask = 0;  // classes without taps: exact zeros, written apart
+    DgradClass* cls = pl.cls;
+    IgemmBatch& b = pl.b;
+    int& ncls = pl.ncls;
+    uint32_t& zero_mask = pl.zero_mask;
+    const void* ws = packed;
+    pl.dx = dx;
     int64_t off = 0;
     for (int a = 0; a < st; a++) {
         for (int bb = 0; bb < st; bb++) {
@@ -389,9 +395,21 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
         b.p[0].zsib = 7;
         zero_mask = 0;
     }
-    hipError_t e = repack_dgrad_run(w, (int8_t*)ws, cls, ncls, K, R, S, C, st, st, as_stream(stream));
-    if (e != hipSuccess) return NITI_ERR_HIP;
-    e = zero_classes_run(dx, d->n, d->h, d->w, d->c, st, zero_mask, as_stream(stream));
+}
+
+hipError_t pack_dgrad(const niti_conv_desc* d, const int8_t* w, int8_t* packed, const DgradPlan& pl,
+                      hipStream_t stream) {
+    const int st = d->stride_h;
+    return repack_dgrad_run(w, packed, pl.cls, pl.ncls, (int)d->k, (int)d->r, (int)d->s, (int)d->c, st, st, stream);
+}
+
+// Zero classes, then the classes with taps (or, with none, an all-zero dx).
+niti_status run_dgrad(const niti_conv_desc* d, DgradPlan& pl, niti_round_mode mode, niti_stats* stats,
+                      void* stream) {
+    const int st = d->stride_h;
+    const int K = (int)d->k, R = (int)d->r, S = (int)d->s;
+    IgemmBatch& b = pl.b;
+    hipError_t e = zero_classes_run(pl.dx, d->n, d->h, d->w, d->c, st, pl.zero_mask, as_stream(stream));
     if (e != hipSuccess) return NITI_ERR_HIP;
     if (b.nprob == 0) {
         // No class has taps (a 1x1 filter that only ever sees padding): dx is
@@ -409,6 +427,65 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
     ctl.mode = mode;
     ctl.static_flags = acc_flags((int64_t)K * R * S);
     return hip_status(igemm_run(b, ctl, as_stream(stream)));
+}
+
+// Shared argument checks of the back-propagation entry points.
+niti_status check_dgrad(const niti_conv_desc* d, const int8_t* dy, const void* packed, int8_t* dx,
+                        const int8_t* relu_src, niti_round_mode mode, niti_stats* stats, size_t packed_bytes,
+                        int64_t* P, int64_t* Q) {
+    if (!d) return NITI_ERR_NULL;
+    if (!dy || !packed || !dx || !stats) return NITI_ERR_NULL;
+    if (mis16(dy) || mis16(packed) || mis16(dx) || mis16(relu_src)) return NITI_ERR_ARG;
+    if (!valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, P, Q);
+    if (s != NITI_OK) return s;
+    if (packed_bytes < niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0)) return NITI_ERR_WORKSPACE;
+    return NITI_OK;
+}
+
+}  // namespace
+
+niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const int8_t* w, int8_t* dx,
+                               const int8_t* relu_src, niti_round_mode mode, niti_stats* stats, void* ws,
+                               size_t ws_bytes, void* stream) {
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!dy || !w || !dx || !stats) return NITI_ERR_NULL;
+    if (mis16(dy) || mis16(w) || mis16(dx) || mis16(relu_src) || mis16(ws)) return NITI_ERR_ARG;
+    if (!valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    const size_t need = niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0);
+    if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
+    DgradPlan pl;
+    plan_dgrad(d, P, Q, dy, (const int8_t*)ws, dx, relu_src, pl);
+    if (pack_dgrad(d, w, (int8_t*)ws, pl, as_stream(stream)) != hipSuccess) return NITI_ERR_HIP;
+    return run_dgrad(d, pl, mode, stats, stream);
+}
+
+niti_status niti_conv_pack_bwd_data(const niti_conv_desc* d, const int8_t* w, void* packed, size_t packed_bytes,
+                                    void* stream) {
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!w || !packed) return NITI_ERR_NULL;
+    if (mis16(w) || mis16(packed)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    if (packed_bytes < niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0)) return NITI_ERR_WORKSPACE;
+    DgradPlan pl;
+    plan_dgrad(d, P, Q, nullptr, (const int8_t*)packed, nullptr, nullptr, pl);
+    return hip_status(pack_dgrad(d, w, (int8_t*)packed, pl, as_stream(stream)));
+}
+
+niti_status niti_conv_bwd_data_packed(const niti_conv_desc* d, const int8_t* dy, const void* packed, int8_t* dx,
+                                      const int8_t* relu_src, niti_round_mode mode, niti_stats* stats,
+                                      size_t packed_bytes, void* stream) {
+    int64_t P, Q;
+    niti_status s = check_dgrad(d, dy, packed, dx, relu_src, mode, stats, packed_bytes, &P, &Q);
+    if (s != NITI_OK) return s;
+    DgradPlan pl;
+    plan_dgrad(d, P, Q, dy, (const int8_t*)packed, dx, relu_src, pl);
+    return run_dgrad(d, pl, mode, stats, stream);
 }
 
 niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const int8_t* dy, int8_t* w,

@@ -80,7 +80,8 @@ _lock = threading.Lock()
 _lib = None
 
 EXPORTS = [
-    "niti_gemm_fwd", "niti_conv_fwd", "niti_conv_bwd_data", "niti_conv_bwd_weight",
+    "niti_gemm_fwd", "niti_conv_fwd", "niti_conv_bwd_data", "niti_conv_pack_bwd_data",
+    "niti_conv_bwd_data_packed", "niti_conv_bwd_weight",
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
     "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read",
@@ -103,6 +104,8 @@ def lib():
                 "niti_gemm_fwd": [P, P, P, I64, I64, I64, P, P, P, I, I, I, P, P],
                 "niti_conv_fwd": [P, P, P, P, P, P, P, I, I, P, P, Z, P],
                 "niti_conv_bwd_data": [P, P, P, P, P, I, P, P, Z, P],
+                "niti_conv_pack_bwd_data": [P, P, P, Z, P],
+                "niti_conv_bwd_data_packed": [P, P, P, P, P, I, P, Z, P],
                 "niti_conv_bwd_weight": [P, P, P, P, P, I, I, P, P, Z, P],
                 "niti_round_psr": [P, P, I64, I, I, I, P, P, P, P],
                 "niti_int_ce_loss_grad": [P, P, P, P, I64, I64, I, P, P, Z, P],
@@ -310,6 +313,21 @@ def conv_bwd_data(d: ConvDesc, dy, w, dx, stats, ws, relu_src=None, mode=PSR, st
     _dev(ws, torch.uint8, "ws")
     _run("niti_conv_bwd_data", ctypes.byref(d), _ptr(dy), _ptr(w), _ptr(dx), _ptr(relu_src), int(mode),
                                     _stats_ptr(stats, stats_index), _ptr(ws), ws.numel(), _stream(stream))
+
+
+def conv_pack_bwd_data(d: ConvDesc, w, packed, stream=None):
+    torch = _torch()
+    _conv_check(d, w=w)
+    _dev(packed, torch.uint8, "packed")
+    _run("niti_conv_pack_bwd_data", ctypes.byref(d), _ptr(w), _ptr(packed), packed.numel(), _stream(stream))
+
+
+def conv_bwd_data_packed(d: ConvDesc, dy, packed, dx, stats, relu_src=None, mode=PSR, stats_index=0, stream=None):
+    torch = _torch()
+    _conv_check(d, dy=dy, dx=dx, relu_src=relu_src)
+    _dev(packed, torch.uint8, "packed")
+    _run("niti_conv_bwd_data_packed", ctypes.byref(d), _ptr(dy), _ptr(packed), _ptr(dx), _ptr(relu_src), int(mode),
+         _stats_ptr(stats, stats_index), packed.numel(), _stream(stream))
 
 
 def conv_bwd_weight(d: ConvDesc, x, dy, w, stats, ws=None, g32_out=None, mu=5, mode=PSR, stats_index=0,

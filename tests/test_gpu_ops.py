@@ -124,6 +124,7 @@ CONV_CASES = [
     # classes of unequal size)
     (2, 32, 9, 11, 64, 3, 3, 2, 1, True),
     (1, 64, 8, 8, 128, 3, 3, 2, 1, False),
+    (2, 128, 13, 13, 256, 3, 3, 2, 1, True),
     # strided 1x1: three of four sub-pixel classes have no taps
     (2, 64, 14, 14, 128, 1, 1, 2, 0, True),
     (2, 64, 7, 9, 256, 1, 1, 2, 0, False),
@@ -184,6 +185,33 @@ def test_conv_bwd_data_parity(case):
     for rep in range(2):
         dx.fill_(55)
         niti.conv_bwd_data(gd, dev(nhwc(dy)), dev(krsc(wt)), dx, stats, ws, relu_src=mask)
+        torch.cuda.synchronize()
+        g = niti.read_stats(stats)[0]
+        assert (nchw(host(dx)) == exp_out).all(), "rep %d" % rep
+        assert same_stats(g, st)
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_bwd_data_packed_parity(case):
+    """The filter packed once, then changed in place: the packed calls still
+    compute the back-propagation of the filter as it was packed."""
+    import torch
+    say("conv_bwd_data_packed", case)
+    d, gd, x, wt, dy = _conv_inputs(case, 5 * case[2] + case[4])
+    use_mask = case[-1]
+    relu_src = I.weights(57, (d.n, d.c, d.h, d.w)) if use_mask else None
+    exp_out, _, st = oracle.conv_bwd_data(d, dy, wt, relu_src=relu_src)
+    dx = torch.empty(gd.x_shape(), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats()
+    packed = niti.new_workspace(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, gd))
+    packed.fill_(0x5A)
+    w = dev(krsc(wt))
+    mask = dev(nhwc(relu_src)) if use_mask else None
+    niti.conv_pack_bwd_data(gd, w, packed)
+    w.fill_(3)
+    for rep in range(2):
+        dx.fill_(55)
+        niti.conv_bwd_data_packed(gd, dev(nhwc(dy)), packed, dx, stats, relu_src=mask)
         torch.cuda.synchronize()
         g = niti.read_stats(stats)[0]
         assert (nchw(host(dx)) == exp_out).all(), "rep %d" % rep
