@@ -339,7 +339,6 @@ void plan_dgrad(const niti_conv_desc* d, int64_t P, int64_t Q, const int8_t* dy,
     IgemmBatch& b = pl.b;
     int& ncls = pl.ncls;
     uint32_t& zero_mask = pl.zero_mask;
-    const void* ws = packed;
     pl.dx = dx;
     int64_t off = 0;
     for (int a = 0; a < st; a++) {
@@ -363,7 +362,7 @@ void plan_dgrad(const niti_conv_desc* d, int64_t P, int64_t Q, const int8_t* dy,
             const int da = (a + d->pad_h - c.r0) / st;
             const int db = (bb + d->pad_w - c.s0) / st;
             p.act = dy;
-            p.wgt = (const int8_t*)ws + c.offset;
+            p.wgt = packed + c.offset;
             p.out = dx;
             p.mask = relu_src;
             p.Nout = C;
