@@ -109,7 +109,8 @@ class ResNetStep:
         # next layer's back-propagation (the image layer's, which has no
         # back-propagation, runs on A after the chain).  B's update of w(l) follows A's
         # back-propagation of layer l (which reads w(l)), and the next step's
-        # forward pass follows all of B's updates.
+        # forward pass follows all of B's updates from its second layer on (the
+        # image layer's filter is updated on A).
         self.sA = torch.cuda.Stream()
         self.sB = torch.cuda.Stream()
         self.ev_bwd = [torch.cuda.Event() for _ in range(sum(L["count"] for L in self.layers) + 1)]
@@ -195,7 +196,6 @@ class ResNetStep:
                         niti.conv_pack_bwd_data(L["desc"], L["w"][c], L["packed"][c])
             niti.conv_pack_bwd_data(fd, self.wfc.view(fout, 1, 1, fin), self.fc_packed)
 
-        wait(A, self.ev_upd)             # the previous step's weight updates
         # The filters rearranged for the back-propagation, on stream B (in
         # order after the previous step's updates, and nearly idle in the
         # forward pass); A waits for them before the back-propagation.
@@ -207,7 +207,14 @@ class ResNetStep:
         # stream B (idle in the forward pass) beside the two 3x3 convolutions.
         blk = 0
         pending = None
+        upd_waited = False
         for L in self.layers:
+            if L["bwd_data"] and not upd_waited:
+                # The image layer's filter is updated on A itself, so its
+                # forward overlaps B's last weight updates; every later layer
+                # waits for them.
+                wait(A, self.ev_upd)
+                upd_waited = True
             if L["name"].endswith("_1x1s2"):
                 seg(B, lambda: conv_fwd(L, 0, self.ws_b))
                 pending = self.ev_fwd[2 * blk + 1]
@@ -251,7 +258,6 @@ class ResNetStep:
                 seg(B, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws_b, mu=self.mu,
                                                     stats_index=s0 + 2))
         rec(self.ev_upd, B)
-        wait(A, self.ev_upd)
 
     def prepare(self):
         """Run one step and keep it as a plan for step_prepared()."""
@@ -527,7 +533,7 @@ def main():
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(job.sA)   # a step starts and ends on stream A (A waits for B's updates)
+    e0.record(job.sA)   # steps start on stream A; A waits for B's last updates before e1
     h0 = time.perf_counter()
     for _ in range(args.steps):
         if prepared:
@@ -535,6 +541,7 @@ def main():
         else:
             job.step()
     host_ms = (time.perf_counter() - h0) * 1e3 / args.steps
+    job.sA.wait_event(job.ev_upd)
     e1.record(job.sA)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
