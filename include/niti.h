@@ -183,6 +183,29 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc *d, const int8_t *x, const
                                  int8_t *w, int32_t *g32_out, int mu, niti_round_mode mode,
                                  niti_stats *stats, void *ws, size_t ws_bytes, void *stream);
 
+/* niti_conv_bwd_weight for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc):
+ * the same computation and results, with the temporary memory (split
+ * partial sums, the int32 gradient when g32_out is NULL, the padded input
+ * copy of few-channel layers) taken from a fixed array of
+ * NITI_NOALLOC_SCRATCH_BYTES inside the library instead of a workspace.
+ * Each GPU that the library runs on holds its own copy of that array until
+ * the process ends; the array's address on the current device is looked up
+ * on the first call made on that device, so the current device must be the
+ * device of `stream`.  The call allocates and frees nothing.  Calls whose
+ * niti_workspace_bytes(NITI_OP_CONV_BWD_WEIGHT, d, ...) exceeds
+ * NITI_NOALLOC_SCRATCH_BYTES return NITI_ERR_WORKSPACE before anything is
+ * enqueued.  Every call on one GPU uses the same array: two such calls whose
+ * work overlaps on one GPU (different streams, no ordering between them)
+ * race and give wrong results; calls in order on one stream are safe.  No
+ * part of the array needs to start at zero (every value a kernel reads from
+ * it was written earlier in the same call).  Other errors as
+ * niti_conv_bwd_weight. */
+#define NITI_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+niti_status niti_conv_bwd_weight_noalloc(const niti_conv_desc *d, const int8_t *x, const int8_t *dy,
+                                         int8_t *w, int32_t *g32_out, int mu, niti_round_mode mode,
+                                         niti_stats *stats, void *stream);
+
 /* Shift and round an int32 tensor (Algorithm 2 with Algorithm 3).  bp >= 0
  * rounds with that binary point (stats may be NULL; magnitudes are held at
  * 127); bp < 0 finds the block exponent first, bp = max(0, B(x) -

@@ -3,7 +3,16 @@
 // memory or waits on the device.
 #include <limits.h>
 
+#include <mutex>
+
 #include "niti_internal.h"
+
+// Temporary memory of niti_conv_bwd_weight_noalloc: one fixed array per GPU
+// (each device that loads this library holds its own copy until the process
+// ends).  In host code this name is only a handle for the runtime; the array's
+// device address is resolved per device with hipGetSymbolAddress below and
+// only that address is passed to kernels.
+static __device__ __align__(256) uint8_t scratch[NITI_NOALLOC_SCRATCH_BYTES];
 
 using namespace niti;
 
@@ -534,6 +543,52 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
     return hip_status(update_run(w, g32, nw, mu, mode, stats, acc_flags(npix), strm));
+}
+
+namespace {
+
+constexpr size_t kScratchBytes = NITI_NOALLOC_SCRATCH_BYTES;   // size of `scratch`
+constexpr int kMaxDevices = 64;
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch` per device, once resolved
+
+// Device address of this device's copy of `scratch`, resolved on the first
+// call made on each device (with that device current).
+niti_status scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return NITI_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return NITI_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return NITI_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return NITI_OK;
+}
+
+}  // namespace
+
+niti_status niti_conv_bwd_weight_noalloc(const niti_conv_desc* d, const int8_t* x, const int8_t* dy, int8_t* w,
+                                         int32_t* g32_out, int mu, niti_round_mode mode, niti_stats* stats,
+                                         void* stream) {
+    // The checks of niti_conv_bwd_weight that do not involve the workspace,
+    // made here first so that a rejected call touches no device state.
+    int64_t P, Q;
+    if (!d) return NITI_ERR_NULL;
+    if (!x || !dy || !w || !stats) return NITI_ERR_NULL;
+    if (mis16(x) || mis16(dy) || mis16(w) || mis16(g32_out)) return NITI_ERR_ARG;
+    if (mu < 1 || mu > 8 || !valid_mode(mode)) return NITI_ERR_ARG;
+    niti_status s = check_conv(d, &P, &Q);
+    if (s != NITI_OK) return s;
+    if (too_big(d->n * P * Q)) return NITI_ERR_UNSUPPORTED;
+    if (niti_workspace_bytes(NITI_OP_CONV_BWD_WEIGHT, d, 0, 0, 0) > kScratchBytes) return NITI_ERR_WORKSPACE;
+    void* ws = nullptr;
+    s = scratch_address(&ws);
+    if (s != NITI_OK) return s;
+    return niti_conv_bwd_weight(d, x, dy, w, g32_out, mu, mode, stats, ws, kScratchBytes, stream);
 }
 
 niti_status niti_round_psr(const int32_t* x, int8_t* y, int64_t n, int bp, int target_bits,

@@ -81,7 +81,7 @@ _lib = None
 
 EXPORTS = [
     "niti_gemm_fwd", "niti_conv_fwd", "niti_conv_bwd_data", "niti_conv_pack_bwd_data",
-    "niti_conv_bwd_data_packed", "niti_conv_bwd_weight",
+    "niti_conv_bwd_data_packed", "niti_conv_bwd_weight", "niti_conv_bwd_weight_noalloc",
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
     "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read",
@@ -107,6 +107,7 @@ def lib():
                 "niti_conv_pack_bwd_data": [P, P, P, Z, P],
                 "niti_conv_bwd_data_packed": [P, P, P, P, P, I, P, Z, P],
                 "niti_conv_bwd_weight": [P, P, P, P, P, I, I, P, P, Z, P],
+                "niti_conv_bwd_weight_noalloc": [P, P, P, P, P, I, I, P, P],
                 "niti_round_psr": [P, P, I64, I, I, I, P, P, P, P],
                 "niti_int_ce_loss_grad": [P, P, P, P, I64, I64, I, P, P, Z, P],
                 "niti_sgd_update": [P, P, I64, I, I, P, P],
@@ -343,6 +344,22 @@ def conv_bwd_weight(d: ConvDesc, x, dy, w, stats, ws=None, g32_out=None, mu=5, m
     _run("niti_conv_bwd_weight", ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(w), _ptr(g32_out), int(mu),
                                       int(mode), _stats_ptr(stats, stats_index), _ptr(ws),
                                       ws.numel() if ws is not None else 0, _stream(stream))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def conv_bwd_weight_noalloc(d: ConvDesc, x, dy, w, stats, g32_out=None, mu=5, mode=PSR, stats_index=0,
+                            stream=None):
+    """conv_bwd_weight with the library's fixed per-GPU scratch array in place of a workspace."""
+    torch = _torch()
+    _conv_check(d, x=x, dy=dy, w=w)
+    if g32_out is not None:
+        _dev(g32_out, torch.int32, "g32_out")
+        if tuple(g32_out.shape) != tuple(d.w_shape()):
+            raise ValueError("g32_out shape")
+    _run("niti_conv_bwd_weight_noalloc", ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(w), _ptr(g32_out), int(mu),
+         int(mode), _stats_ptr(stats, stats_index), _stream(stream))
 
 
 def round_psr(x, y, bp=-1, target_bits=7, stats=None, s_in=None, s_out=None, mode=PSR, stats_index=0,

@@ -125,3 +125,18 @@ def test_misaligned_pointers_rejected():
     assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, odd, None, None, None, 0, 0, FAKE,
                            None, 0, None) == -6
     assert L.niti_sgd_update(FAKE, odd, 16, 5, 0, S, None) == -6
+
+
+def test_noalloc_weight_gradient_rejects_on_host():
+    """The workspace-free weight gradient checks its arguments and the size
+    of its fixed scratch array before it touches any device."""
+    L = niti.lib()
+    big = niti.ConvDesc.make(256, 224, 224, 4, 64, 7, 7, 2, 3)       # ~88 MiB of temporary memory
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, big) > niti.NOALLOC_SCRATCH_BYTES
+    assert L.niti_conv_bwd_weight_noalloc(ctypes.byref(big), FAKE, FAKE, FAKE, None, 5, 0, FAKE, None) == -4
+    d = niti.ConvDesc.make(2, 8, 8, 64, 16, 3, 3, 1, 1)
+    assert L.niti_conv_bwd_weight_noalloc(None, FAKE, FAKE, FAKE, None, 5, 0, FAKE, None) == -1
+    assert L.niti_conv_bwd_weight_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, None, 5, 0, None, None) == -1
+    assert L.niti_conv_bwd_weight_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE, None, 9, 0, FAKE, None) == -6
+    odd = niti.ConvDesc.make(2, 8, 8, 3, 16, 3, 3, 1, 1)
+    assert L.niti_conv_bwd_weight_noalloc(ctypes.byref(odd), FAKE, FAKE, FAKE, None, 5, 0, FAKE, None) == -3
