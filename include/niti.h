@@ -73,9 +73,10 @@ typedef enum niti_round_mode {
 } niti_round_mode;
 
 /* niti_stats.flags bits */
-#define NITI_FLAG_ACC_BOUND 1u  /* reduction long enough that int32 sums may wrap (K*127*127 >= 2^31); sums are kept mod 2^32 */
+#define NITI_FLAG_ACC_BOUND 1u  /* reduction of 2^17 or more int8 products, so int32 sums may wrap (each product is
+                                   at most 2^14 in magnitude); sums are kept mod 2^32 */
 #define NITI_FLAG_EXP_RANGE 2u  /* an output exponent left [-128, 127] and was held at the end */
-#define NITI_FLAG_LOSS_SA   4u  /* loss exponent below -22: the Taylor branch used s_a = -22 */
+#define NITI_FLAG_LOSS_SA   4u  /* loss exponent below -54: evaluated at s_a = -54 (same int8 error) */
 #define NITI_FLAG_HINT_MISS 8u  /* the speculated binary point was wrong; the output was recomputed */
 
 /* Per-tensor statistics and working state, 128 bytes of device memory.
@@ -218,11 +219,15 @@ niti_status niti_round_psr(const int32_t *x, int8_t *y, int64_t n, int bp, int t
 /* Integer cross-entropy gradient (Section 3.5).  logits [batch][classes]
  * int8 with exponent *s_logits; labels int32 in [0, classes).  Per sample:
  * s_a <= -7 uses t_i = 2^(1-2 s_a) + a_i 2^(1-s_a) + a_i^2 (second-order
- * Taylor series, scaled to integers; s_a below -22 is taken as -22 and
- * flagged); s_a > -7 uses t_i = 1 << max(0, xhat_i - p) with
- * xhat_i = floor(47274 a_i 2^(s_a-15)) and p = max(xhat) - 10.  Then
- * e32_i = t_i - [i == label] sum(t), and err = round(e32) with target 7 over
- * the whole batch.  classes in 1..65536.  Workspace:
+ * Taylor series, scaled to integers and evaluated exactly in 128-bit
+ * integers; below s_a = -54 the int8 result no longer depends on s_a, so
+ * s_a = -54 is evaluated and NITI_FLAG_LOSS_SA is set); s_a > -7 uses
+ * t_i = 1 << max(0, xhat_i - p) with xhat_i = floor(47274 a_i 2^(s_a-15))
+ * and p = max(xhat) - 10.  Then e_i = t_i - [i == label] sum(t), and
+ * err = round(e) with target 7 over the whole batch.  stats.b and stats.bp
+ * are exact; below s_a = -22 the largest |e_i| can exceed 64 bits, and
+ * stats.max_abs holds it shifted right by 2 (-22 - s_a) bits.  classes in
+ * 1..65536.  Workspace (16 bytes per logit):
  * niti_workspace_bytes(NITI_OP_INT_CE_LOSS, NULL, batch, classes, 0). */
 niti_status niti_int_ce_loss_grad(const int8_t *logits, const int8_t *s_logits,
                                   const int32_t *labels, int8_t *err, int64_t batch,

@@ -26,9 +26,11 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 _lock = threading.Lock()
 _lib = None
 
-FLAG_ACC_BOUND = 1
+FLAG_ACC_BOUND = 1    # reduction of 2^17 or more products: int32 sums may wrap
 FLAG_EXP_RANGE = 2
 FLAG_LOSS_SA = 4
+FLAG_ACC_WRAP = 16    # oracle only: an exact sum left the int32 range
+ACC_BOUND_LEN = 1 << 17
 
 PSR = 0
 RTN = 1
@@ -82,10 +84,10 @@ def _load():
                 "orc_conv_bwd_data_raw": (None, [P, P, P, P]),
                 "orc_conv_bwd_weight_raw": (None, [P, P, P, P]),
                 "orc_conv_fwd_one": (I64, [P, P, P, I64, I64, I64, I64]),
-                "orc_finish_i64": (None, [P, I64, I, I, I, P, P, P]),
+                "orc_finish_i64": (None, [P, I64, I, I, I, P, P, P, I64]),
                 "orc_sgd_update": (None, [P, P, I64, I, I, P]),
                 "orc_loss_t_case": (I, [I]),
-                "orc_int_ce_loss_grad": (None, [P, I, P, I64, I64, I, P, P, P]),
+                "orc_int_ce_loss_grad": (None, [P, I, P, I64, I64, I, P, P, P, P]),
                 "orc_relu_mask": (None, [P, P, I64]),
                 "orc_maxpool2_fwd": (None, [P, I64, I64, I64, I64, P, P]),
                 "orc_maxpool2_bwd": (None, [P, P, I64, I64, I64, I64, P]),
@@ -253,8 +255,9 @@ def conv_fwd_one(d: Conv, x, w, n, k, p, q):
 
 
 # ---------------------------------------------------------------- composites
-def finish(S, relu: bool, target: int, mode: int = PSR):
+def finish(S, relu: bool, target: int, mode: int = PSR, red_len: int = 0):
     """Exact sums -> int32 accumulators -> (ReLU) -> block exponent -> int8.
+    red_len: products per sum (FLAG_ACC_BOUND when >= 2^17).
 
     Returns (int8 out, int32 accumulators, stats dict)."""
     S, ps = _c(S, np.int64)
@@ -262,23 +265,23 @@ def finish(S, relu: bool, target: int, mode: int = PSR):
     acc = np.empty(S.shape, np.int32)
     st = Stats()
     _load().orc_finish_i64(ps, S.size, int(bool(relu)), int(target), int(mode),
-                           _ptr(out), _ptr(acc), ctypes.byref(st))
+                           _ptr(out), _ptr(acc), ctypes.byref(st), int(red_len))
     return out, acc, st.as_dict()
 
 
 def gemm_fwd(A, B, relu=False, mode=PSR, target=7):
     """Fully-connected / plain GEMM forward step: int8 A (M x K), B (N x K)."""
-    return finish(gemm_nt_raw(A, B), relu, target, mode)
+    return finish(gemm_nt_raw(A, B), relu, target, mode, np.shape(A)[1])
 
 
 def conv_fwd(d, x, w, relu=False, mode=PSR, target=7):
-    return finish(conv_fwd_raw(d, x, w), relu, target, mode)
+    return finish(conv_fwd_raw(d, x, w), relu, target, mode, d.c * d.r * d.s)
 
 
 def conv_bwd_data(d, dy, w, mode=PSR, relu_src=None, target=7):
     """Error back-propagation step; the optional ReLU mask (reading R5) is
     applied to the rounded int8 error and does not move its exponent."""
-    out, acc, st = finish(conv_bwd_data_raw(d, dy, w), False, target, mode)
+    out, acc, st = finish(conv_bwd_data_raw(d, dy, w), False, target, mode, d.k * d.r * d.s)
     if relu_src is not None:
         relu_mask(out, relu_src)
     return out, acc, st
@@ -297,10 +300,11 @@ def sgd_update(w, g32, mu: int = 5, mode: int = PSR):
 def conv_bwd_weight(d, x, dy, w, mu: int = 5, mode: int = PSR):
     """Weight gradient + discrete update.  Returns (new w, g32, stats)."""
     S = conv_bwd_weight_raw(d, x, dy)
+    P, Q = conv_out_hw(d)
     fl = np.zeros(1, np.int32)
     g32 = wrap32(S, fl)
     w2, st = sgd_update(w, g32, mu, mode)
-    st["flags"] |= int(fl[0])
+    st["flags"] |= int(fl[0]) | (FLAG_ACC_BOUND if d.n * P * Q >= ACC_BOUND_LEN else 0)
     return w2, g32, st
 
 
@@ -308,24 +312,35 @@ def wrap32(S, flags_out=None):
     """int64 exact sums -> int32 two's complement accumulators."""
     S = np.asarray(S, np.int64)
     if flags_out is not None and S.size and (S.max() >= 2 ** 31 or S.min() < -2 ** 31):
-        flags_out[0] |= FLAG_ACC_BOUND
+        flags_out[0] |= FLAG_ACC_WRAP
     return S.astype(np.uint64).astype(np.uint32).view(np.int32).reshape(S.shape)
 
 
 def int_ce_loss_grad(logits, s_a: int, labels, mode: int = PSR):
     """Integer cross-entropy gradient (Section 3.5).
 
-    Returns (int8 err [B x N], int64 pre-rounding e32, stats dict)."""
+    Returns (int8 err [B x N], pre-rounding values, stats dict).  The
+    pre-rounding values are an int64 array when they all fit 64 bits, else an
+    object array of Python integers (the Taylor branch below s_a = -22)."""
     logits, pl = _c(logits, np.int8)
     labels, plab = _c(labels, np.int32)
     B, N = logits.shape
     assert labels.shape == (B,) and (labels >= 0).all() and (labels < N).all()
     err = np.empty((B, N), np.int8)
-    e32 = np.empty((B, N), np.int64)
+    hi = np.empty((B, N), np.int64)
+    lo = np.empty((B, N), np.uint64)
     st = Stats()
     _load().orc_int_ce_loss_grad(pl, int(s_a), plab, B, N, int(mode), _ptr(err),
-                                 _ptr(e32), ctypes.byref(st))
-    return err, e32, st.as_dict()
+                                 _ptr(hi), _ptr(lo), ctypes.byref(st))
+    lo_signed = lo.view(np.int64)
+    fits = ((hi == 0) & (lo_signed >= 0)) | ((hi == -1) & (lo_signed < 0))
+    if fits.all():
+        e = lo_signed.copy()
+    else:
+        e = np.empty((B, N), dtype=object)
+        for idx in np.ndindex(B, N):
+            e[idx] = (int(hi[idx]) << 64) + int(lo[idx])
+    return err, e, st.as_dict()
 
 
 def relu_mask(e, a):

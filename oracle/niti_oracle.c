@@ -11,7 +11,9 @@
  * Conventions
  *   - Every contraction is summed exactly in int64, then reduced to the
  *     int32 accumulator the method stores (two's complement, mod 2^32).
- *     A sum whose magnitude reaches 2^31 raises ORC_FLAG_ACC_BOUND.
+ *     ORC_FLAG_ACC_BOUND marks a reduction of 2^17 or more products (only
+ *     then can int8 products, each at most 2^14 in magnitude, leave the int32
+ *     range); ORC_FLAG_ACC_WRAP marks a sum that actually left it.
  *   - Tensors are NCHW (activations, errors) and KCRS (weights), the
  *     convention the method's layer equations are usually written in.
  *   - No blocking, fusion or reordering beyond the definitions.  The outer
@@ -30,17 +32,23 @@
  *   R7 the loss constant is 47274 (the decimal value printed; the hex
  *      spelling next to it is 47272).
  *   R8 xhat is an arithmetic (flooring) shift by 15 - s_a.
- *   R9 the Taylor branch of the loss is formed exactly in int64 at the
- *      smallest scale that makes every term an integer, 2^(1-2 s_a); below
- *      s_a = -22 that no longer fits, and s_a is held at -22 with a flag.
+ *   R9 the Taylor branch of the loss is formed exactly, in 128-bit
+ *      integers, at the smallest scale that makes every term an integer,
+ *      2^(1-2 s_a).  That holds every value for s_a >= -54.  Below -54 the
+ *      rounded int8 error no longer depends on s_a (the three terms sit in
+ *      disjoint bit ranges far from the binary point), so the oracle
+ *      evaluates s_a = -54 there and raises a flag; a test compares that
+ *      with the literal formula in unbounded integers.
  */
 #include <stdint.h>
 #include <string.h>
 #include <stdlib.h>
 
-#define ORC_FLAG_ACC_BOUND 1   /* an exact sum left the int32 range      */
+#define ORC_FLAG_ACC_BOUND 1   /* reduction length >= 2^17: sums may wrap */
 #define ORC_FLAG_EXP_RANGE 2   /* an int8 block exponent left [-128,127] */
-#define ORC_FLAG_LOSS_SA   4   /* loss s_a below the int64 Taylor range  */
+#define ORC_FLAG_LOSS_SA   4   /* loss s_a below -54: evaluated at -54   */
+#define ORC_FLAG_ACC_WRAP  16  /* an exact sum left the int32 range      */
+#define ORC_ACC_BOUND_LEN ((int64_t)1 << 17)
 
 typedef struct orc_stats {
     uint64_t max_abs; /* max magnitude over the whole tensor            */
@@ -131,7 +139,7 @@ static int64_t round_one(int64_t v, int bp, int mode)
 static int32_t wrap32(int64_t s, int32_t *flags)
 {
     if (s >= ((int64_t)1 << 31) || s < -((int64_t)1 << 31))
-        *flags |= ORC_FLAG_ACC_BOUND;
+        *flags |= ORC_FLAG_ACC_WRAP;
     return (int32_t)(uint32_t)(uint64_t)s;
 }
 
@@ -386,13 +394,14 @@ int64_t orc_conv_fwd_one(const orc_conv *d, const int8_t *x, const int8_t *w,
 /* ------------------------------------------------------------------ */
 /* Composite steps, each the method's sequence for one layer.           */
 
-/* Exact sums -> int32 accumulators (flagging the bound) -> optional ReLU
+/* Exact sums -> int32 accumulators (flagging wrapped sums) -> optional ReLU
  * (reading R5) -> block exponent -> rounding with target bits.  `acc32`
- * receives the int32 accumulators (after ReLU) when non-NULL. */
+ * receives the int32 accumulators (after ReLU) when non-NULL; red_len is the
+ * number of products in each sum (for ORC_FLAG_ACC_BOUND). */
 void orc_finish_i64(const int64_t *S, int64_t n, int relu, int target, int mode,
-                    int8_t *out, int32_t *acc32, orc_stats *st)
+                    int8_t *out, int32_t *acc32, orc_stats *st, int64_t red_len)
 {
-    int32_t flags = 0;
+    int32_t flags = red_len >= ORC_ACC_BOUND_LEN ? ORC_FLAG_ACC_BOUND : 0;
     int32_t *a = acc32 ? acc32 : (int32_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     int64_t i;
     for (i = 0; i < n; i++) {
@@ -441,6 +450,12 @@ void orc_sgd_update(int8_t *w, const int32_t *g32, int64_t n, int mu, int mode,
  *   `e32` receives the pre-rounding values when non-NULL. */
 int orc_loss_t_case(int s_a) { return s_a <= -7 ? 1 : 2; }
 
+#define ORC_LOSS_MIN_SA  (-54)  /* lowest s_a evaluated (reading R9)              */
+#define ORC_LOSS_WIDE_SA (-22)  /* below it the largest value may exceed 2^63   */
+
+typedef __int128 i128;
+typedef unsigned __int128 u128;
+
 static int64_t loss_xhat(int64_t a, int s_a)
 {
     int64_t prod = 47274 * a;
@@ -453,51 +468,117 @@ static int64_t loss_xhat(int64_t a, int s_a)
     return prod * 2;
 }
 
+static u128 mag128(i128 v)
+{
+    return v < 0 ? (u128)0 - (u128)v : (u128)v;
+}
+
+static int bitlen128(u128 m)
+{
+    int b = 0;
+    while (m) {
+        b++;
+        m >>= 1;
+    }
+    return b;
+}
+
+/* Algorithm 3 (or nearest) on a 128-bit value, the same steps as orc_psr. */
+static int8_t round128(i128 v, int bp, int mode)
+{
+    u128 x = mag128(v), q, f, thi, rlo;
+    int nb, h;
+    if (bp <= 0) {
+        q = x;
+    } else if (mode == 1) {
+        q = (x >> bp) + ((x >> (bp - 1)) & 1);
+    } else {
+        q = x >> bp;
+        f = x & ((((u128)1) << bp) - 1);
+        nb = bp;
+        if (nb & 1) {
+            f >>= 1;
+            nb -= 1;
+        }
+        h = nb / 2;
+        thi = f >> h;
+        rlo = f & ((((u128)1) << h) - 1);
+        if (thi > rlo)
+            q += 1;
+    }
+    if (q > 127)
+        q = 127;
+    return (int8_t)(v < 0 ? -(int)q : (int)q);
+}
+
+/* e_hi / e_lo (each may be NULL) receive the pre-rounding values as 128-bit
+ * two's complement (high signed half, low unsigned half).  Statistics: b and
+ * bp of the evaluated values; max_abs is their maximum, shifted right by
+ * 2 (-22 - s_a) bits when s_a < -22 (it would not fit 64 bits otherwise). */
 void orc_int_ce_loss_grad(const int8_t *logits, int s_a, const int32_t *labels,
                           int64_t B, int64_t N, int mode, int8_t *err,
-                          int64_t *e32, orc_stats *st)
+                          int64_t *e_hi, uint64_t *e_lo, orc_stats *st)
 {
-    int64_t *e = e32 ? e32 : (int64_t *)malloc((size_t)(B * N > 0 ? B * N : 1) * sizeof(int64_t));
+    i128 *e = (i128 *)malloc((size_t)(B * N > 0 ? B * N : 1) * sizeof(i128));
     int32_t flags = 0;
     int64_t bi, i;
-    if (s_a <= -7 && s_a < -22) {
+    u128 mx = 0;
+    int b, bp, sh;
+    if (s_a < ORC_LOSS_MIN_SA) {
         flags |= ORC_FLAG_LOSS_SA;
-        s_a = -22;
+        s_a = ORC_LOSS_MIN_SA;
     }
     for (bi = 0; bi < B; bi++) {
         const int8_t *a = logits + bi * N;
-        int64_t *ev = e + bi * N;
-        int64_t C = 0;
+        i128 *ev = e + bi * N;
+        i128 C = 0;
         if (s_a <= -7) {
             const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
             for (i = 0; i < N; i++) {
-                const int64_t ai = a[i];
-                ev[i] = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
+                const i128 ai = a[i];
+                ev[i] = ((i128)1 << e1) + ai * ((i128)1 << e2) + ai * ai;
             }
         } else {
-            int64_t mx = 0, p;
+            int64_t xmax = 0, p;
             for (i = 0; i < N; i++) {
                 const int64_t xh = loss_xhat(a[i], s_a);
-                if (i == 0 || xh > mx)
-                    mx = xh;
+                if (i == 0 || xh > xmax)
+                    xmax = xh;
             }
-            p = mx - 10;
+            p = xmax - 10;
             for (i = 0; i < N; i++) {
                 int64_t xt = loss_xhat(a[i], s_a) - p;
                 if (xt < 0)
                     xt = 0;
-                ev[i] = (int64_t)1 << xt;
+                ev[i] = (i128)1 << xt;
             }
         }
         for (i = 0; i < N; i++)
             C += ev[i];
         ev[labels[bi]] -= C;
     }
-    orc_shift_round_i64(e, B * N, 7, mode, err, st);
-    if (st)
-        st->flags |= flags;
-    if (!e32)
-        free(e);
+    /* Algorithms 1 and 2 over the whole [B][N] tensor, target 7. */
+    for (i = 0; i < B * N; i++)
+        if (mag128(e[i]) > mx)
+            mx = mag128(e[i]);
+    b = bitlen128(mx);
+    bp = b - 7 > 0 ? b - 7 : 0;
+    for (i = 0; i < B * N; i++)
+        err[i] = round128(e[i], bp, mode);
+    sh = s_a < ORC_LOSS_WIDE_SA ? 2 * (ORC_LOSS_WIDE_SA - s_a) : 0;
+    if (st) {
+        st->max_abs = (uint64_t)(mx >> sh);
+        st->b = b;
+        st->bp = bp;
+        st->flags = flags;
+    }
+    for (i = 0; i < B * N; i++) {
+        if (e_hi)
+            e_hi[i] = (int64_t)(e[i] >> 64);
+        if (e_lo)
+            e_lo[i] = (uint64_t)(u128)e[i];
+    }
+    free(e);
 }
 
 /* ------------------------------------------------------------------ */

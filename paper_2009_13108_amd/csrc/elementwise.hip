@@ -300,7 +300,24 @@ __global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict_
 
 // ---------------------------------------------------------------------------
 // Integer cross-entropy gradient, one wave per sample (Section 3.5).
-constexpr int kLossMinSa = -22;
+//
+// The Taylor branch (s_a <= -7) is exact: t_i = 2^(1-2 s_a) + a_i 2^(1-s_a) +
+// a_i^2 in 128-bit integers, which holds every value (row sums included) for
+// s_a >= -54.  Below -54 the rounded int8 error does not depend on s_a any
+// more (the three terms sit in disjoint bit ranges far from the binary
+// point), so s_a = -54 is evaluated and NITI_FLAG_LOSS_SA is raised.  Values
+// go to the workspace as 128-bit integers.  Below s_a = -22 the largest value
+// can exceed 64 bits, so the block maximum is folded in shifted right by
+// kLossShift(s_a) = 2 (-22 - s_a) bits (exact for the effective bitwidth:
+// every nonzero row has a value of at least 2^(-2 s_a) > 2^shift).
+constexpr int kLossMinSa = -54;
+constexpr int kLossWideSa = -22;
+
+typedef __int128 i128;
+typedef unsigned __int128 u128;
+
+__device__ __forceinline__ int loss_eval_sa(int s_a) { return s_a < kLossMinSa ? kLossMinSa : s_a; }
+__device__ __forceinline__ int loss_max_shift(int s_a) { return s_a < kLossWideSa ? 2 * (kLossWideSa - s_a) : 0; }
 
 __device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
     const int64_t prod = 47274 * a;
@@ -311,32 +328,51 @@ __device__ __forceinline__ int64_t loss_xhat(int64_t a, int s_a) {
     return prod * 2;
 }
 
+__device__ __forceinline__ u128 mag128(i128 v) { return v < 0 ? (u128)0 - (u128)v : (u128)v; }
+
+__device__ __forceinline__ i128 wave_sum_i128(i128 v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t lo = (uint64_t)(u128)v, hi = (uint64_t)((u128)v >> 64);
+        const uint64_t lo2 = __shfl_xor(lo, o, kWave), hi2 = __shfl_xor(hi, o, kWave);
+        v += (i128)(((u128)hi2 << 64) | (u128)lo2);
+    }
+    return v;
+}
+
+// One term t_i of a row (Section 3.5); p is the row's offset (base-2 branch).
+__device__ __forceinline__ i128 loss_term(int a, int s_a, int64_t p) {
+    if (s_a <= -7) {
+        const i128 ai = a;
+        return ((i128)1 << (1 - 2 * s_a)) + (ai << (1 - s_a)) + ai * ai;
+    }
+    int64_t xt = loss_xhat(a, s_a) - p;
+    xt = xt < 0 ? 0 : xt;
+    return (i128)((int64_t)1 << xt);
+}
+
 // One wave per sample.  NPL > 0: every lane keeps its NPL entries (lane,
-// lane + 64, ...) in registers, so the logits are read once and e64 is only
-// written (classes <= 64 * NPL); NPL == 0 streams any number of classes
-// through e64.
+// lane + 64, ...) in registers, so the logits are read once and e128 is
+// only written (classes <= 64 * NPL); NPL == 0 streams any number of classes
+// through e128.
 template <int NPL>
 __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __restrict__ s_logits,
-                            const int32_t* __restrict__ labels, int64_t* __restrict__ e64, int64_t batch,
+                            const int32_t* __restrict__ labels, i128* __restrict__ e128, int64_t batch,
                             int64_t classes, niti_stats* st) {
     const int slot = call_slot(st);
     const uint64_t snap = max_snapshot(st, slot);
     begin_call(st, slot, -1);
     const int lane = threadIdx.x & 63;
     const int64_t sample = (int64_t)blockIdx.x * (blockDim.x / 64) + (threadIdx.x >> 6);
-    int s_a = (int)*s_logits;
-    bool flag_sa = false;
-    if (s_a < kLossMinSa) {
-        flag_sa = true;
-        s_a = kLossMinSa;
-    }
+    const int s_in = (int)*s_logits;
+    const int s_a = loss_eval_sa(s_in);
+    const int msh = loss_max_shift(s_a);
     uint64_t m = 0;
     if (sample < batch) {
         const int8_t* a = logits + sample * classes;
-        int64_t* e = e64 + sample * classes;
+        i128* e = e128 + sample * classes;
         const int32_t y = labels[sample];
         const bool taylor = s_a <= -7;
-        const int e1 = 1 - 2 * s_a, e2 = 1 - s_a;
         if constexpr (NPL > 0) {
             // All NPL loads in flight at once: entries past the row read its
             // last entry (in bounds, unconditional) and are zeroed after.
@@ -346,16 +382,8 @@ __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __r
 #pragma unroll
             for (int j = 0; j < NPL; j++)
                 if (lane + 64 * j >= classes) av[j] = 0;
-            int64_t t[NPL];
-            int64_t C = 0;
-            if (taylor) {
-#pragma unroll
-                for (int j = 0; j < NPL; j++) {
-                    const int64_t ai = av[j];
-                    t[j] = lane + 64 * j < classes ? ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai : 0;
-                    C += t[j];
-                }
-            } else {
+            int64_t p = 0;
+            if (!taylor) {
                 int64_t mx = INT64_MIN;
 #pragma unroll
                 for (int j = 0; j < NPL; j++)
@@ -363,16 +391,16 @@ __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __r
                         const int64_t xh = loss_xhat(av[j], s_a);
                         mx = xh > mx ? xh : mx;
                     }
-                const int64_t p = wave_max_i64(mx) - 10;
-#pragma unroll
-                for (int j = 0; j < NPL; j++) {
-                    int64_t xt = loss_xhat(av[j], s_a) - p;
-                    xt = xt < 0 ? 0 : xt;
-                    t[j] = lane + 64 * j < classes ? (int64_t)1 << xt : 0;
-                    C += t[j];
-                }
+                p = wave_max_i64(mx) - 10;
             }
-            C = wave_sum_i64(C);
+            i128 t[NPL];
+            i128 C = 0;
+#pragma unroll
+            for (int j = 0; j < NPL; j++) {
+                t[j] = lane + 64 * j < classes ? loss_term(av[j], s_a, p) : (i128)0;
+                C += t[j];
+            }
+            C = wave_sum_i128(C);
             // The owner of the label's entry subtracts C (a label outside
             // [0, classes) contributes no term).
             const bool own = y >= 0 && y < classes && (y & 63) == lane;
@@ -382,68 +410,78 @@ __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __r
                 if (own && (y >> 6) == j) t[j] -= C;
                 if (i < classes) {
                     e[i] = t[j];
-                    const uint64_t mg = t[j] < 0 ? 0ull - (uint64_t)t[j] : (uint64_t)t[j];
+                    const uint64_t mg = (uint64_t)(mag128(t[j]) >> msh);
                     m = mg > m ? mg : m;
                 }
             }
         } else {
-            int64_t C = 0;
-            if (taylor) {
-                for (int64_t i = lane; i < classes; i += 64) {
-                    const int64_t ai = a[i];
-                    const int64_t t = ((int64_t)1 << e1) + ai * ((int64_t)1 << e2) + ai * ai;
-                    e[i] = t;
-                    C += t;
-                }
-            } else {
+            int64_t p = 0;
+            if (!taylor) {
                 int64_t mx = INT64_MIN;
                 for (int64_t i = lane; i < classes; i += 64) {
                     const int64_t xh = loss_xhat(a[i], s_a);
                     mx = xh > mx ? xh : mx;
                 }
-                mx = wave_max_i64(mx);
-                const int64_t p = mx - 10;
-                for (int64_t i = lane; i < classes; i += 64) {
-                    int64_t xt = loss_xhat(a[i], s_a) - p;
-                    xt = xt < 0 ? 0 : xt;
-                    const int64_t t = (int64_t)1 << xt;
-                    e[i] = t;
-                    C += t;
-                }
+                p = wave_max_i64(mx) - 10;
             }
-            C = wave_sum_i64(C);
+            i128 C = 0;
+            for (int64_t i = lane; i < classes; i += 64) {
+                const i128 t = loss_term(a[i], s_a, p);
+                e[i] = t;
+                C += t;
+            }
+            C = wave_sum_i128(C);
             // Lane i owns entries i, i+64, ...; the owner of the label's entry
             // subtracts C (a label outside [0, classes) contributes no term).
             if (y >= 0 && y < classes && (y & 63) == lane) e[y] -= C;
             for (int64_t i = lane; i < classes; i += 64) {
-                const int64_t v = e[i];
-                const uint64_t mg = v < 0 ? 0ull - (uint64_t)v : (uint64_t)v;
+                const uint64_t mg = (uint64_t)(mag128(e[i]) >> msh);
                 m = mg > m ? mg : m;
             }
         }
     }
-    if (flag_sa && threadIdx.x == 0 && blockIdx.x == 0)
+    if (s_in < kLossMinSa && threadIdx.x == 0 && blockIdx.x == 0)
         atomicOr(&st->wflags[slot], NITI_FLAG_LOSS_SA);
     block_publish_max(st, slot, m, snap);
 }
 
-// Rounds e64 with the call's block binary point (finishing launch); each
+// Algorithm 3 (or nearest) on a 128-bit value with binary point bp <= 126.
+__device__ __forceinline__ int8_t round_i128(i128 v, int bp, int rtn) {
+    const u128 x = mag128(v);
+    u128 q = x >> bp;
+    if (bp > 0) {
+        if (rtn) {
+            q += (x >> (bp - 1)) & 1u;
+        } else {
+            const int odd = bp & 1, h = (bp - odd) >> 1;
+            const u128 f = (x & (((u128)1 << bp) - 1)) >> odd;
+            q += (f >> h) > (f & (((u128)1 << h) - 1)) ? 1u : 0u;
+        }
+    }
+    const int qi = q < 127 ? (int)q : 127;
+    return (int8_t)(v < 0 ? -qi : qi);
+}
+
+// Rounds e128 with the call's block binary point (finishing launch); each
 // thread issues its LR loads before any store.
 constexpr int LR = 4;
-__global__ void loss_round_kernel(const int64_t* __restrict__ e64, int8_t* __restrict__ err, int64_t n, int mode,
-                                  niti_stats* st) {
-    const int bp = block_bp(load_cur_acc(st), 7);
-    const RoundK rk = make_round(bp, mode);
+__global__ void loss_round_kernel(const i128* __restrict__ e128, int8_t* __restrict__ err, int64_t n, int mode,
+                                  const int8_t* __restrict__ s_logits, niti_stats* st) {
+    const int msh = loss_max_shift(loss_eval_sa((int)*s_logits));
+    const uint64_t mx = load_cur_acc(st);
+    const int b = mx ? bitlen64(mx) + msh : 0;
+    const int bp = b > 7 ? b - 7 : 0;
+    const int rtn = mode == NITI_ROUND_RTN;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += LR * stride) {
-        int64_t v[LR];
+        i128 v[LR];
 #pragma unroll
-        for (int j = 0; j < LR; j++) v[j] = i0 + j * stride < n ? e64[i0 + j * stride] : 0;
+        for (int j = 0; j < LR; j++) v[j] = i0 + j * stride < n ? e128[i0 + j * stride] : (i128)0;
 #pragma unroll
         for (int j = 0; j < LR; j++)
-            if (i0 + j * stride < n) err[i0 + j * stride] = round_i64(v[j], rk);
+            if (i0 + j * stride < n) err[i0 + j * stride] = round_i128(v[j], bp, rtn);
     }
-    if (is_finisher()) finish_call(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0);
+    if (is_finisher()) finish_call(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0, msh);
 }
 
 // ---------------------------------------------------------------------------
@@ -727,22 +765,22 @@ hipError_t update_run(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode
 }
 
 hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t* labels, int8_t* err,
-                    int64_t* e64, int64_t batch, int64_t classes, int mode, niti_stats* st,
-                    hipStream_t s) {
+                    void* ws, int64_t batch, int64_t classes, int mode, niti_stats* st, hipStream_t s) {
+    i128* e128 = (i128*)ws;
     const int per_block = kThreads / 64;
     const int64_t blocks = (batch + per_block - 1) / per_block;
     const dim3 grid((unsigned)(blocks > 0 ? blocks : 1));
     if (classes <= 64 * 16)
-        hipLaunchKernelGGL(loss_kernel<16>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e64, batch,
+        hipLaunchKernelGGL(loss_kernel<16>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e128, batch,
                            classes, st);
     else
-        hipLaunchKernelGGL(loss_kernel<0>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e64, batch,
+        hipLaunchKernelGGL(loss_kernel<0>, grid, dim3(kThreads), 0, s, logits, s_logits, labels, e128, batch,
                            classes, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = batch * classes;
-    hipLaunchKernelGGL(loss_round_kernel, dim3(grid_for(n, LR)), dim3(kThreads), 0, s, e64, err, n, mode,
-                       st);
+    hipLaunchKernelGGL(loss_round_kernel, dim3(grid_for(n, LR)), dim3(kThreads), 0, s, e128, err, n, mode,
+                       s_logits, st);
     return hipGetLastError();
 }
 

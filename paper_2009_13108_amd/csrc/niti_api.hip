@@ -19,7 +19,9 @@ using namespace niti;
 namespace {
 
 constexpr int64_t kMaxBytes = (int64_t)1 << 31;  // 32-bit offsets inside kernels
-constexpr int64_t kAccLimit = (int64_t)1 << 31;
+// Reductions of at least this many int8 products may leave the int32 range
+// (each product is at most 2^14 in magnitude); shorter ones cannot.
+constexpr int64_t kAccBoundLen = (int64_t)1 << 17;
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
@@ -31,9 +33,7 @@ inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
 
 inline niti_status hip_status(hipError_t e) { return e == hipSuccess ? NITI_OK : NITI_ERR_HIP; }
 
-inline uint32_t acc_flags(int64_t red_len) {
-    return (red_len * 127 * 127 >= kAccLimit) ? NITI_FLAG_ACC_BOUND : 0u;
-}
+inline uint32_t acc_flags(int64_t red_len) { return red_len >= kAccBoundLen ? NITI_FLAG_ACC_BOUND : 0u; }
 
 bool valid_mode(niti_round_mode m) { return m == NITI_ROUND_PSR || m == NITI_ROUND_RTN; }
 
@@ -190,7 +190,7 @@ size_t niti_workspace_bytes(int op, const niti_conv_desc* d, int64_t M, int64_t 
                             (w.win ? w.wp.xpad_bytes : 0));
         }
         case NITI_OP_INT_CE_LOSS:
-            return (M > 0 && N > 0) ? (size_t)round_up(M * N * 8, 256) : 0;
+            return (M > 0 && N > 0) ? (size_t)round_up(M * N * 16, 256) : 0;
         default:
             return 0;
     }
@@ -619,11 +619,10 @@ niti_status niti_int_ce_loss_grad(const int8_t* logits, const int8_t* s_logits, 
     if (mis16(logits) || mis16(labels) || mis16(err) || mis16(ws)) return NITI_ERR_ARG;
     if (batch < 1 || classes < 1) return NITI_ERR_SHAPE;
     if (classes > 65536 || !valid_mode(mode)) return NITI_ERR_ARG;
-    if (too_big(batch * classes * 8)) return NITI_ERR_UNSUPPORTED;
+    if (too_big(batch * classes * 16)) return NITI_ERR_UNSUPPORTED;
     const size_t need = niti_workspace_bytes(NITI_OP_INT_CE_LOSS, nullptr, batch, classes, 0);
     if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
-    return hip_status(loss_run(logits, s_logits, labels, err, (int64_t*)ws, batch, classes, mode, stats,
-                               as_stream(stream)));
+    return hip_status(loss_run(logits, s_logits, labels, err, ws, batch, classes, mode, stats, as_stream(stream)));
 }
 
 niti_status niti_sgd_update(int8_t* w, const int32_t* g32, int64_t n, int mu, niti_round_mode mode,

@@ -314,8 +314,10 @@ struct ExpArgs {
 // the statistics, make bp the next call's first guess, clear the other
 // slot and count the call.
 // Every value it reads is loaded before any is used (one memory round trip).
+// max_shift: the maximum was folded in shifted right by that many bits (its
+// effective bitwidth is then bitlen + max_shift; see the integer loss).
 __device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint32_t static_flags,
-                                   int hinted) {
+                                   int hinted, int max_shift = 0) {
     const uint64_t a0 = load_acc(st, 0), a1 = load_acc(st, 1);
     const uint32_t f0 = __hip_atomic_load(&st->wflags[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t f1 = __hip_atomic_load(&st->wflags[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -326,8 +328,8 @@ __device__ inline void finish_call(niti_stats* st, int target, ExpArgs ex, uint3
     const int sb = ex.s_out && ex.s_b ? (int)*ex.s_b : 0;
     const uint64_t mx = cur ? a1 : a0;
     const uint32_t wf = cur ? f1 : f0;
-    const int b = bitlen64(mx);
-    const int bp = block_bp(mx, target);
+    const int b = mx ? bitlen64(mx) + max_shift : 0;
+    const int bp = b > target ? b - target : 0;
     uint32_t fl = wf | static_flags;
     if (hinted && bp != hint_used) {
         fl |= NITI_FLAG_HINT_MISS;

@@ -137,8 +137,9 @@ hipError_t reduce_max_run(const int32_t* part, int splits, int32_t* g32, int64_t
                           hipStream_t s);
 hipError_t update_run(int8_t* w, const int32_t* g32, int64_t n, int mu, int mode, niti_stats* st,
                       uint32_t static_flags, hipStream_t s);
+// ws: 16 bytes per logit (the 128-bit pre-rounding values).
 hipError_t loss_run(const int8_t* logits, const int8_t* s_logits, const int32_t* labels,
-                    int8_t* err, int64_t* e64, int64_t batch, int64_t classes, int mode,
+                    int8_t* err, void* ws, int64_t batch, int64_t classes, int mode,
                     niti_stats* st, hipStream_t s);
 // Back-propagation filters: wc[class][c][t][u][k] = w[k][r(t)][s(u)][c].
 struct DgradClass {

@@ -41,5 +41,26 @@ def say(*args):
     sys.stdout.flush()
 
 
-def same_stats(gpu, orc, keys=("max_abs", "b", "bp")):
-    return all(int(gpu[k]) == int(orc[k]) for k in keys)
+FLAG_HINT_MISS = 8   # library only: the speculated shift was wrong (timing, not a result)
+FLAG_ACC_WRAP = 16   # oracle only: an exact sum actually left the int32 range
+FLAG_ACC_BOUND = 1   # both: reduction of 2^17 or more products
+
+
+def same_flags(gpu_flags, orc_flags):
+    """Library flags equal the oracle's except for the library's speculation
+    bit and the oracle's observed-wrap bit; every observed wrap lies under
+    the static accumulator bound the library reports."""
+    g, o = int(gpu_flags), int(orc_flags)
+    if o & FLAG_ACC_WRAP and not g & FLAG_ACC_BOUND:
+        return False
+    return (g & ~FLAG_HINT_MISS) == (o & ~FLAG_ACC_WRAP)
+
+
+def same_stats(gpu, orc, keys=("max_abs", "b", "bp", "flags")):
+    for k in keys:
+        if k == "flags":
+            if not same_flags(gpu[k], orc[k]):
+                return False
+        elif int(gpu[k]) != int(orc[k]):
+            return False
+    return True

@@ -177,10 +177,25 @@ def test_gemm_all_ones_and_overflow_flag():
     A = np.full((1, K), 127, np.int8)
     out, acc, st = oracle.gemm_fwd(A, A)
     assert acc[0, 0] == np.int32(np.uint32((K * 127 * 127) % (1 << 32)).view(np.int32))
-    assert st["flags"] & oracle.FLAG_ACC_BOUND
+    assert st["flags"] == oracle.FLAG_ACC_BOUND | oracle.FLAG_ACC_WRAP
+    # a long reduction that stays in range: the static bound only
+    _, acc, st = oracle.gemm_fwd(np.ones((1, K), np.int8), np.ones((1, K), np.int8))
+    assert acc[0, 0] == K and st["flags"] == oracle.FLAG_ACC_BOUND
     ones = np.ones((2, 100), np.int8)
     _, acc, st = oracle.gemm_fwd(ones, ones)
     assert (acc == 100).all() and st["flags"] == 0
+
+
+def test_accumulator_bound_covers_every_wrap():
+    """Below 2^17 products no int8 sum can leave the int32 range (each product
+    is at most 2^14 in magnitude: (-128)^2), at 2^17 one can."""
+    n = oracle.ACC_BOUND_LEN
+    assert (n - 1) * 128 * 128 < 2 ** 31 <= n * 128 * 128
+    A = np.full((1, n), -128, np.int8)
+    _, acc, st = oracle.gemm_fwd(A, A)
+    assert st["flags"] == oracle.FLAG_ACC_BOUND | oracle.FLAG_ACC_WRAP and acc[0, 0] == -2 ** 31
+    _, acc, st = oracle.gemm_fwd(A[:, 1:], A[:, 1:])
+    assert st["flags"] == 0 and acc[0, 0] == 2 ** 31 - 2 ** 14
 
 
 CONV_CASES = [
@@ -357,11 +372,77 @@ def test_loss_gradient_signs():
             assert err[b, labels[b]] <= 0 and (np.delete(err[b], labels[b]) >= 0).all()
 
 
-def test_loss_deep_taylor_is_flagged():
-    logits = I.weights(1, (2, 10)); labels = I.labels(2, 2, 10)
-    _, e32a, st = oracle.int_ce_loss_grad(logits, -40, labels)
-    _, e32b, _ = oracle.int_ce_loss_grad(logits, -22, labels)
-    assert st["flags"] & oracle.FLAG_LOSS_SA and (e32a == e32b).all()
+def _literal_loss(logits, s_a, labels, mode=oracle.PSR):
+    """Section 3.5 in unbounded Python integers (tests/alg1_bigint.py, which
+    shares nothing with the oracle): (err, pre-rounding values, max, bp)."""
+    import alg1_bigint as R
+    rows = []
+    for a, y in zip(logits.tolist(), labels.tolist()):
+        t = R.loss_terms(a, s_a)
+        c = sum(t)
+        t[y] -= c
+        rows.append(t)
+    flat = [v for r in rows for v in r]
+    err, bp = R.shift_and_round(flat, 7, R.PSR if mode == oracle.PSR else R.RTN)
+    return np.array(err, np.int8).reshape(logits.shape), rows, max(abs(v) for v in flat), bp
+
+
+def _loss_logits(kind, seed, B, N):
+    if kind == "uniform":
+        return I.weights(seed, (B, N))
+    if kind == "5bit":
+        return I.errors5(seed, (B, N))
+    lg = np.full((B, N), 127, np.int8)
+    if kind == "edge":
+        lg[:, ::3] = -127
+    elif kind == "min":
+        lg[:, ::2] = -128
+    return lg
+
+
+@pytest.mark.parametrize("s_a", [-7, -8, -15, -22, -23, -24, -31, -40, -54])
+@pytest.mark.parametrize("N,B,kind", [(1, 3, "uniform"), (2, 4, "uniform"), (10, 8, "uniform"),
+                                      (1000, 2, "edge"), (1000, 2, "5bit"), (4097, 1, "min")])
+def test_loss_taylor_exact_against_bigint(s_a, N, B, kind):
+    """The Taylor branch is evaluated exactly for -54 <= s_a <= -7: every
+    pre-rounding value, the block b and bp, and the int8 error equal the
+    literal formula in unbounded integers; max_abs is the maximum shifted
+    right by 2 (-22 - s_a) bits below s_a = -22."""
+    logits = _loss_logits(kind, 700 + N + B, B, N)
+    labels = I.labels(701 + N, B, N)
+    for mode in (oracle.PSR, oracle.RTN):
+        err, e, st = oracle.int_ce_loss_grad(logits, s_a, labels, mode=mode)
+        ref_err, rows, mx, bp = _literal_loss(logits, s_a, labels, mode)
+        assert [[int(v) for v in r] for r in e] == rows
+        assert st["flags"] == 0 and st["bp"] == bp and st["b"] == mx.bit_length()
+        assert st["max_abs"] == mx >> (2 * (-22 - s_a) if s_a < -22 else 0)
+        assert (err == ref_err).all()
+
+
+@pytest.mark.parametrize("s_a", [-55, -64, -100, -128])
+@pytest.mark.parametrize("N,B,kind", [(10, 8, "uniform"), (100, 4, "edge"), (1000, 2, "edge"),
+                                      (1000, 2, "5bit"), (4097, 1, "min")])
+def test_loss_below_hold_equals_literal(s_a, N, B, kind):
+    """Below s_a = -54 the oracle evaluates s_a = -54 and flags it; its int8
+    error equals the literal formula at the true s_a (the rounded result no
+    longer depends on s_a there)."""
+    logits = _loss_logits(kind, 900 + N + B, B, N)
+    labels = I.labels(901 + N, B, N)
+    err, _, st = oracle.int_ce_loss_grad(logits, s_a, labels)
+    ref_err, _, _, _ = _literal_loss(logits, s_a, labels)
+    assert st["flags"] & oracle.FLAG_LOSS_SA
+    assert (err == ref_err).all()
+
+
+def test_loss_hold_at_22_would_be_wrong():
+    """The reason the Taylor branch is wide: s_a = -23 gives a different
+    int8 error than s_a = -22 for a 1000-class row of extreme logits."""
+    logits = _loss_logits("edge", 1000 + 4 + 2, 4, 1000)
+    labels = I.labels(1000 + 4, 4, 1000)
+    e22, _, _ = oracle.int_ce_loss_grad(logits, -22, labels)
+    e23, _, _ = oracle.int_ce_loss_grad(logits, -23, labels)
+    ref23, _, _, _ = _literal_loss(logits, -23, labels)
+    assert (e23 == ref23).all() and not (e23 == e22).all()
 
 
 def test_loss_constant_is_log2e():
