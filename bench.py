@@ -14,9 +14,16 @@ resident in device memory before timing starts.
 
 Printed: one JSON line.  value = algorithmic int8 tera-operations per second
 of the whole step (2 ops per multiply-accumulate of each contraction,
-counted on the unpadded channel count); roofline = the dominant kernel
-family timed live with HIP events on its stream; cpu_baseline = the CPU
-oracle on a bounded sample of the same layer set.
+counted on the unpadded channel count); roofline = the contraction kernel
+with the most time in the step, timed live with HIP events on its launch
+stream; c4_layers = every layer's forward, back-propagation and weight
+gradient + update against its own bound (int8 MFMA or HBM); passes = the
+split-sum, update and loss passes in GB/s; c1-c3 = the other training
+workloads (fully-connected layer, MLP, VGG-style CNN) in microseconds per
+step; c5 = the fused GEMM + exponent + rounding sweep over M, N, K in
+{4096, 8192, 16384}; table7_context = the paper's GPU conv shapes, with its
+RTX 3090 figures beside them; cpu_baseline = the CPU oracle on a bounded
+sample of the layer set.
 """
 from __future__ import annotations
 
@@ -275,36 +282,65 @@ class ResNetStep:
             else:
                 op[1].wait_event(op[2])
 
-    def step_serial(self):
-        """The same calls, all on the current stream, one after another (for
-        per-call kernel durations without overlap)."""
+    def serial_plan(self):
+        """The step's calls one after another on the current stream, as a
+        list of (layer, pass, ops, algorithmic bytes, call); contraction calls
+        launch exactly one main kernel each (pass fwd / dgrad / wgrad), the
+        loss none.  Algorithmic bytes: int8 operands read once and the int8
+        output written once (+ the ReLU source read by the back-propagation;
+        the weight read and written by the update)."""
         niti = self.niti
         Bsz = self.batch
         fin, fout = self.fc_desc.c, self.fc_desc.k
         s = self.fc_stats
         fd = self.fc_desc
+        plan = []
         for L in self.layers:
+            d = L["desc"]
+            xb, yb = d.n * d.h * d.w * d.c, d.n * d.p * d.q * d.k
+            wb = d.k * d.r * d.s * d.c
             for c in range(L["count"]):
-                niti.conv_fwd(L["desc"], L["x"], L["w"][c], L["y"], self.stats, relu=True,
-                              stats_index=L["stats"] + 3 * c, ws=self.ws)
-        niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc, self.s_logits, 7, False,
-                      stats_index=s)
-        niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats, self.ws,
-                              stats_index=s + 1)
-        niti.conv_bwd_data(fd, self.err.view(Bsz, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
-                           self.dfeat.view(Bsz, 1, 1, fin), self.stats, self.ws,
-                           relu_src=self.feat.view(Bsz, 1, 1, fin), stats_index=s + 2)
-        niti.conv_bwd_weight(fd, self.feat.view(Bsz, 1, 1, fin), self.err.view(Bsz, 1, 1, fout),
-                             self.wfc.view(fout, 1, 1, fin), self.stats, self.ws, mu=self.mu, stats_index=s + 3)
+                plan.append((L["name"], "fwd", 2 * L["macs"], xb + wb + yb,
+                             lambda L=L, c=c: niti.conv_fwd(L["desc"], L["x"], L["w"][c], L["y"], self.stats,
+                                                            relu=True, stats_index=L["stats"] + 3 * c, ws=self.ws)))
+        plan.append(("fc", "fwd", 2 * self.fc_macs, Bsz * fin + fout * fin + Bsz * fout,
+                     lambda: niti.gemm_fwd(self.feat, self.wfc, self.logits, self.stats, self.s_feat, self.s_wfc,
+                                           self.s_logits, 7, False, stats_index=s)))
+        plan.append(("fc", "loss", 0, 2 * Bsz * fout,
+                     lambda: niti.int_ce_loss_grad(self.logits, self.s_logits, self.labels, self.err, self.stats,
+                                                   self.ws, stats_index=s + 1)))
+        plan.append(("fc", "dgrad", 2 * self.fc_macs, Bsz * fout + fout * fin + 2 * Bsz * fin,
+                     lambda: niti.conv_bwd_data(fd, self.err.view(Bsz, 1, 1, fout), self.wfc.view(fout, 1, 1, fin),
+                                                self.dfeat.view(Bsz, 1, 1, fin), self.stats, self.ws,
+                                                relu_src=self.feat.view(Bsz, 1, 1, fin), stats_index=s + 2)))
+        plan.append(("fc", "wgrad", 2 * self.fc_macs, Bsz * fin + Bsz * fout + 2 * fout * fin,
+                     lambda: niti.conv_bwd_weight(fd, self.feat.view(Bsz, 1, 1, fin), self.err.view(Bsz, 1, 1, fout),
+                                                  self.wfc.view(fout, 1, 1, fin), self.stats, self.ws, mu=self.mu,
+                                                  stats_index=s + 3)))
         for L in reversed(self.layers):
             d = L["desc"]
+            xb, yb = d.n * d.h * d.w * d.c, d.n * d.p * d.q * d.k
+            wb = d.k * d.r * d.s * d.c
             for c in reversed(range(L["count"])):
-                w = L["w"][c]
                 s0 = L["stats"] + 3 * c
                 if L["bwd_data"]:
-                    niti.conv_bwd_data(d, L["dy"], w, L["dx"], self.stats, self.ws, relu_src=L["x"],
-                                       stats_index=s0 + 1)
-                niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu, stats_index=s0 + 2)
+                    plan.append((L["name"], "dgrad", 2 * L["macs"], yb + wb + 2 * xb,
+                                 lambda L=L, c=c, s0=s0: niti.conv_bwd_data(L["desc"], L["dy"], L["w"][c], L["dx"],
+                                                                            self.stats, self.ws, relu_src=L["x"],
+                                                                            stats_index=s0 + 1)))
+                plan.append((L["name"], "wgrad", 2 * L["macs"], xb + yb + 2 * wb,
+                             lambda L=L, c=c, s0=s0: niti.conv_bwd_weight(L["desc"], L["x"], L["dy"], L["w"][c],
+                                                                          self.stats, self.ws, mu=self.mu,
+                                                                          stats_index=s0 + 2)))
+        return plan
+
+    def step_serial(self):
+        """The same calls, all on the current stream, one after another (for
+        per-call kernel durations without overlap)."""
+        if not hasattr(self, "_serial"):
+            self._serial = self.serial_plan()
+        for entry in self._serial:
+            entry[-1]()
 
     def misses(self):
         st = self.niti.read_stats(self.stats)
@@ -325,6 +361,253 @@ class ResNetStep:
             if m:
                 out["fc/%s" % name] = m
         return out
+
+
+# ----------------------------------------------------------------------------
+def _bound(ops, nbytes):
+    """The roofline bound of a pass: (name, microseconds at that bound)."""
+    t_mfma = ops / (PEAK_INT8_TOPS * 1e12) * 1e6
+    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9) * 1e6
+    return ("mfma", t_mfma) if t_mfma >= t_hbm else ("hbm", t_hbm)
+
+
+def _spin():
+    """Let the host queue run ahead of the GPU, so that no timing event
+    waits on the host."""
+    import torch
+    torch.cuda.synchronize()
+    try:
+        torch.cuda._sleep(int(0.05 * 2.4e9))
+    except Exception:
+        pass
+
+
+def measure_serial(job, steps):
+    """`steps` serial steps with the library's timing records on.  Records
+    come in enqueue order; every plan entry opens with one record of family
+    IGEMM (forward, back-propagation), WGRAD (weight gradient) or LOSS, and
+    the KERNEL / SUM / UPDATE records that follow belong to it."""
+    import collections
+    import torch
+    niti = job.niti
+    plan = job.serial_plan()
+    job._serial = plan
+    _spin()
+    niti.timing_enable(True)
+    for _ in range(steps):
+        job.step_serial()
+    niti.timing_enable(False)
+    torch.cuda.synchronize()
+    recs = niti.timing_records()
+    lead = {niti.TIMING_IGEMM, niti.TIMING_WGRAD, niti.TIMING_LOSS}
+    calls = []
+    for fam, name, ms in recs:
+        if fam in lead:
+            calls.append({"fam": fam, "ms": ms, "kernel": None, "kernel_ms": 0.0, "sum": None, "update_ms": 0.0})
+        elif fam == niti.TIMING_KERNEL:
+            calls[-1]["kernel"], calls[-1]["kernel_ms"] = name, ms
+        elif fam == niti.TIMING_SUM:
+            calls[-1]["sum"] = (name, ms)
+        elif fam == niti.TIMING_UPDATE:
+            calls[-1]["update_ms"] = ms
+    assert len(calls) == steps * len(plan), (len(calls), steps, len(plan))
+    kern = collections.OrderedDict()
+    fam = {"igemm": [0, 0.0, 0], "wgrad": [0, 0.0, 0]}
+    layer = collections.OrderedDict()
+    passes = {"split_sum": [0.0, 0, 0], "update": [0.0, 0, 0], "loss": [0.0, 0, 0]}
+    for i, c in enumerate(calls):
+        lname, pss, ops, nbytes, _ = plan[i % len(plan)]
+        if pss == "loss":
+            passes["loss"][0] += c["ms"]
+            passes["loss"][1] += 1
+            passes["loss"][2] += job.batch * job.fc_desc.k * (1 + 16 + 16 + 1) + 4 * job.batch
+            call_ms = c["ms"]
+        else:
+            k = kern.setdefault(c["kernel"], [0, 0.0, 0])
+            k[0] += 1
+            k[1] += c["kernel_ms"]
+            k[2] += ops
+            f = fam["wgrad" if pss == "wgrad" else "igemm"]
+            f[0] += 1
+            f[1] += c["ms"]
+            f[2] += ops
+            call_ms = c["ms"]
+            if pss == "wgrad":
+                d = job.fc_desc if lname == "fc" else [L for L in job.layers if L["name"] == lname][0]["desc"]
+                nw = d.k * d.r * d.s * d.c
+                sname, sms = c["sum"]
+                splits = int(sname.split("<")[1].rstrip(">"))
+                passes["split_sum"][0] += sms
+                passes["split_sum"][1] += 1
+                passes["split_sum"][2] += 4 * nw * splits + (4 * nw if splits > 1 else 0)
+                passes["update"][0] += c["update_ms"]
+                passes["update"][1] += 1
+                passes["update"][2] += 6 * nw
+                call_ms += sms + c["update_ms"]
+        e = layer.setdefault((lname, pss), [0, 0.0, ops, nbytes])
+        e[0] += 1
+        e[1] += call_ms
+    return {"kernels": kern, "families": fam, "layers": layer, "passes": passes}
+
+
+def c4_layer_table(ser):
+    out = []
+    for (lname, pss), (n, ms, ops, nbytes) in ser["layers"].items():
+        us = ms * 1e3 / n
+        bname, t_bound = _bound(ops, nbytes)
+        rec = {"layer": lname, "pass": pss, "us": round(us, 2), "bound": bname,
+               "frac_of_bound": round(t_bound / us, 4)}
+        if ops:
+            rec["tops"] = round(ops / (us * 1e-6) / 1e12, 1)
+        out.append(rec)
+    return out
+
+
+def c5_sweep(reps=5, sizes=(4096, 8192, 16384), dists=("u127", "u15")):
+    """The fused GEMM + block maximum + Algorithm 3 rounding (one
+    niti_gemm_fwd call: main kernel and finishing launch) on every (M, N, K)
+    in sizes^3, int8 operands U[-127,127] and U[-15,15].  A cold call (no
+    binary-point guess yet: the output is rounded twice) is timed apart from
+    the median of `reps` steady calls."""
+    import torch
+    from paper_2009_13108_amd import inputs as I
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    big = max(sizes)
+    out = []
+    C = torch.empty(big * big, dtype=torch.int8, device="cuda")
+    for di, dist in enumerate(dists):
+        gen = I.weights if dist == "u127" else I.errors5
+        A = gen(I.base_seed(5, 1 + 10 * di), (big * big,), device="cuda")
+        B = gen(I.base_seed(5, 2 + 10 * di), (big * big,), device="cuda")
+        for M in sizes:
+            for N in sizes:
+                for K in sizes:
+                    a, b, c = A[:M * K].view(M, K), B[:N * K].view(N, K), C[:M * N].view(M, N)
+                    stats = niti.new_stats()
+                    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * (reps + 1))]
+                    torch.cuda.synchronize()
+                    for r in range(reps + 1):
+                        ev[2 * r].record()
+                        niti.gemm_fwd(a, b, c, stats)
+                        ev[2 * r + 1].record()
+                    torch.cuda.synchronize()
+                    t = [ev[2 * r].elapsed_time(ev[2 * r + 1]) for r in range(reps + 1)]
+                    steady = sorted(t[1:])[reps // 2]
+                    tops = 2.0 * M * N * K / (steady * 1e-3) / 1e12
+                    st = niti.read_stats(stats)[0]
+                    out.append({"M": M, "N": N, "K": K, "dist": dist, "ms": round(steady, 4),
+                                "cold_ms": round(t[0], 4), "tops": round(tops, 1),
+                                "frac": round(tops / PEAK_INT8_TOPS, 4), "misses": st["misses"]})
+        del A, B
+    return out
+
+
+def _replay_time(calls, reps):
+    import torch
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    for _ in range(2):
+        niti.replay(calls)
+    _spin()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        niti.replay(calls)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def small_configs(reps=50):
+    """Configs 1-3 as whole steps, each step's library calls marshalled once
+    and replayed (so that the host does not pace the GPU).
+      c1: fully-connected 784->128, batch 32: forward, back-propagation of
+          5-bit errors, weight gradient + update;
+      c2: MLP 784-256-128-10, batch 256: input quantisation, forward, loss,
+          backward (Algorithm 1);
+      c3: VGG-style CNN on 32x32x3, batch 256, the same."""
+    import torch
+    from paper_2009_13108_amd import inputs as I
+    from paper_2009_13108_amd import model as M
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    res = {}
+    # c1
+    B, K, N = 32, 784, 128
+    x = I.activations(I.base_seed(1, 1), (B, K), device="cuda")
+    w = I.weights(I.base_seed(1, 2), (N, K), device="cuda")
+    e = I.errors5(I.base_seed(1, 3), (B, N), device="cuda")
+    gd = niti.ConvDesc.make(B, 1, 1, K, N, 1, 1, 1, 0)
+    stats = niti.new_stats(3)
+    y = torch.empty((B, N), dtype=torch.int8, device="cuda")
+    dx = torch.empty((B, 1, 1, K), dtype=torch.int8, device="cuda")
+    ws = niti.new_workspace(max(niti.workspace_bytes(niti.OP_CONV_BWD_DATA, gd),
+                                niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gd)))
+    s_x, s_w, s_y = (torch.tensor([v], dtype=torch.int8, device="cuda") for v in (-7, -7, 0))
+    with niti.recording() as calls:
+        niti.gemm_fwd(x, w, y, stats, s_x, s_w, s_y, stats_index=0)
+        niti.conv_bwd_data(gd, e.view(B, 1, 1, N), w.view(N, 1, 1, K), dx, stats, ws, stats_index=1)
+        niti.conv_bwd_weight(gd, x.view(B, 1, 1, K), e.view(B, 1, 1, N), w.view(N, 1, 1, K), stats, ws, mu=5,
+                             stats_index=2)
+    ms = _replay_time(calls, reps)
+    ops = 3 * 2 * B * K * N
+    res["c1"] = {"workload": "fc784x128_b32", "us_per_step": round(ms * 1e3, 2),
+                 "tops": round(ops / (ms * 1e-3) / 1e12, 3), "ops_per_step": ops}
+    # c2, c3
+    for key, specs, hwc, img_c, batch, cfg, name in (
+            ("c2", M.MLP_784, (28, 28, 1), 1, 256, 2, "mlp784_256_128_10_b256"),
+            ("c3", M.VGG_32, (32, 32, 4), 3, 256, 3, "vgg32_64_64_128_128_256_256_fc10_b256")):
+        ws_, exps = M.synthetic_weights(specs, hwc[2], cfg, image_channels=img_c if hwc[2] != img_c else None)
+        net = M.IntNet(specs, hwc, batch, ws_, exps)
+        px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hwc[0], hwc[1]), device="cuda")
+        lab = I.labels(I.base_seed(cfg, 2), batch, 10, device="cuda")
+        xq = torch.empty((batch,) + hwc, dtype=torch.int8, device="cuda")
+        s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+        with niti.recording() as calls:
+            niti.quantize_u8(px, xq)
+            net.step(xq, s0, lab)
+        ms = _replay_time(calls, reps if key != "c3" else 10)
+        ops = 2 * M.contraction_macs(specs, hwc, batch, img_c if hwc[2] != img_c else None)
+        res[key] = {"workload": name, "us_per_step": round(ms * 1e3, 2),
+                    "tops": round(ops / (ms * 1e-3) / 1e12, 3), "ops_per_step": ops}
+    return res
+
+
+# RTX 3090 int8 times (ms) the paper's Table 7 reports for these shapes: context only.
+TABLE7_PAPER_3090_MS = {"a": {224: 3.928, 112: 1.006, 56: 0.289, 28: 0.089, 14: 0.038},
+                        "e": {224: 4.731, 112: 1.269, 56: 0.453, 28: 0.185, 14: 0.117},
+                        "g": {224: 122.301, 112: 27.327, 56: 6.911, 28: 1.074, 14: 0.272}}
+
+
+def table7(reps=5):
+    """The paper's GPU shapes (batch 64, 64 -> 128 channels, 3x3, stride 1,
+    pad 1; inputs 224 ... 14): a = forward (fused exponent and rounding),
+    e = error back-propagation (fused), g = weight gradient + update."""
+    import torch
+    from paper_2009_13108_amd import inputs as I
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    out = []
+    for hw in (224, 112, 56, 28, 14):
+        d = niti.ConvDesc.make(64, hw, hw, 64, 128, 3, 3, 1, 1)
+        x = I.activations(I.base_seed(7, 1), d.x_shape(), device="cuda")
+        w = I.weights(I.base_seed(7, 2), d.w_shape(), device="cuda")
+        dy = I.errors8(I.base_seed(7, 3), d.y_shape(), device="cuda")
+        y = torch.empty(d.y_shape(), dtype=torch.int8, device="cuda")
+        dx = torch.empty(d.x_shape(), dtype=torch.int8, device="cuda")
+        stats = niti.new_stats(3)
+        ws = niti.new_workspace(max(niti.workspace_bytes(op, d) for op in (1, 2, 3)))
+        passes = {"a": lambda: niti.conv_fwd(d, x, w, y, stats, relu=True, ws=ws, stats_index=0),
+                  "e": lambda: niti.conv_bwd_data(d, dy, w, dx, stats, ws, relu_src=x, stats_index=1),
+                  "g": lambda: niti.conv_bwd_weight(d, x, dy, w, stats, ws, mu=5, stats_index=2)}
+        macs = 64 * hw * hw * 128 * 64 * 9
+        for k, fn in passes.items():
+            with niti.recording() as calls:
+                fn()
+            ms = _replay_time(calls, reps)
+            out.append({"input": hw, "pass": k, "ms": round(ms, 4),
+                        "tops": round(2 * macs / (ms * 1e-3) / 1e12, 1),
+                        "paper_rtx3090_int8_ms": TABLE7_PAPER_3090_MS[k][hw]})
+        del x, dy, y, dx, ws
+    return out
 
 
 # ----------------------------------------------------------------------------
@@ -391,8 +674,8 @@ def kernel_sources_digest():
     return h.hexdigest()
 
 
-def measured_traffic(family):
-    """HBM bytes per call of a family from the committed counter summary, or
+def measured_traffic(kernel):
+    """HBM bytes per launch of a kernel from the committed counter summary, or
     None when the kernel sources changed since the counters were taken."""
     try:
         vals = {}
@@ -402,65 +685,67 @@ def measured_traffic(family):
                 vals[k.strip()] = v.strip()
         if vals.get("kernel_sources_sha256") != kernel_sources_digest():
             return None
-        return int(vals["%s_hbm_bytes_per_call" % family])
+        return int(vals["%s_hbm_bytes_per_launch" % kernel])
     except (OSError, KeyError, ValueError):
         return None
 
 
+def kernel_label(profiler_name):
+    """The library's label for a profiler kernel name: the kernel's own name
+    and its template arguments, without namespaces, spaces or the argument
+    list (niti::(anonymous namespace)::igemm_dma_main<128, 128, 4, 4, 2, 1>(...)
+    -> igemm_dma_main<128,128,4,4,2,1>)."""
+    import re
+    n = profiler_name.replace("(anonymous namespace)::", "").replace("void ", "")
+    n = re.sub(r"^niti::", "", n)
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    return n[:cut].replace(" ", "")
+
+
 def summarize_kernel_trace(path):
-    """Per-kernel and per-family durations from a rocprofv3 kernel-trace CSV
-    (--kernel-trace --output-format csv), grouped the way the library's timing
-    hooks group them: igemm = implicit-GEMM kernels and their finishing
-    launches, wgrad = weight-gradient contraction kernels."""
+    """Per-kernel durations from a rocprofv3 kernel-trace CSV
+    (--kernel-trace --output-format csv), labelled as the library labels its
+    timing records."""
     import collections
     import csv
-    import re
 
-    rows = list(csv.DictReader(open(path)))
     per = collections.OrderedDict()
-    for r in rows:
-        name = re.sub(r"\(.*", "", r["Kernel_Name"].replace("(anonymous namespace)::", "")).replace("void ", "")
+    for r in csv.DictReader(open(path)):
+        if "niti::" not in r["Kernel_Name"]:
+            continue
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        per.setdefault(name, []).append(dur)
-    print("%-58s %7s %11s %9s" % ("kernel", "calls", "total_us", "avg_us"))
+        per.setdefault(kernel_label(r["Kernel_Name"]), []).append(dur)
+    print("%-44s %7s %11s %9s" % ("kernel", "calls", "total_us", "avg_us"))
     for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
-        if "niti::" in name:
-            print("%-58s %7d %11.1f %9.2f" % (name[:58], len(v), sum(v), sum(v) / len(v)))
-    fam = {"igemm": (r"niti::igemm_(dma_|wres_)?(main|fixup)<", r"niti::igemm_(dma_|wres_)?main<"),
-           "wgrad": (r"niti::wgrad_\w*kernel<", r"niti::wgrad_\w*kernel<")}
-    for f, (member, counter) in fam.items():
-        tot = sum(sum(v) for n, v in per.items() if re.search(member, n))
-        calls = sum(len(v) for n, v in per.items() if re.search(counter, n))
-        if calls:
-            print("family %-6s calls %6d  total %11.1f us  per call %8.2f us" % (f, calls, tot, tot / calls))
+        print("%-44s %7d %11.1f %9.2f" % (name[:44], len(v), sum(v), sum(v) / len(v)))
 
 
 def summarize_counters(path):
-    """Per-family sums of a rocprofv3 --pmc counter CSV (one counter per run,
-    e.g. FETCH_SIZE or WRITE_SIZE in KiB per dispatch): total over the
-    family's kernels divided by its calls, plus the calibration copy."""
+    """Per-kernel averages of a rocprofv3 --pmc counter CSV (e.g. FETCH_SIZE
+    or WRITE_SIZE in KiB per dispatch), labelled as above, plus the plain
+    copy kernel used for calibration."""
     import collections
     import csv
-    import re
 
     per = collections.defaultdict(lambda: collections.defaultdict(float))
     disp = collections.defaultdict(set)
     for r in csv.DictReader(open(path)):
         name = r["Kernel_Name"]
-        per[r["Counter_Name"]][name] += float(r["Counter_Value"])
-        disp[name].add(r["Dispatch_Id"])
-    calls = {n: len(d) for n, d in disp.items()}
-    fam = {"igemm": (r"niti::\(anonymous namespace\)::igemm_(dma_|wres_)?(main|fixup)<", r"igemm_(dma_|wres_)?main<"),
-           "wgrad": (r"niti::\(anonymous namespace\)::wgrad_\w*kernel<", r"wgrad_\w*kernel<")}
+        lab = kernel_label(name) if "niti::" in name else name[:60]
+        per[r["Counter_Name"]][lab] += float(r["Counter_Value"])
+        disp[lab].add(r["Dispatch_Id"])
     for cname, vals in per.items():
-        for f, (member, counter) in fam.items():
-            tot = sum(v for n, v in vals.items() if re.search(member, n))
-            n = sum(c for k, c in calls.items() if re.search(counter, k))
-            if n:
-                print("%s family %-6s calls %6d  per call %12.1f KiB" % (cname, f, n, tot / n))
-        cp = [(n, v) for n, v in vals.items() if "copy" in n.lower() or "elementwise" in n.lower()]
-        for n, v in cp:
-            print("%s copy-like kernel %s... calls %d per call %.1f KiB" % (cname, n[:60], calls[n], v / max(1, calls[n])))
+        for lab, v in sorted(vals.items(), key=lambda kv: -kv[1]):
+            n = len(disp[lab])
+            print("%s %-60s launches %6d per launch %14.1f" % (cname, lab, n, v / n))
 
 
 def copy_calibration(nbytes):
@@ -484,7 +769,12 @@ def main():
     ap.add_argument("--batch", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=64)
-    ap.add_argument("--layers", action="store_true", help="per-layer timing table on stderr")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip configs 1-3, the config-5 GEMM sweep and the Table 7 shapes")
+    ap.add_argument("--only", choices=("c5", "small", "table7"),
+                    help="run only the config-5 sweep, configs 1-3 or the Table 7 shapes and print their JSON "
+                         "(for profiling one workload)")
+    ap.add_argument("--c5-sizes", default="4096,8192,16384", help="sizes of the --only c5 sweep")
     ap.add_argument("--no-prepared", action="store_true",
                     help="enqueue every call through the checked binding instead of replaying prepared calls")
     ap.add_argument("--kernel-trace", metavar="CSV",
@@ -511,6 +801,15 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.only:
+        if args.only == "c5":
+            res = c5_sweep(sizes=tuple(int(v) for v in args.c5_sizes.split(",")))
+        elif args.only == "small":
+            res = small_configs()
+        else:
+            res = table7()
+        print(json.dumps({"only": args.only, "result": res}), flush=True)
+        return
     print("[bench] building inputs", file=sys.stderr, flush=True)
     job = ResNetStep(batch=args.batch)
     torch.cuda.synchronize()
@@ -547,40 +846,40 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     m1, c1 = job.misses()
 
-    # roofline: the same steps again, with the library's own HIP events
-    # recorded on the launch stream around every contraction launch.  A spin
-    # kernel first lets the host queue run ahead, so that no event waits on
-    # the host.
-    # (serialized on one stream, so that no other call's kernels share the GPU
-    # while a call is timed)
-    torch.cuda.synchronize()
-    try:
-        torch.cuda._sleep(int(0.05 * 2.4e9))
-    except Exception:
-        pass
-    niti = job.niti
-    niti.timing_enable(True)
-    for _ in range(args.steps):
-        job.step_serial()
-    niti.timing_enable(False)
-    torch.cuda.synchronize()
-    fams = {"igemm": niti.timing_read(niti.TIMING_IGEMM), "wgrad": niti.timing_read(niti.TIMING_WGRAD)}
-    for f, (_, n) in fams.items():
-        assert n == args.steps * job.fam_calls[f], (f, n)
-    fam = max(fams, key=lambda f: fams[f][0])
-    per_call_ms = fams[fam][0] / fams[fam][1]
-    ops_per_call = job.fam_ops[fam] / job.fam_calls[fam]
-    achieved = ops_per_call / (per_call_ms * 1e-3) / 1e12
+    # Kernel-level timing: the same steps again, serialized on one stream (so
+    # that no other call's kernels share the GPU while a call is timed), with
+    # the library's own HIP events recorded on the launch stream around each
+    # contraction's main kernel, each call's kernels, and the sum, update and
+    # loss passes.
+    ser = measure_serial(job, args.steps)
+    kern = ser["kernels"]
+    top = max(kern, key=lambda k: kern[k][1])
+    n_top, ms_top, ops_top = kern[top]
+    achieved = ops_top / (ms_top * 1e-3) / 1e12
     value = job.ops_per_step / (ms * 1e-3) / 1e12
+    fam = ser["families"]
 
-    if args.layers:
-        report_layers(job)
+    extra = {}
+    if not args.no_configs:
+        print("[bench] configs 1-3", file=sys.stderr, flush=True)
+        extra.update(small_configs())
+        print("[bench] config 5 GEMM sweep", file=sys.stderr, flush=True)
+        extra["c5"] = c5_sweep()
+        print("[bench] paper Table 7 shapes", file=sys.stderr, flush=True)
+        extra["table7_context"] = table7()
 
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle, batch %d)" % args.cpu_batch, file=sys.stderr, flush=True)
         cpu = cpu_baseline(args.cpu_batch)
 
+    passes = {}
+    for k, (pms, n, nbytes) in ser["passes"].items():
+        if n:
+            passes[k] = {"calls_per_step": n // args.steps, "us_per_call": round(pms * 1e3 / n, 2),
+                         "gbs": round(nbytes / (pms * 1e-3) / 1e9, 1),
+                         "frac_of_hbm": round(nbytes / (pms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    c5 = extra.get("c5", [])
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -605,51 +904,33 @@ def main():
         "pct_of_int8_mfma_peak": round(100.0 * value / PEAK_INT8_TOPS, 2),
         "ops_per_step": job.ops_per_step,
         "hint": {"misses_timed": m1 - m0, "calls_timed": c1 - c0, "misses_by_call": job.miss_table()},
-        "roofline": {"bound": "mfma", "kernel": fam, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
+        "roofline": {"bound": "mfma", "kernel": top, "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                      "unit": "TOPS", "frac": round(achieved / PEAK_INT8_TOPS, 4),
-                     "traffic": measured_traffic(fam),
-                     "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "algorithmic_bytes_per_call": job.fam_bytes[fam] // job.fam_calls[fam],
-                     "per_call_ms": round(per_call_ms, 5), "calls_per_step": job.fam_calls[fam],
-                     "family_ms_per_step": {f: round(v[0] / args.steps, 4) for f, v in fams.items()},
-                     "family_tops": {f: round(job.fam_ops[f] * args.steps / (v[0] * 1e-3) / 1e12, 2)
-                                     for f, v in fams.items()}},
+                     "traffic": measured_traffic(top),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "launches_per_step": n_top // args.steps,
+                     "avg_us": round(ms_top * 1e3 / n_top, 2),
+                     "algorithmic_ops_per_launch": ops_top // n_top,
+                     "kernels": {k: {"launches_per_step": v[0] // args.steps, "avg_us": round(v[1] * 1e3 / v[0], 2),
+                                     "tops": round(v[2] / (v[1] * 1e-3) / 1e12, 1)}
+                                 for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])},
+                     "family_tops": {f: round(v[2] / (v[1] * 1e-3) / 1e12, 1) for f, v in fam.items()},
+                     "family_ms_per_step": {f: round(v[1] / args.steps, 4) for f, v in fam.items()}},
+        "passes": passes,
+        "c4_layers": c4_layer_table(ser),
         "cpu_baseline": cpu,
     }
+    for k in ("c1", "c2", "c3"):
+        if k in extra:
+            out[k] = extra[k]
+    if c5:
+        out["c5"] = c5
+        big = [r for r in c5 if r["M"] == r["N"] == r["K"]]
+        out["c5_square_frac"] = {"%s_%d" % (r["dist"], r["M"]): r["frac"] for r in big}
+        out["c5_best_frac"] = max(r["frac"] for r in c5)
+    if "table7_context" in extra:
+        out["table7_context"] = extra["table7_context"]
     print(json.dumps(out), flush=True)
-
-
-def report_layers(job, reps=5):
-    """Per-layer pass times (stderr), for the design notes."""
-    import torch
-    niti = job.niti
-    print("%-12s %10s %10s %10s %8s %8s %8s" % ("layer", "fwd_us", "dgrad_us", "wgrad_us", "fwdTOPS",
-                                                 "dgTOPS", "wgTOPS"), file=sys.stderr)
-    for L in job.layers:
-        d, w, s0 = L["desc"], L["w"][0], L["stats"]
-        calls = [lambda: niti.conv_fwd(d, L["x"], w, L["y"], job.stats, relu=True, stats_index=s0, ws=job.ws),
-                 (lambda: niti.conv_bwd_data(d, L["dy"], w, L["dx"], job.stats, job.ws, relu_src=L["x"],
-                                             stats_index=s0 + 1)) if L["bwd_data"] else None,
-                 lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, job.stats, job.ws, mu=job.mu,
-                                              stats_index=s0 + 2)]
-        us = []
-        for fn in calls:
-            if fn is None:
-                us.append(float("nan"))
-                continue
-            fn()
-            torch.cuda.synchronize()
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record()
-            for _ in range(reps):
-                fn()
-            b.record()
-            torch.cuda.synchronize()
-            us.append(a.elapsed_time(b) * 1e3 / reps)
-        tops = [2 * L["macs"] / (u * 1e-6) / 1e12 if u == u else float("nan") for u in us]
-        print("%-12s %10.1f %10.1f %10.1f %8.1f %8.1f %8.1f" % ((L["name"],) + tuple(us) + tuple(tops)),
-              file=sys.stderr, flush=True)
 
 
 if __name__ == "__main__":

@@ -273,20 +273,37 @@ niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
 size_t niti_stats_bytes(void);
 
 /* ---- Kernel timing (a profiling aid; no effect on results) ----
- * While enabled, every call records a HIP event pair on its own stream
- * around its contraction launches: family NITI_TIMING_IGEMM brackets the
- * implicit-GEMM kernel and its finishing launch (niti_gemm_fwd,
- * niti_conv_fwd, niti_conv_bwd_data), NITI_TIMING_WGRAD the weight-gradient
- * contraction kernel of niti_conv_bwd_weight (not its sum, maximum and
- * update passes).  niti_timing_enable(1) clears the record and starts,
- * niti_timing_enable(0) stops.  niti_timing_read waits for the recorded
- * events and returns the summed milliseconds and the number of calls of a
- * family.  The record is process-wide and not guarded against calls from
- * several host threads at once.  Returns NITI_ERR_ARG for an unknown
- * family, NITI_ERR_HIP if an event fails. */
-enum { NITI_TIMING_IGEMM = 0, NITI_TIMING_WGRAD = 1 };
+ * While enabled, calls record HIP event pairs on their own stream:
+ *   NITI_TIMING_IGEMM   the implicit-GEMM kernel and its finishing launch of
+ *                       every niti_gemm_fwd / niti_conv_fwd /
+ *                       niti_conv_bwd_data(_packed) call;
+ *   NITI_TIMING_WGRAD   the weight-gradient contraction kernel of every
+ *                       niti_conv_bwd_weight call;
+ *   NITI_TIMING_KERNEL  every contraction kernel launch alone (the main
+ *                       implicit-GEMM or weight-gradient kernel), labelled
+ *                       with the kernel and its template arguments;
+ *   NITI_TIMING_SUM     the split-sum and maximum pass of a weight gradient;
+ *   NITI_TIMING_UPDATE  the rounding and update pass of a weight gradient;
+ *   NITI_TIMING_LOSS    the two launches of niti_int_ce_loss_grad.
+ * niti_timing_enable(1) clears the record and starts, niti_timing_enable(0)
+ * stops.  niti_timing_read waits for the recorded events and returns the
+ * summed milliseconds and the number of records of a family;
+ * niti_timing_record returns record i (in enqueue order) with its family,
+ * label ("" when none; static storage) and milliseconds.  The record is
+ * process-wide and not guarded against calls from several host threads at
+ * once.  Return NITI_ERR_ARG for an unknown family or an index past the
+ * end, NITI_ERR_HIP if an event fails. */
+enum {
+    NITI_TIMING_IGEMM = 0,
+    NITI_TIMING_WGRAD = 1,
+    NITI_TIMING_KERNEL = 2,
+    NITI_TIMING_SUM = 3,
+    NITI_TIMING_UPDATE = 4,
+    NITI_TIMING_LOSS = 5
+};
 niti_status niti_timing_enable(int on);
 niti_status niti_timing_read(int family, double *ms, int64_t *calls);
+niti_status niti_timing_record(int64_t i, int *family, const char **name, double *ms);
 
 #ifdef __cplusplus
 }

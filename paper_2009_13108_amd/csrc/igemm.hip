@@ -356,7 +356,11 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         base += p.tiles_m * p.tiles_n;
     }
     b.total_tiles = base;
+    const int tk = timing_on()
+                       ? timing_begin(NITI_TIMING_KERNEL, stream, kernel_label("igemm_main<%d,%d>", TBM, TBN))
+                       : -1;
     hipLaunchKernelGGL((igemm_main<TBM, TBN>), dim3(base), dim3(NTHREADS), 0, stream, b, ctl);
+    timing_end(tk, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int fix_grid = base < kFixupGrid ? base : kFixupGrid;

@@ -504,8 +504,13 @@ hipError_t launch_dma(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
         base += p.tiles_m * p.tiles_n;
     }
     b.total_tiles = base;
+    const int tk = timing_on() ? timing_begin(NITI_TIMING_KERNEL, stream,
+                                              kernel_label("igemm_dma_main<%d,%d,%d,%d,%d,%d>", BM, BN, NS, WGM,
+                                                           WGN, MODE))
+                               : -1;
     hipLaunchKernelGGL((igemm_dma_main<BM, BN, NS, WGM, WGN, MODE>), dim3(base), dim3(T::NT), T::LDS_BYTES, stream,
                        b, ctl);
+    timing_end(tk, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int fix_grid = base < kFixupGrid ? base : kFixupGrid;

@@ -197,7 +197,9 @@ bool igemm_small_eligible(const IgemmBatch& b) {
 hipError_t igemm_small_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     const IgemmProblem& p = b.p[0];
     const int ntiles = ((p.M + 31) / 32) * ((p.Nout + 31) / 32);
+    const int tk = timing_begin(NITI_TIMING_KERNEL, stream, "igemm_small_main");
     hipLaunchKernelGGL(igemm_small_main, dim3(ntiles), dim3(ST), 0, stream, p, ctl);
+    timing_end(tk, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int fix_grid = ntiles < kFixupGrid ? ntiles : kFixupGrid;

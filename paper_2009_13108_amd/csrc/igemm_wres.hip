@@ -424,7 +424,11 @@ hipError_t launch_wres(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
     const int tasks = (p.M + 31) / 32;
     int grid = (tasks + NWAVES - 1) / NWAVES;
     if (grid > per_cu * resident) grid = per_cu * resident;
+    const int tk = timing_on() ? timing_begin(NITI_TIMING_KERNEL, stream,
+                                              kernel_label("igemm_wres_main<%d,%d,%d>", NF, MODE, D))
+                               : -1;
     hipLaunchKernelGGL((igemm_wres_main<NF, MODE, D>), dim3(grid), dim3(NT), lds, stream, b, ctl, tasks);
+    timing_end(tk, stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((igemm_wres_fixup<NF, MODE, D>), dim3(grid), dim3(NT), lds, stream, b, ctl, tasks);

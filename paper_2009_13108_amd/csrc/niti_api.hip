@@ -540,9 +540,14 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
         e = wgrad_dma_eligible(p) ? wgrad_dma_run(p, plan, strm) : wgrad_run(p, plan, strm);
     timing_end(tix, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
+    const int tsum = timing_on() ? timing_begin(NITI_TIMING_SUM, strm, kernel_label("split_sum<%d>", plan.splits)) : -1;
     e = reduce_max_run(part, plan.splits, g32, nw, stats, strm);
+    timing_end(tsum, strm);
     if (e != hipSuccess) return NITI_ERR_HIP;
-    return hip_status(update_run(w, g32, nw, mu, mode, stats, acc_flags(npix), strm));
+    const int tupd = timing_begin(NITI_TIMING_UPDATE, strm);
+    e = update_run(w, g32, nw, mu, mode, stats, acc_flags(npix), strm);
+    timing_end(tupd, strm);
+    return hip_status(e);
 }
 
 namespace {
@@ -622,7 +627,10 @@ niti_status niti_int_ce_loss_grad(const int8_t* logits, const int8_t* s_logits, 
     if (too_big(batch * classes * 16)) return NITI_ERR_UNSUPPORTED;
     const size_t need = niti_workspace_bytes(NITI_OP_INT_CE_LOSS, nullptr, batch, classes, 0);
     if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
-    return hip_status(loss_run(logits, s_logits, labels, err, ws, batch, classes, mode, stats, as_stream(stream)));
+    const int t = timing_begin(NITI_TIMING_LOSS, as_stream(stream));
+    const hipError_t e = loss_run(logits, s_logits, labels, err, ws, batch, classes, mode, stats, as_stream(stream));
+    timing_end(t, as_stream(stream));
+    return hip_status(e);
 }
 
 niti_status niti_sgd_update(int8_t* w, const int32_t* g32, int64_t n, int mu, niti_round_mode mode,

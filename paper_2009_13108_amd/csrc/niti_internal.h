@@ -76,9 +76,13 @@ struct IgemmCtl {
 
 hipError_t igemm_run(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream);
 // Kernel timing hooks (timing.hip): begin returns a record index, or -1 when
-// timing is off; end closes that record on the same stream.
-int timing_begin(int family, hipStream_t s);
+// timing is off; end closes that record on the same stream.  name labels a
+// NITI_TIMING_KERNEL record (a string that lives as long as the process:
+// kernel_label() makes one from a format, once per distinct text).
+int timing_begin(int family, hipStream_t s, const char* name = nullptr);
 void timing_end(int idx, hipStream_t s);
+bool timing_on();
+const char* kernel_label(const char* fmt, ...);
 // Few outputs, long reduction (igemm_small.hip): a single plain matrix
 // product of at most 1024 rows.
 bool igemm_small_eligible(const IgemmBatch& b);

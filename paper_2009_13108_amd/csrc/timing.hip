@@ -1,5 +1,12 @@
 // Kernel timing hooks: HIP event pairs recorded on a call's stream around
-// its contraction launches, summed per family on request.  Host code only.
+// its launches, summed per family or read one by one on request.  Host code
+// only.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "niti_internal.h"
@@ -15,11 +22,28 @@ struct Pair {
 bool g_on = false;
 std::vector<Pair> g_pool;          // events created so far, reused after a restart
 std::vector<int> g_family;         // family of pair i (i < g_used)
+std::vector<const char*> g_name;   // kernel of pair i (NITI_TIMING_KERNEL) or NULL
 size_t g_used = 0;
 
 }  // namespace
 
-int timing_begin(int family, hipStream_t s) {
+const char* kernel_label(const char* fmt, ...) {
+    static std::mutex mu;
+    static std::unordered_map<std::string, std::string*> names;   // held for the process
+    char buf[128];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = names.find(buf);
+    if (it == names.end()) it = names.emplace(buf, new std::string(buf)).first;
+    return it->second->c_str();
+}
+
+bool timing_on() { return g_on; }
+
+int timing_begin(int family, hipStream_t s, const char* name) {
     if (!g_on) return -1;
     if (g_used == g_pool.size()) {
         Pair p{};
@@ -30,10 +54,12 @@ int timing_begin(int family, hipStream_t s) {
         }
         g_pool.push_back(p);
         g_family.push_back(0);
+        g_name.push_back(nullptr);
     }
     const int i = (int)g_used;
     if (hipEventRecord(g_pool[i].a, s) != hipSuccess) return -1;
     g_family[i] = family;
+    g_name[i] = name;
     g_used++;
     return i;
 }
@@ -56,7 +82,7 @@ niti_status niti_timing_enable(int on) {
 }
 
 niti_status niti_timing_read(int family, double* ms, int64_t* calls) {
-    if (family != NITI_TIMING_IGEMM && family != NITI_TIMING_WGRAD) return NITI_ERR_ARG;
+    if (family < NITI_TIMING_IGEMM || family > NITI_TIMING_LOSS) return NITI_ERR_ARG;
     if (!ms || !calls) return NITI_ERR_NULL;
     double tot = 0.0;
     int64_t n = 0;
@@ -70,6 +96,20 @@ niti_status niti_timing_read(int family, double* ms, int64_t* calls) {
     }
     *ms = tot;
     *calls = n;
+    return NITI_OK;
+}
+
+niti_status niti_timing_record(int64_t i, int* family, const char** name, double* ms) {
+    if (!family || !name || !ms) return NITI_ERR_NULL;
+    if (i < 0 || (size_t)i >= g_used) return NITI_ERR_ARG;
+    *family = g_family[i];
+    *name = g_name[i] ? g_name[i] : "";
+    *ms = -1.0;
+    if (g_family[i] < 0) return NITI_OK;
+    if (hipEventSynchronize(g_pool[i].b) != hipSuccess) return NITI_ERR_HIP;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, g_pool[i].a, g_pool[i].b) != hipSuccess) return NITI_ERR_HIP;
+    *ms = t;
     return NITI_OK;
 }
 

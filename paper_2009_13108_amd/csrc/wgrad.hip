@@ -222,7 +222,11 @@ template <int TBK, int TBC>
 hipError_t launch_wgrad(const WgradProblem& p, const WgradPlan& plan, hipStream_t stream) {
     const int tc = (p.ncol + TBC - 1) / TBC;
     const int tk = (p.K + TBK - 1) / TBK;
+    const int t = timing_on()
+                      ? timing_begin(NITI_TIMING_KERNEL, stream, kernel_label("wgrad_kernel<%d,%d>", TBK, TBC))
+                      : -1;
     hipLaunchKernelGGL((wgrad_kernel<TBK, TBC>), dim3(tc, tk, plan.splits), dim3(NTHREADS), 0, stream, p);
+    timing_end(t, stream);
     return hipGetLastError();
 }
 

@@ -267,8 +267,12 @@ hipError_t launch(const WgradProblem& p, const WgradPlan& plan, hipStream_t stre
     const int tc = ((p.win ? p.ncol_w : p.ncol) + TBC - 1) / TBC;
     const int tk = (p.K + TBK - 1) / TBK;
     const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
+    const int t = timing_on() ? timing_begin(NITI_TIMING_KERNEL, stream,
+                                             kernel_label("wgrad_dma_kernel<%d,%d,%d>", TBK, TBC, NS))
+                              : -1;
     hipLaunchKernelGGL((wgrad_dma_kernel<TBK, TBC, NS>), dim3((unsigned)grid), dim3(256), T::LDS, stream, p, tc, tk,
                        plan.splits);
+    timing_end(t, stream);
     return hipGetLastError();
 }
 

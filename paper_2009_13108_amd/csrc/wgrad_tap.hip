@@ -381,7 +381,9 @@ hipError_t wgrad_tap_run(WgradProblem& p, const WgradPlan& plan, hipStream_t str
     p.chunk = plan.chunk;
     const int tc = p.C / CW, tk = p.K / 64;
     const int64_t grid = (int64_t)8 * (((int64_t)tc * tk * plan.splits + 7) / 8);
+    const int t = timing_on() ? timing_begin(NITI_TIMING_KERNEL, stream, kernel_label("wgrad_tap_kernel<%d>", NS)) : -1;
     hipLaunchKernelGGL((wgrad_tap_kernel<NS>), dim3((unsigned)grid), dim3(NTHREADS), LDS, stream, p, tc, tk, plan.splits);
+    timing_end(t, stream);
     return hipGetLastError();
 }
 

@@ -185,3 +185,58 @@ RESNET18_LAYERS = [
     ("l4_3x3", 512, 512, 3, 1, 1, 7, 3),
 ]
 RESNET18_FC = (512, 1000)
+
+
+# ------------------------------------------------------------------ synthetic set-up
+def synthetic_weights(specs, in_channels, cfg, image_channels=None, first_id=10):
+    """Seeded U[-127,127] weights in the library's layouts for a layer list:
+    KRSC for convolutions (channels past image_channels of the first layer
+    zero), [out][in] for fully-connected layers with the input read in
+    (h, w, c) order; plus the static exponents (He-uniform style, from the
+    real fan-in).  Returns (weights as numpy arrays, exponents)."""
+    from . import inputs as I
+    ws, exps = [], []
+    wi = 0
+    for sp in specs:
+        if sp[0] == "conv":
+            _, cin, cout, k = sp[:4]
+            w = I.weights(I.base_seed(cfg, first_id + wi), (cout, k, k, cin))
+            real = cin
+            if wi == 0 and image_channels is not None and image_channels < cin:
+                w[..., image_channels:] = 0
+                real = image_channels
+            ws.append(w)
+            exps.append(I.weight_exponent(real * k * k))
+            wi += 1
+        elif sp[0] == "fc":
+            ws.append(I.weights(I.base_seed(cfg, first_id + wi), (sp[2], sp[1])))
+            exps.append(I.weight_exponent(sp[1]))
+            wi += 1
+    return ws, exps
+
+
+def contraction_macs(specs, in_shape, batch, image_channels=None):
+    """Multiply-accumulates of one training step of a layer list (forward,
+    back-propagation of every layer but the first, weight gradient), counted
+    on the real channel count of the image layer."""
+    h, w, c = in_shape
+    macs = 0
+    first = True
+    for sp in specs:
+        if sp[0] == "conv":
+            _, cin, cout, k, st, pd = sp[:6]
+            p = (h + 2 * pd - k) // st + 1
+            q = (w + 2 * pd - k) // st + 1
+            real = image_channels if (first and image_channels) else cin
+            m = batch * p * q * cout * real * k * k
+            macs += m * (2 if first else 3)
+            h, w, c = p, q, cout
+            first = False
+        elif sp[0] == "fc":
+            m = batch * sp[1] * sp[2]
+            macs += m * (2 if first else 3)
+            h, w, c = 1, 1, sp[2]
+            first = False
+        else:
+            h, w = h // 2, w // 2
+    return macs

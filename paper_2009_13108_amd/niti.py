@@ -84,11 +84,15 @@ EXPORTS = [
     "niti_conv_bwd_data_packed", "niti_conv_bwd_weight", "niti_conv_bwd_weight_noalloc",
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
-    "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read",
+    "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read", "niti_timing_record",
 ]
 
 TIMING_IGEMM = 0
 TIMING_WGRAD = 1
+TIMING_KERNEL = 2
+TIMING_SUM = 3
+TIMING_UPDATE = 4
+TIMING_LOSS = 5
 
 
 def lib():
@@ -117,6 +121,7 @@ def lib():
                 "niti_relu_mask": [P, P, I64, P],
                 "niti_timing_enable": [I],
                 "niti_timing_read": [I, P, P],
+                "niti_timing_record": [I64, P, P, P],
             }
             for name, args in sig.items():
                 f = getattr(L, name)
@@ -148,6 +153,22 @@ def timing_read(family: int):
     n = ctypes.c_int64(0)
     _check(lib().niti_timing_read(int(family), ctypes.byref(ms), ctypes.byref(n)), "niti_timing_read")
     return ms.value, n.value
+
+
+def timing_records():
+    """Every timing record in enqueue order: (family, label, milliseconds)."""
+    out = []
+    fam = ctypes.c_int(0)
+    name = ctypes.c_char_p()
+    ms = ctypes.c_double(0.0)
+    i = 0
+    while True:
+        st = lib().niti_timing_record(i, ctypes.byref(fam), ctypes.byref(name), ctypes.byref(ms))
+        if st == -6:
+            return out
+        _check(st, "niti_timing_record")
+        out.append((fam.value, name.value.decode(), ms.value))
+        i += 1
 
 
 # ------------------------------------------------------------------ helpers

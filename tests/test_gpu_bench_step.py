@@ -1,0 +1,59 @@
+"""The benchmark's timed step (two streams, filters packed on the second
+stream, calls marshalled once and replayed) leaves exactly the state that
+the same calls issued one after another on one stream leave: every weight,
+every output buffer the serial step also writes, and every statistics
+block, after several steps."""
+import numpy as np
+import pytest
+
+from paper_2009_13108_amd import niti
+from helpers import FLAG_HINT_MISS, host, say
+
+pytestmark = pytest.mark.gpu
+
+STEPS = 3
+BATCH = 8
+
+
+def _state(job):
+    import torch
+    torch.cuda.synchronize()
+    out = {}
+    for li, L in enumerate(job.layers):
+        for c, w in enumerate(L["w"]):
+            out["w%d.%d" % (li, c)] = host(w).copy()
+        out["y%d" % li] = host(L["y"]).copy()
+        if L["bwd_data"]:
+            out["dx%d" % li] = host(L["dx"]).copy()
+    for name in ("wfc", "logits", "err", "dfeat", "s_logits"):
+        out[name] = host(getattr(job, name)).copy()
+    return out
+
+
+def _stats(job):
+    st = niti.read_stats(job.stats)
+    return [(s["max_abs"], s["b"], s["bp"], s["flags"] & ~FLAG_HINT_MISS, s["s_out"], s["calls"]) for s in st]
+
+
+def test_two_stream_prepared_steps_equal_serial_steps():
+    import torch
+    import bench
+    say("bench step: two streams vs serial, batch", BATCH, "steps", STEPS)
+    par = bench.ResNetStep(batch=BATCH)
+    ser = bench.ResNetStep(batch=BATCH)
+    torch.cuda.synchronize()
+    a0, b0 = _state(par), _state(ser)
+    assert all(np.array_equal(a0[k], b0[k]) for k in a0 if k.startswith("w"))
+    par.prepare()                       # step 1 (recorded)
+    for _ in range(STEPS - 1):
+        par.step_prepared()
+    par.sA.wait_event(par.ev_upd)
+    for _ in range(STEPS):
+        ser.step_serial()
+    a, b = _state(par), _state(ser)
+    moved = sum(not np.array_equal(a[k], a0[k]) for k in a if k.startswith("w"))
+    assert moved > 0
+    bad = [k for k in a if not np.array_equal(a[k], b[k])]
+    assert not bad, bad
+    sa, sb = _stats(par), _stats(ser)
+    assert sa == sb, [i for i, (x, y) in enumerate(zip(sa, sb)) if x != y]
