@@ -238,7 +238,7 @@ __global__ void zero_classes_kernel(uint32_t* out, int32_t h, int32_t w, int32_t
 // the call in progress; this is its finishing launch.
 __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_fixed, int target,
                                  int mode, niti_stats* st, ExpArgs ex) {
-    const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(load_cur_acc(st), target);
+    const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(shared_call_state(st).mx, target);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
@@ -258,7 +258,7 @@ __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_
 // g = round(g32, max(0, B(g32) - mu)); w <- clamp(w - g).
 __global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict__ g32, int64_t n, int mu, int mode,
                               niti_stats* st, uint32_t static_flags) {
-    const int bp = block_bp(load_cur_acc(st), mu);
+    const int bp = block_bp(shared_call_state(st).mx, mu);
     const RoundK rk = make_round(bp, mode);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -468,7 +468,7 @@ constexpr int LR = 4;
 __global__ void loss_round_kernel(const i128* __restrict__ e128, int8_t* __restrict__ err, int64_t n, int mode,
                                   const int8_t* __restrict__ s_logits, niti_stats* st) {
     const int msh = loss_max_shift(loss_eval_sa((int)*s_logits));
-    const uint64_t mx = load_cur_acc(st);
+    const uint64_t mx = shared_call_state(st).mx;
     const int b = mx ? bitlen64(mx) + msh : 0;
     const int bp = b > 7 ? b - 7 : 0;
     const int rtn = mode == NITI_ROUND_RTN;

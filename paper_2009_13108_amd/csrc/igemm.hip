@@ -331,8 +331,9 @@ template <int TBM, int TBN>
 __global__ __launch_bounds__(NTHREADS) void igemm_fixup(IgemmBatch batch, IgemmCtl ctl) {
     __shared__ Smem<TBM, TBN> sm;
     niti_stats* st = ctl.stats;
-    const int hint = st->hint_used;
-    const int bp = block_bp(load_cur_acc(st), ctl.target);
+    const CallState cs = shared_call_state(st);
+    const int hint = cs.hint;
+    const int bp = block_bp(cs.mx, ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         for (int tt = blockIdx.x; tt < batch.total_tiles; tt += gridDim.x) {

@@ -467,8 +467,9 @@ template <int BM, int BN, int NS, int WGM, int WGN, int MODE>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void igemm_dma_fixup(IgemmBatch batch, IgemmCtl ctl) {
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
-    const int hint = st->hint_used;
-    const int bp = block_bp(load_cur_acc(st), ctl.target);
+    const CallState cs = shared_call_state(st, dyn_lds);
+    const int hint = cs.hint;
+    const int bp = block_bp(cs.mx, ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         for (int t = blockIdx.x; t < batch.total_tiles; t += gridDim.x) {

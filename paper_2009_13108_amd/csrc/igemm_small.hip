@@ -167,8 +167,9 @@ __global__ __launch_bounds__(ST) void igemm_small_main(IgemmProblem P, IgemmCtl 
 __global__ __launch_bounds__(ST) void igemm_small_fixup(IgemmProblem P, IgemmCtl ctl, int ntiles) {
     __shared__ __attribute__((aligned(16))) int32_t red[SW * 32 * RP];
     niti_stats* st = ctl.stats;
-    const int hint = st->hint_used;
-    const int bp = block_bp(load_cur_acc(st), ctl.target);
+    const CallState cs = shared_call_state(st);
+    const int hint = cs.hint;
+    const int bp = block_bp(cs.mx, ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         uint32_t dummy = 0;

@@ -383,8 +383,9 @@ template <int NF, int MODE, int D>
 __global__ __launch_bounds__(NT, (WrCfg<NF, D>::MINW)) void igemm_wres_fixup(IgemmBatch batch, IgemmCtl ctl, int tasks) {
     extern __shared__ __attribute__((aligned(1024))) int8_t dyn_lds[];
     niti_stats* st = ctl.stats;
-    const int hint = st->hint_used;
-    const int bp = block_bp(load_cur_acc(st), ctl.target);
+    const CallState cs = shared_call_state(st, dyn_lds);
+    const int hint = cs.hint;
+    const int bp = block_bp(cs.mx, ctl.target);
     if (bp != hint) {
         const RoundK rk = make_round(bp, ctl.mode);
         uint32_t dummy = 0;

@@ -243,6 +243,34 @@ __device__ __forceinline__ uint64_t load_cur_acc(niti_stats* st) {
     return (st->cur & 1) ? a1 : a0;
 }
 
+// The maximum of the call in progress and the guess that call tried, for a
+// finishing launch: read by one thread of the workgroup and handed to the
+// others through LDS.  All of a launch's requests go to the one stats
+// address and queue behind each other, so one request per workgroup instead
+// of one per wave keeps a launch whose guess was right short.  Every thread
+// of the workgroup must call it; lds is 16 bytes of LDS the kernel may
+// reuse afterwards.
+struct CallState {
+    uint64_t mx;
+    int hint;
+};
+__device__ __forceinline__ CallState shared_call_state(niti_stats* st, void* lds) {
+    uint64_t* sh = (uint64_t*)lds;
+    if (threadIdx.x == 0) {
+        sh[0] = load_cur_acc(st);
+        sh[1] = (uint64_t)(uint32_t)st->hint_used;
+    }
+    __syncthreads();
+    const CallState r{sh[0], (int)(uint32_t)sh[1]};
+    __syncthreads();   // every thread has its copy before the LDS is reused
+    return r;
+}
+// The same for kernels without LDS of their own (16 bytes of static LDS).
+__device__ __forceinline__ CallState shared_call_state(niti_stats* st) {
+    __shared__ uint64_t sh[2];
+    return shared_call_state(st, sh);
+}
+
 // Snapshot of the tensor maximum taken when a workgroup starts (by thread 0,
 // the one that publishes).  The maximum only grows, so a workgroup maximum
 // not above the snapshot can be skipped without a fresh read at the end.
