@@ -39,8 +39,18 @@
  *               state; two calls in flight at once must not share one.
  *   Rounding    mode NITI_ROUND_PSR is Algorithm 3; NITI_ROUND_RTN rounds
  *               to nearest with ties away from zero (Section 4.3 uses it for
- *               activations and errors).  A rounded magnitude that would
- *               reach 128 is held at 127, so outputs lie in [-127, 127].
+ *               activations and errors); NITI_ROUND_SR is the stochastic
+ *               rounding Section 3.4 compares against: the magnitude
+ *               x = q 2^bp + f is rounded up exactly when the top bp bits of
+ *               a 64-bit draw r are below f (probability f / 2^bp), where
+ *               r = SplitMix64 (Steele, Lea and Flood, OOPSLA 2014) output
+ *               number c * 2^40 + i + 1 of the stream seeded with
+ *               stats.sr_seed, c = stats.calls before the call, i = the
+ *               element's offset in its output tensor (NHWC activations and
+ *               errors, KRSC weights, row-major matrices).  Convolution and
+ *               matrix calls in this mode run on the general kernels.  A
+ *               rounded magnitude that would reach 128 is held at 127, so
+ *               outputs lie in [-127, 127].
  *   Speculation The library first rounds with the binary point that the
  *               same stats block reported last time (bp_hint), checks it
  *               against the true block maximum, and recomputes the output
@@ -69,7 +79,8 @@ typedef enum niti_status {
 
 typedef enum niti_round_mode {
     NITI_ROUND_PSR = 0, /* pseudo stochastic rounding, Algorithm 3 */
-    NITI_ROUND_RTN = 1  /* round to nearest, ties away from zero   */
+    NITI_ROUND_RTN = 1, /* round to nearest, ties away from zero   */
+    NITI_ROUND_SR = 2   /* stochastic rounding with a counter-based draw (Section 3.4) */
 } niti_round_mode;
 
 /* niti_stats.flags bits */
@@ -98,7 +109,9 @@ typedef struct niti_stats {
     uint32_t wflags[2];
     int32_t cur;         /* slot of the call in progress  */
     int32_t hint_used;   /* guess the call in progress tried */
-    uint32_t reserved[14];
+    uint64_t sr_seed;    /* in: seed of the NITI_ROUND_SR draws (zero-filled is seed 0) */
+    uint32_t sr_call;    /* draw index c of the call in progress */
+    uint32_t reserved[11];
 } niti_stats;
 
 /* Convolution geometry.  Input x is NHWC [n][h][w][c]; filter is KRSC

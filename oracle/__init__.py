@@ -34,6 +34,7 @@ ACC_BOUND_LEN = 1 << 17
 
 PSR = 0
 RTN = 1
+SR = 2
 
 
 def build(force: bool = False) -> str:
@@ -70,13 +71,17 @@ def _load():
             P = ctypes.c_void_p
             I64 = ctypes.c_int64
             I = ctypes.c_int
+            U64 = ctypes.c_uint64
+            U32 = ctypes.c_uint32
             sig = {
                 "orc_bitlen": (I, [ctypes.c_uint64]),
                 "orc_psr": (I64, [I64, I]),
                 "orc_rtn": (I64, [I64, I]),
-                "orc_shift_round_i64": (I, [P, I64, I, I, P, P]),
-                "orc_shift_round_i32": (I, [P, I64, I, I, P, P]),
-                "orc_round_fixed_i32": (None, [P, I64, I, I, P]),
+                "orc_sr": (I64, [I64, I, U64]),
+                "orc_sr_draw": (U64, [U64, U32, U64]),
+                "orc_shift_round_i64": (I, [P, I64, I, I, P, P, U64, U32, P]),
+                "orc_shift_round_i32": (I, [P, I64, I, I, P, P, U64, U32, P]),
+                "orc_round_fixed_i32": (None, [P, I64, I, I, P, U64, U32]),
                 "orc_out_exponent": (I, [I, I, I, P]),
                 "orc_gemm_nt_raw": (None, [P, P, I64, I64, I64, P]),
                 "orc_gemm_nt_pick": (None, [P, P, I64, P, P, I64, P]),
@@ -84,10 +89,10 @@ def _load():
                 "orc_conv_bwd_data_raw": (None, [P, P, P, P]),
                 "orc_conv_bwd_weight_raw": (None, [P, P, P, P]),
                 "orc_conv_fwd_one": (I64, [P, P, P, I64, I64, I64, I64]),
-                "orc_finish_i64": (None, [P, I64, I, I, I, P, P, P, I64]),
-                "orc_sgd_update": (None, [P, P, I64, I, I, P]),
+                "orc_finish_i64": (None, [P, I64, I, I, I, P, P, P, I64, U64, U32, P]),
+                "orc_sgd_update": (None, [P, P, I64, I, I, P, U64, U32]),
                 "orc_loss_t_case": (I, [I]),
-                "orc_int_ce_loss_grad": (None, [P, I, P, I64, I64, I, P, P, P, P]),
+                "orc_int_ce_loss_grad": (None, [P, I, P, I64, I64, I, P, P, P, P, U64, U32]),
                 "orc_relu_mask": (None, [P, P, I64]),
                 "orc_maxpool2_fwd": (None, [P, I64, I64, I64, I64, P, P]),
                 "orc_maxpool2_bwd": (None, [P, P, I64, I64, I64, I64, P]),
@@ -137,7 +142,33 @@ def loss_case(s_a: int) -> int:
 
 
 # ---------------------------------------------------------------- rounding
-def shift_round(v, target: int, mode: int = PSR):
+def sr(v: int, bp: int, draw: int) -> int:
+    """Stochastic rounding of one value with a given 64-bit draw (Section 3.4)."""
+    return _load().orc_sr(int(v), int(bp), int(draw) & 0xFFFFFFFFFFFFFFFF)
+
+
+def sr_draw(seed: int, call: int, index: int) -> int:
+    """The 64-bit draw of element `index` in call `call` (SplitMix64 stream)."""
+    return int(_load().orc_sr_draw(int(seed) & 0xFFFFFFFFFFFFFFFF, int(call), int(index)))
+
+
+def nhwc_index(shape):
+    """Storage offsets in NHWC order of the elements of an NCHW tensor (the
+    stochastic draws are keyed by the library's storage order); for a KCRS
+    filter the same map gives KRSC offsets."""
+    n, c, h, w = shape
+    i = np.arange(n * h * w * c, dtype=np.int64).reshape(n, h, w, c)
+    return np.ascontiguousarray(i.transpose(0, 3, 1, 2))
+
+
+def _idx_ptr(idx):
+    if idx is None:
+        return None, None
+    a = np.ascontiguousarray(idx, dtype=np.int64)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def shift_round(v, target: int, mode: int = PSR, sr_seed: int = 0, sr_call: int = 0):
     """Block exponent + rounding of a whole tensor (Algorithms 1-3).
 
     ``v`` is int32 (accumulators) or int64 (loss values).  Returns
@@ -145,20 +176,24 @@ def shift_round(v, target: int, mode: int = PSR):
     v = np.asarray(v)
     st = Stats()
     out = np.empty(v.shape, np.int8)
+    seed = int(sr_seed) & 0xFFFFFFFFFFFFFFFF
     if v.dtype == np.int64:
         vc, pv = _c(v, np.int64)
-        _load().orc_shift_round_i64(pv, vc.size, int(target), int(mode), _ptr(out), ctypes.byref(st))
+        _load().orc_shift_round_i64(pv, vc.size, int(target), int(mode), _ptr(out), ctypes.byref(st),
+                                    seed, int(sr_call), None)
     else:
         vc, pv = _c(v, np.int32)
-        _load().orc_shift_round_i32(pv, vc.size, int(target), int(mode), _ptr(out), ctypes.byref(st))
+        _load().orc_shift_round_i32(pv, vc.size, int(target), int(mode), _ptr(out), ctypes.byref(st),
+                                    seed, int(sr_call), None)
     return out, st.as_dict()
 
 
-def round_fixed(v, bp: int, mode: int = PSR):
+def round_fixed(v, bp: int, mode: int = PSR, sr_seed: int = 0, sr_call: int = 0):
     """Round an int32 tensor with a given binary point."""
     vc, pv = _c(v, np.int32)
     out = np.empty(vc.shape, np.int8)
-    _load().orc_round_fixed_i32(pv, vc.size, int(bp), int(mode), _ptr(out))
+    _load().orc_round_fixed_i32(pv, vc.size, int(bp), int(mode), _ptr(out),
+                                int(sr_seed) & 0xFFFFFFFFFFFFFFFF, int(sr_call))
     return out
 
 
@@ -255,55 +290,74 @@ def conv_fwd_one(d: Conv, x, w, n, k, p, q):
 
 
 # ---------------------------------------------------------------- composites
-def finish(S, relu: bool, target: int, mode: int = PSR, red_len: int = 0):
+def finish(S, relu: bool, target: int, mode: int = PSR, red_len: int = 0, sr_seed: int = 0, sr_call: int = 0,
+           sr_index=None):
     """Exact sums -> int32 accumulators -> (ReLU) -> block exponent -> int8.
-    red_len: products per sum (FLAG_ACC_BOUND when >= 2^17).
+    red_len: products per sum (FLAG_ACC_BOUND when >= 2^17); sr_index: the
+    storage-order offset of each element for stochastic draws (default: its
+    position in S).
 
     Returns (int8 out, int32 accumulators, stats dict)."""
     S, ps = _c(S, np.int64)
     out = np.empty(S.shape, np.int8)
     acc = np.empty(S.shape, np.int32)
     st = Stats()
+    idx, pidx = _idx_ptr(sr_index)
     _load().orc_finish_i64(ps, S.size, int(bool(relu)), int(target), int(mode),
-                           _ptr(out), _ptr(acc), ctypes.byref(st), int(red_len))
+                           _ptr(out), _ptr(acc), ctypes.byref(st), int(red_len),
+                           int(sr_seed) & 0xFFFFFFFFFFFFFFFF, int(sr_call), pidx)
     return out, acc, st.as_dict()
 
 
-def gemm_fwd(A, B, relu=False, mode=PSR, target=7):
+def gemm_fwd(A, B, relu=False, mode=PSR, target=7, sr_seed=0, sr_call=0):
     """Fully-connected / plain GEMM forward step: int8 A (M x K), B (N x K)."""
-    return finish(gemm_nt_raw(A, B), relu, target, mode, np.shape(A)[1])
+    return finish(gemm_nt_raw(A, B), relu, target, mode, np.shape(A)[1], sr_seed, sr_call)
 
 
-def conv_fwd(d, x, w, relu=False, mode=PSR, target=7):
-    return finish(conv_fwd_raw(d, x, w), relu, target, mode, d.c * d.r * d.s)
+def conv_fwd(d, x, w, relu=False, mode=PSR, target=7, sr_seed=0, sr_call=0):
+    P, Q = conv_out_hw(d)
+    idx = nhwc_index((d.n, d.k, P, Q)) if mode == SR else None
+    return finish(conv_fwd_raw(d, x, w), relu, target, mode, d.c * d.r * d.s, sr_seed, sr_call, idx)
 
 
-def conv_bwd_data(d, dy, w, mode=PSR, relu_src=None, target=7):
+def conv_bwd_data(d, dy, w, mode=PSR, relu_src=None, target=7, sr_seed=0, sr_call=0):
     """Error back-propagation step; the optional ReLU mask (reading R5) is
     applied to the rounded int8 error and does not move its exponent."""
-    out, acc, st = finish(conv_bwd_data_raw(d, dy, w), False, target, mode, d.k * d.r * d.s)
+    idx = nhwc_index((d.n, d.c, d.h, d.w)) if mode == SR else None
+    out, acc, st = finish(conv_bwd_data_raw(d, dy, w), False, target, mode, d.k * d.r * d.s, sr_seed, sr_call,
+                          idx)
     if relu_src is not None:
         relu_mask(out, relu_src)
     return out, acc, st
 
 
-def sgd_update(w, g32, mu: int = 5, mode: int = PSR):
-    """Discrete weight update (Section 3.3).  Returns (new w, stats)."""
+def sgd_update(w, g32, mu: int = 5, mode: int = PSR, sr_seed: int = 0, sr_call: int = 0):
+    """Discrete weight update (Section 3.3).  Returns (new w, stats).  The
+    stochastic draws are keyed by the flat position in w and g32."""
     w = np.array(w, dtype=np.int8, copy=True, order="C")
     g32, pg = _c(g32, np.int32)
     assert w.size == g32.size
     st = Stats()
-    _load().orc_sgd_update(_ptr(w), pg, w.size, int(mu), int(mode), ctypes.byref(st))
+    _load().orc_sgd_update(_ptr(w), pg, w.size, int(mu), int(mode), ctypes.byref(st),
+                           int(sr_seed) & 0xFFFFFFFFFFFFFFFF, int(sr_call))
     return w, st.as_dict()
 
 
-def conv_bwd_weight(d, x, dy, w, mu: int = 5, mode: int = PSR):
-    """Weight gradient + discrete update.  Returns (new w, g32, stats)."""
+def conv_bwd_weight(d, x, dy, w, mu: int = 5, mode: int = PSR, sr_seed: int = 0, sr_call: int = 0):
+    """Weight gradient + discrete update.  Returns (new w, g32, stats).  In
+    SR mode the draws follow the filter's KRSC storage order."""
     S = conv_bwd_weight_raw(d, x, dy)
     P, Q = conv_out_hw(d)
     fl = np.zeros(1, np.int32)
     g32 = wrap32(S, fl)
-    w2, st = sgd_update(w, g32, mu, mode)
+    if mode == SR:
+        # update in the KRSC order the draws are keyed by, then back to KCRS
+        perm = (0, 2, 3, 1)
+        w2k, st = sgd_update(np.ascontiguousarray(np.asarray(w).transpose(perm)),
+                             np.ascontiguousarray(g32.transpose(perm)), mu, mode, sr_seed, sr_call)
+        w2 = np.ascontiguousarray(w2k.transpose(0, 3, 1, 2))
+    else:
+        w2, st = sgd_update(w, g32, mu, mode)
     st["flags"] |= int(fl[0]) | (FLAG_ACC_BOUND if d.n * P * Q >= ACC_BOUND_LEN else 0)
     return w2, g32, st
 
@@ -316,7 +370,7 @@ def wrap32(S, flags_out=None):
     return S.astype(np.uint64).astype(np.uint32).view(np.int32).reshape(S.shape)
 
 
-def int_ce_loss_grad(logits, s_a: int, labels, mode: int = PSR):
+def int_ce_loss_grad(logits, s_a: int, labels, mode: int = PSR, sr_seed: int = 0, sr_call: int = 0):
     """Integer cross-entropy gradient (Section 3.5).
 
     Returns (int8 err [B x N], pre-rounding values, stats dict).  The
@@ -331,7 +385,8 @@ def int_ce_loss_grad(logits, s_a: int, labels, mode: int = PSR):
     lo = np.empty((B, N), np.uint64)
     st = Stats()
     _load().orc_int_ce_loss_grad(pl, int(s_a), plab, B, N, int(mode), _ptr(err),
-                                 _ptr(hi), _ptr(lo), ctypes.byref(st))
+                                 _ptr(hi), _ptr(lo), ctypes.byref(st),
+                                 int(sr_seed) & 0xFFFFFFFFFFFFFFFF, int(sr_call))
     lo_signed = lo.view(np.int64)
     fits = ((hi == 0) & (lo_signed >= 0)) | ((hi == -1) & (lo_signed < 0))
     if fits.all():

@@ -128,8 +128,55 @@ int64_t orc_rtn(int64_t v, int bp)
     return v < 0 ? -(int64_t)q : (int64_t)q;
 }
 
-static int64_t round_one(int64_t v, int bp, int mode)
+/* Stochastic rounding (the Rs definition of Section 3.4): the magnitude
+ * q.f is rounded up with probability f / 2^bp.  The random number is a
+ * 64-bit draw r, and the magnitude goes up exactly when the top bp bits of
+ * r, read as an integer below 2^bp, are smaller than f (for bp > 64: when r
+ * is smaller than the top 64 bits of f). */
+int64_t orc_sr(int64_t v, int bp, uint64_t r)
 {
+    uint64_t x = mag64(v);
+    uint64_t q;
+    if (bp <= 0) {
+        q = x;
+    } else { /* bp in 1..63 */
+        const uint64_t f = x & (((uint64_t)1 << bp) - 1);
+        q = x >> bp;
+        if ((r >> (64 - bp)) < f)
+            q += 1;
+    }
+    if (q > 127)
+        q = 127;
+    return v < 0 ? -(int64_t)q : (int64_t)q;
+}
+
+/* The draws: output number c * 2^40 + i + 1 of the SplitMix64 generator
+ * (Steele, Lea and Flood, "Fast splittable pseudorandom number generators",
+ * OOPSLA 2014) started from the seed: the state advances by the golden
+ * gamma 0x9E3779B97F4A7C15 per output and each state is scrambled by the
+ * published finaliser. c counts the calls made with one statistics block,
+ * i is the element's position in its tensor's storage order (NHWC for
+ * activations and errors, KRSC for weights, row-major for matrices). */
+uint64_t orc_sr_draw(uint64_t seed, uint32_t call, uint64_t index)
+{
+    uint64_t z = seed + ((((uint64_t)call) << 40) + index + 1) * 0x9E3779B97F4A7C15ULL;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+/* Key of the stochastic draws of one call: seed, call counter and, per
+ * element, its storage-order index (idx[i], or i when idx is NULL). */
+typedef struct orc_srkey {
+    uint64_t seed;
+    uint32_t call;
+    const int64_t *idx;
+} orc_srkey;
+
+static int64_t round_one(int64_t v, int bp, int mode, const orc_srkey *k, int64_t i)
+{
+    if (mode == 2)
+        return orc_sr(v, bp, orc_sr_draw(k->seed, k->call, (uint64_t)(k->idx ? k->idx[i] : i)));
     return mode == 1 ? orc_rtn(v, bp) : orc_psr(v, bp);
 }
 
@@ -147,8 +194,10 @@ static int32_t wrap32(int64_t s, int32_t *flags)
  * max |v| (uint64 magnitude) -> b = B(max) -> bp = max(0, b - target) ->
  * every element rounded with that one bp.  Returns bp. */
 int orc_shift_round_i64(const int64_t *v, int64_t n, int target, int mode,
-                        int8_t *out, orc_stats *st)
+                        int8_t *out, orc_stats *st, uint64_t seed, uint32_t call,
+                        const int64_t *idx)
 {
+    const orc_srkey key = {seed, call, idx};
     uint64_t mx = 0;
     int64_t i;
     int b, bp;
@@ -163,7 +212,7 @@ int orc_shift_round_i64(const int64_t *v, int64_t n, int target, int mode,
         bp = 0;
 #pragma omp parallel for schedule(static)
     for (i = 0; i < n; i++)
-        out[i] = (int8_t)round_one(v[i], bp, mode);
+        out[i] = (int8_t)round_one(v[i], bp, mode, &key, i);
     if (st) {
         st->max_abs = mx;
         st->b = b;
@@ -174,8 +223,10 @@ int orc_shift_round_i64(const int64_t *v, int64_t n, int target, int mode,
 
 /* Same on an int32 tensor (accumulators, gradients). */
 int orc_shift_round_i32(const int32_t *v, int64_t n, int target, int mode,
-                        int8_t *out, orc_stats *st)
+                        int8_t *out, orc_stats *st, uint64_t seed, uint32_t call,
+                        const int64_t *idx)
 {
+    const orc_srkey key = {seed, call, idx};
     uint64_t mx = 0;
     int64_t i;
     int b, bp;
@@ -190,7 +241,7 @@ int orc_shift_round_i32(const int32_t *v, int64_t n, int target, int mode,
         bp = 0;
 #pragma omp parallel for schedule(static)
     for (i = 0; i < n; i++)
-        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode);
+        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode, &key, i);
     if (st) {
         st->max_abs = mx;
         st->b = b;
@@ -200,12 +251,14 @@ int orc_shift_round_i32(const int32_t *v, int64_t n, int target, int mode,
 }
 
 /* Round with a caller-given binary point (no block exponent search). */
-void orc_round_fixed_i32(const int32_t *v, int64_t n, int bp, int mode, int8_t *out)
+void orc_round_fixed_i32(const int32_t *v, int64_t n, int bp, int mode, int8_t *out,
+                         uint64_t seed, uint32_t call)
 {
+    const orc_srkey key = {seed, call, NULL};
     int64_t i;
 #pragma omp parallel for schedule(static)
     for (i = 0; i < n; i++)
-        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode);
+        out[i] = (int8_t)round_one((int64_t)v[i], bp, mode, &key, i);
 }
 
 /* Algorithm 2, exponent line: s_q = s_q32 + bp, with s_q32 = s_a + s_w
@@ -399,7 +452,8 @@ int64_t orc_conv_fwd_one(const orc_conv *d, const int8_t *x, const int8_t *w,
  * receives the int32 accumulators (after ReLU) when non-NULL; red_len is the
  * number of products in each sum (for ORC_FLAG_ACC_BOUND). */
 void orc_finish_i64(const int64_t *S, int64_t n, int relu, int target, int mode,
-                    int8_t *out, int32_t *acc32, orc_stats *st, int64_t red_len)
+                    int8_t *out, int32_t *acc32, orc_stats *st, int64_t red_len,
+                    uint64_t seed, uint32_t call, const int64_t *idx)
 {
     int32_t flags = red_len >= ORC_ACC_BOUND_LEN ? ORC_FLAG_ACC_BOUND : 0;
     int32_t *a = acc32 ? acc32 : (int32_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
@@ -410,7 +464,7 @@ void orc_finish_i64(const int64_t *S, int64_t n, int relu, int target, int mode,
             v = 0;
         a[i] = v;
     }
-    orc_shift_round_i32(a, n, target, mode, out, st);
+    orc_shift_round_i32(a, n, target, mode, out, st, seed, call, idx);
     if (st)
         st->flags |= flags;
     if (!acc32)
@@ -420,11 +474,11 @@ void orc_finish_i64(const int64_t *S, int64_t n, int relu, int target, int mode,
 /* Section 3.3 / Algorithm 1: the discrete update.  b = B(g32),
  * g = round(g32, max(0, b - mu)), w <- w - g held to [-127, 127] (R4). */
 void orc_sgd_update(int8_t *w, const int32_t *g32, int64_t n, int mu, int mode,
-                    orc_stats *st)
+                    orc_stats *st, uint64_t seed, uint32_t call)
 {
     int8_t *g = (int8_t *)malloc((size_t)(n > 0 ? n : 1));
     int64_t i;
-    orc_shift_round_i32(g32, n, mu, mode, g, st);
+    orc_shift_round_i32(g32, n, mu, mode, g, st, seed, call, NULL);
     for (i = 0; i < n; i++) {
         int v = (int)w[i] - (int)g[i];
         if (v > 127)
@@ -484,7 +538,7 @@ static int bitlen128(u128 m)
 }
 
 /* Algorithm 3 (or nearest) on a 128-bit value, the same steps as orc_psr. */
-static int8_t round128(i128 v, int bp, int mode)
+static int8_t round128(i128 v, int bp, int mode, uint64_t r)
 {
     u128 x = mag128(v), q, f, thi, rlo;
     int nb, h;
@@ -492,6 +546,12 @@ static int8_t round128(i128 v, int bp, int mode)
         q = x;
     } else if (mode == 1) {
         q = (x >> bp) + ((x >> (bp - 1)) & 1);
+    } else if (mode == 2) {
+        /* stochastic: as orc_sr, on 128 bits */
+        f = x & ((((u128)1) << bp) - 1);
+        q = x >> bp;
+        if (bp <= 64 ? ((u128)(r >> (64 - bp)) < f) : ((u128)r < (f >> (bp - 64))))
+            q += 1;
     } else {
         q = x >> bp;
         f = x & ((((u128)1) << bp) - 1);
@@ -517,7 +577,8 @@ static int8_t round128(i128 v, int bp, int mode)
  * 2 (-22 - s_a) bits when s_a < -22 (it would not fit 64 bits otherwise). */
 void orc_int_ce_loss_grad(const int8_t *logits, int s_a, const int32_t *labels,
                           int64_t B, int64_t N, int mode, int8_t *err,
-                          int64_t *e_hi, uint64_t *e_lo, orc_stats *st)
+                          int64_t *e_hi, uint64_t *e_lo, orc_stats *st,
+                          uint64_t seed, uint32_t call)
 {
     i128 *e = (i128 *)malloc((size_t)(B * N > 0 ? B * N : 1) * sizeof(i128));
     int32_t flags = 0;
@@ -564,7 +625,7 @@ void orc_int_ce_loss_grad(const int8_t *logits, int s_a, const int32_t *labels,
     b = bitlen128(mx);
     bp = b - 7 > 0 ? b - 7 : 0;
     for (i = 0; i < B * N; i++)
-        err[i] = round128(e[i], bp, mode);
+        err[i] = round128(e[i], bp, mode, mode == 2 ? orc_sr_draw(seed, call, (uint64_t)i) : 0);
     sh = s_a < ORC_LOSS_WIDE_SA ? 2 * (ORC_LOSS_WIDE_SA - s_a) : 0;
     if (st) {
         st->max_abs = (uint64_t)(mx >> sh);

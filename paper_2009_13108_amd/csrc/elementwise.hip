@@ -239,10 +239,14 @@ __global__ void zero_classes_kernel(uint32_t* out, int32_t h, int32_t w, int32_t
 __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_fixed, int target,
                                  int mode, niti_stats* st, ExpArgs ex) {
     const int bp = bp_fixed >= 0 ? bp_fixed : block_bp(shared_call_state(st).mx, target);
-    const RoundK rk = make_round(bp, mode);
+    RoundK rk = make_round(bp, mode);
+    if (bp_fixed >= 0)
+        sr_key_current(rk, st);    // an explicit binary point: no accumulating launch, calls not counted
+    else
+        sr_key_recorded(rk, st);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        y[i] = round_i32(x[i], rk);
+        y[i] = round_i32_at(x[i], rk, (uint64_t)i);
     if (bp_fixed >= 0) {
         // Algorithm 2: s_q = s_q32 + bp, held to the int8 range.
         if (ex.s_out && is_finisher()) {
@@ -259,7 +263,8 @@ __global__ void round_i32_kernel(const int32_t* x, int8_t* y, int64_t n, int bp_
 __global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict__ g32, int64_t n, int mu, int mode,
                               niti_stats* st, uint32_t static_flags) {
     const int bp = block_bp(shared_call_state(st).mx, mu);
-    const RoundK rk = make_round(bp, mode);
+    RoundK rk = make_round(bp, mode);
+    sr_key_recorded(rk, st);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     // Groups of four weights (one 4-byte word of w, 16 bytes of g32), two
@@ -283,7 +288,7 @@ __global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict_
             uint32_t out = 0;
 #pragma unroll
             for (int e = 0; e < 4; e++) {
-                int v = (int)(int8_t)(wv[j] >> (8 * e)) - (int)round_i32(gv[e], rk);
+                int v = (int)(int8_t)(wv[j] >> (8 * e)) - (int)round_i32_at(gv[e], rk, (uint64_t)(4 * q + e));
                 v = v > 127 ? 127 : (v < -127 ? -127 : v);
                 out |= (uint32_t)(uint8_t)v << (8 * e);
             }
@@ -291,7 +296,7 @@ __global__ void update_kernel(int8_t* __restrict__ w, const int32_t* __restrict_
         }
     }
     for (int64_t i = 4 * nq + tid; i < n; i += stride) {
-        int v = (int)w[i] - (int)round_i32(g32[i], rk);
+        int v = (int)w[i] - (int)round_i32_at(g32[i], rk, (uint64_t)i);
         v = v > 127 ? 127 : (v < -127 ? -127 : v);
         w[i] = (int8_t)v;
     }
@@ -445,17 +450,22 @@ __global__ void loss_kernel(const int8_t* __restrict__ logits, const int8_t* __r
     block_publish_max(st, slot, m, snap);
 }
 
-// Algorithm 3 (or nearest) on a 128-bit value with binary point bp <= 126.
-__device__ __forceinline__ int8_t round_i128(i128 v, int bp, int rtn) {
+// Algorithm 3, nearest, or stochastic (the draw's top bp bits against the
+// fraction; past 64 fraction bits, the draw against the fraction's top 64
+// bits) on a 128-bit value with binary point bp <= 126.
+__device__ __forceinline__ int8_t round_i128(i128 v, int bp, int mode, uint64_t draw) {
     const u128 x = mag128(v);
     u128 q = x >> bp;
     if (bp > 0) {
-        if (rtn) {
+        const u128 f = x & (((u128)1 << bp) - 1);
+        if (mode == NITI_ROUND_RTN) {
             q += (x >> (bp - 1)) & 1u;
+        } else if (mode == NITI_ROUND_SR) {
+            q += bp <= 64 ? ((u128)(draw >> (64 - bp)) < f ? 1u : 0u) : ((u128)draw < (f >> (bp - 64)) ? 1u : 0u);
         } else {
             const int odd = bp & 1, h = (bp - odd) >> 1;
-            const u128 f = (x & (((u128)1 << bp) - 1)) >> odd;
-            q += (f >> h) > (f & (((u128)1 << h) - 1)) ? 1u : 0u;
+            const u128 fe = f >> odd;
+            q += (fe >> h) > (fe & (((u128)1 << h) - 1)) ? 1u : 0u;
         }
     }
     const int qi = q < 127 ? (int)q : 127;
@@ -471,7 +481,8 @@ __global__ void loss_round_kernel(const i128* __restrict__ e128, int8_t* __restr
     const uint64_t mx = shared_call_state(st).mx;
     const int b = mx ? bitlen64(mx) + msh : 0;
     const int bp = b > 7 ? b - 7 : 0;
-    const int rtn = mode == NITI_ROUND_RTN;
+    RoundK rk = make_round(bp < 31 ? bp : 31, mode);
+    sr_key_recorded(rk, st);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += LR * stride) {
         i128 v[LR];
@@ -479,7 +490,9 @@ __global__ void loss_round_kernel(const i128* __restrict__ e128, int8_t* __restr
         for (int j = 0; j < LR; j++) v[j] = i0 + j * stride < n ? e128[i0 + j * stride] : (i128)0;
 #pragma unroll
         for (int j = 0; j < LR; j++)
-            if (i0 + j * stride < n) err[i0 + j * stride] = round_i128(v[j], bp, rtn);
+            if (i0 + j * stride < n)
+                err[i0 + j * stride] = round_i128(v[j], bp, mode,
+                                                  rk.sr ? sr_draw(rk.sr_seed, rk.sr_call, (uint64_t)(i0 + j * stride)) : 0ull);
     }
     if (is_finisher()) finish_call(st, 7, ExpArgs{nullptr, nullptr, nullptr}, 0u, 0, msh);
 }

@@ -279,7 +279,7 @@ __device__ __forceinline__ void run_tile(const IgemmProblem& P, int tm, int tn, 
                     uint32_t packed = 0;
 #pragma unroll
                     for (int i = 0; i < 4; i++)
-                        packed |= (uint32_t)(uint8_t)round_i32(v[i], rk) << (8 * i);
+                        packed |= (uint32_t)(uint8_t)round_i32_at(v[i], rk, (uint64_t)(ooff + n0 + i)) << (8 * i);
                     int8_t* dst = P.out + ooff + n0;
                     if (P.mask) {
                         const int8_t* ms = P.mask + ooff + n0;
@@ -316,7 +316,8 @@ __global__ __launch_bounds__(NTHREADS) void igemm_main(IgemmBatch batch, IgemmCt
     const int hint = st->bp_hint;
     begin_call(st, slot, hint);
     const Tile t = locate_tile(batch, blockIdx.x);
-    const RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
+    RoundK rk = make_round(hint < 0 ? 0 : hint, ctl.mode);
+    sr_key_current(rk, st);
     uint64_t tmax = 0;
     run_tile<TBM, TBN>(batch.p[t.prob], t.tm, t.tn, sm, rk, ctl.relu, hint >= 0, 1, tmax);
     __shared__ uint32_t red[NTHREADS / 64];
@@ -335,7 +336,8 @@ __global__ __launch_bounds__(NTHREADS) void igemm_fixup(IgemmBatch batch, IgemmC
     const int hint = cs.hint;
     const int bp = block_bp(cs.mx, ctl.target);
     if (bp != hint) {
-        const RoundK rk = make_round(bp, ctl.mode);
+        RoundK rk = make_round(bp, ctl.mode);
+        sr_key_recorded(rk, st);
         for (int tt = blockIdx.x; tt < batch.total_tiles; tt += gridDim.x) {
             const Tile t = locate_tile(batch, tt);
             uint64_t dummy = 0;
@@ -374,9 +376,12 @@ hipError_t launch_igemm(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
 namespace {
 
 hipError_t igemm_dispatch(IgemmBatch& b, IgemmCtl ctl, hipStream_t stream) {
-    if (igemm_small_eligible(b)) return igemm_small_run(b, ctl, stream);
-    if (igemm_wres_eligible(b)) return igemm_wres_run(b, ctl, stream);
-    if (igemm_dma_eligible(b)) return igemm_dma_run(b, ctl, stream);
+    // Stochastic rounding keys each draw by the element's offset in the
+    // output, which only this kernel's epilogue carries.
+    const bool sr = ctl.mode == NITI_ROUND_SR;
+    if (!sr && igemm_small_eligible(b)) return igemm_small_run(b, ctl, stream);
+    if (!sr && igemm_wres_eligible(b)) return igemm_wres_run(b, ctl, stream);
+    if (!sr && igemm_dma_eligible(b)) return igemm_dma_run(b, ctl, stream);
     // All problems of a batch share the tile shape; pick it from the largest.
     int maxM = 0, maxN = 0;
     for (int i = 0; i < b.nprob; i++) {

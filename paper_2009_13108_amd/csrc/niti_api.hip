@@ -35,7 +35,7 @@ inline niti_status hip_status(hipError_t e) { return e == hipSuccess ? NITI_OK :
 
 inline uint32_t acc_flags(int64_t red_len) { return red_len >= kAccBoundLen ? NITI_FLAG_ACC_BOUND : 0u; }
 
-bool valid_mode(niti_round_mode m) { return m == NITI_ROUND_PSR || m == NITI_ROUND_RTN; }
+bool valid_mode(niti_round_mode m) { return m == NITI_ROUND_PSR || m == NITI_ROUND_RTN || m == NITI_ROUND_SR; }
 
 // Geometry checks shared by the three convolution passes.
 niti_status check_conv(const niti_conv_desc* d, int64_t* P, int64_t* Q) {
@@ -288,7 +288,7 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
     p.ob = 0;
 
     const WinPlan wp = win_plan(d, P, Q);
-    if (wp.on) {
+    if (wp.on && mode != NITI_ROUND_SR) {
         // zero-padded input and window-extended filter rows in the workspace
         int8_t* xpad = (int8_t*)ws;
         int8_t* wr = xpad + wp.xpad_bytes;
@@ -608,12 +608,13 @@ niti_status niti_round_psr(const int32_t* x, int8_t* y, int64_t n, int bp, int t
         if (!stats) return NITI_ERR_NULL;
         if (target_bits < 1 || target_bits > 31) return NITI_ERR_ARG;
     }
+    if (mode == NITI_ROUND_SR && !stats) return NITI_ERR_NULL;   // the draws' seed and index
     hipStream_t strm = as_stream(stream);
     if (bp < 0) {
         hipError_t e = max_abs_i32(x, n, stats, strm);
         if (e != hipSuccess) return NITI_ERR_HIP;
     }
-    return hip_status(round_i32_run(x, y, n, bp, target_bits, mode, bp < 0 ? stats : nullptr,
+    return hip_status(round_i32_run(x, y, n, bp, target_bits, mode, (bp < 0 || mode == NITI_ROUND_SR) ? stats : nullptr,
                                     ExpArgs{s_in, nullptr, s_out}, strm));
 }
 

@@ -42,6 +42,9 @@ struct RoundK {
     uint64_t fmask;  // bp low bits
     uint64_t hmask;  // h low bits
     int rtn;         // 1: round to nearest instead
+    int sr;          // 1: stochastic rounding (draws keyed by sr_seed, sr_call, element index)
+    uint64_t sr_seed;
+    uint32_t sr_call;
     // Closed form of the 32-bit rounding (round_psr_mag_fast): with
     // r = (x >> odd) & hmask, the rounded value is (x + r * k1 + c0) >> bp.
     int32_t k1;      // -(2^h + 1) * 2^odd
@@ -56,6 +59,9 @@ __host__ __device__ inline RoundK make_round(int bp, int mode) {
     k.fmask = bp >= 64 ? ~0ull : ((1ull << bp) - 1ull);
     k.hmask = (1ull << k.h) - 1ull;
     k.rtn = mode == NITI_ROUND_RTN;
+    k.sr = mode == NITI_ROUND_SR;
+    k.sr_seed = 0;
+    k.sr_call = 0;
     k.k1 = k.h < 16 ? -(int32_t)(((1u << k.h) + 1u) << k.odd) : 0;
     k.c0 = k.h < 16 ? (int32_t)((((1u << (2 * k.h)) - (1u << k.h))) << k.odd) : 0;
     return k;
@@ -96,12 +102,41 @@ __device__ __forceinline__ uint64_t round_mag64(uint64_t x, const RoundK& k) {
     return q < 127ull ? q : 127ull;
 }
 
+// Stochastic rounding (Section 3.4): round the magnitude up with
+// probability f / 2^bp, the draw being output number call * 2^40 + idx + 1
+// of a SplitMix64 stream (Steele, Lea and Flood, "Fast splittable
+// pseudorandom number generators", OOPSLA 2014) seeded with seed.
+__device__ __forceinline__ uint64_t sr_draw(uint64_t seed, uint32_t call, uint64_t idx) {
+    uint64_t z = seed + ((((uint64_t)call) << 40) + idx + 1ull) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// |v| rounded with binary point bp <= 31: up exactly when the top bp bits of
+// the draw are below the fraction; held at 127.
+__device__ __forceinline__ uint32_t round_sr_mag32(uint32_t x, const RoundK& k, uint64_t idx) {
+    uint32_t q = x >> k.bp;
+    if (k.bp) {
+        const uint32_t f = x & ((1u << k.bp) - 1u);
+        q += (uint32_t)(sr_draw(k.sr_seed, k.sr_call, idx) >> (64 - k.bp)) < f ? 1u : 0u;
+    }
+    return q < 127u ? q : 127u;
+}
+
 __device__ __forceinline__ uint32_t mag32(int32_t v) {
     return v < 0 ? 0u - (uint32_t)v : (uint32_t)v;
 }
 
 __device__ __forceinline__ int8_t round_i32(int32_t v, const RoundK& k) {
     int32_t q = (int32_t)round_mag32(mag32(v), k);
+    return (int8_t)(v < 0 ? -q : q);
+}
+
+// round_i32 with the element index that keys a stochastic draw.
+__device__ __forceinline__ int8_t round_i32_at(int32_t v, const RoundK& k, uint64_t idx) {
+    if (!k.sr) return round_i32(v, k);
+    const int32_t q = (int32_t)round_sr_mag32(mag32(v), k, idx);
     return (int8_t)(v < 0 ? -q : q);
 }
 
@@ -327,6 +362,24 @@ __device__ __forceinline__ void begin_call(niti_stats* st, int slot, int hint) {
     if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) {
         st->cur = slot;
         st->hint_used = hint;
+        st->sr_call = st->calls;   // the draw index c of this call, for its later launches
+    }
+}
+
+// The stochastic-rounding key of the call in progress, for a launch after
+// the accumulating one (the finishing thread increments calls meanwhile, so
+// the index recorded by begin_call is read instead).
+__device__ __forceinline__ void sr_key_recorded(RoundK& k, const niti_stats* st) {
+    if (k.sr) {
+        k.sr_seed = st->sr_seed;
+        k.sr_call = st->sr_call;
+    }
+}
+// The same in the accumulating launch itself (calls does not change during it).
+__device__ __forceinline__ void sr_key_current(RoundK& k, const niti_stats* st) {
+    if (k.sr) {
+        k.sr_seed = st->sr_seed;
+        k.sr_call = st->calls;
     }
 }
 

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libniti.so")
 
 PSR = 0
 RTN = 1
+SR = 2
 
 FLAG_ACC_BOUND = 1
 FLAG_EXP_RANGE = 2
@@ -36,7 +37,7 @@ STATS_DTYPE = np.dtype([
     ("max_abs", "<u8"), ("b", "<i4"), ("bp", "<i4"), ("flags", "<i4"), ("s_out", "<i4"),
     ("bp_hint", "<i4"), ("calls", "<u4"), ("misses", "<u4"), ("reserved0", "<u4"),
     ("acc_max", "<u8", (2,)), ("wflags", "<u4", (2,)), ("cur", "<i4"), ("hint_used", "<i4"),
-    ("reserved", "<u4", (14,)),
+    ("sr_seed", "<u8"), ("sr_call", "<u4"), ("reserved", "<u4", (11,)),
 ])
 assert STATS_DTYPE.itemsize == STATS_BYTES
 
@@ -256,6 +257,21 @@ def new_stats(count: int = 1, device="cuda"):
     """Zero-filled niti_stats blocks (count x 128 bytes of device memory)."""
     torch = _torch()
     return torch.zeros((count, STATS_BYTES), dtype=torch.uint8, device=device)
+
+
+def set_sr_seed(stats, seed: int, index=None):
+    """Write the stochastic-rounding seed into stats blocks (all, or one)."""
+    torch = _torch()
+    val = int(seed) & 0xFFFFFFFFFFFFFFFF
+    if val >= 1 << 63:
+        val -= 1 << 64
+    v = torch.tensor([val], dtype=torch.int64).view(torch.uint8).to(stats.device)
+    off = STATS_DTYPE.fields["sr_seed"][1]
+    rows = stats.view(-1, STATS_BYTES)
+    if index is None:
+        rows[:, off:off + 8] = v
+    else:
+        rows[index, off:off + 8] = v
 
 
 def read_stats(stats):

@@ -468,3 +468,66 @@ def test_relu_mask_and_quantize():
     assert oracle.relu_mask(e, a).tolist() == [5, 0, 0, 9]
     px = np.arange(256, dtype=np.uint8)
     assert (oracle.quantize_u8(px) == (np.arange(256) // 2)).all()
+
+
+# ------------------------------------------------------------------ stochastic rounding (Sec 3.4, Rs)
+def test_sr_generator_is_splitmix64():
+    """The draws are the SplitMix64 stream: seed 0 gives the reference
+    implementation's first outputs, and the counter advances by one per
+    element and by 2^40 per call."""
+    assert [oracle.sr_draw(0, 0, i) for i in range(3)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4,
+                                                          0x06C45D188009454F]
+    assert oracle.sr_draw(0, 1, 0) == oracle.sr_draw(0, 0, 1 << 40)
+    assert oracle.sr_draw(5, 0, 0) != oracle.sr_draw(6, 0, 0)
+
+
+@pytest.mark.parametrize("bp", [1, 2, 3, 5, 8, 11])
+def test_sr_expectation_is_exact_over_all_draws(bp):
+    """Rs rounds up with probability f / 2^bp: over the 2^bp equally likely
+    values of the draw's top bits the outputs sum to exactly x (no clamp)."""
+    for x in (0, 1, 3, 1000, (1 << bp) - 1, 100 << bp, (127 << bp) - 1):
+        if (x >> bp) >= 127:
+            continue
+        for sign in (1, -1):
+            tot = sum(oracle.sr(sign * x, bp, r << (64 - bp)) for r in range(1 << bp))
+            assert tot == sign * x, (x, bp)
+
+
+def test_sr_is_unbiased_with_the_generator():
+    """With the generator's draws, the mean rounded value of many equal
+    inputs is x / 2^bp within a few standard errors (Section 3.4: zero
+    rounding bias)."""
+    x, bp, n = 1003, 5, 40000
+    out, _ = oracle.shift_round(np.full(n, x, np.int32), 7, oracle.SR, sr_seed=77)
+    # the block exponent of 1003 is b = 10, bp = 3 for target 7
+    assert int(np.abs(out).max()) <= (x >> 3) + 1
+    mean = out.astype(np.float64).mean()
+    p = (x & 7) / 8
+    assert abs(mean - x / 8) < 5 * math.sqrt(p * (1 - p) / n)
+    r = oracle.round_fixed(np.full(n, -x, np.int32), bp, oracle.SR, sr_seed=3, sr_call=2)
+    p = (x & 31) / 32
+    assert abs(r.astype(np.float64).mean() + x / 32) < 5 * math.sqrt(p * (1 - p) / n)
+
+
+def test_sr_tensor_rounding_uses_the_keyed_draws():
+    v = I.uniform_int(11, (3000,), -(1 << 20), 1 << 20, dtype=np.int32)
+    out, st = oracle.shift_round(v, 7, oracle.SR, sr_seed=12345, sr_call=9)
+    bp = st["bp"]
+    exp = [oracle.sr(int(a), bp, oracle.sr_draw(12345, 9, i)) for i, a in enumerate(v[:300])]
+    assert out[:300].tolist() == exp
+    out2, _ = oracle.shift_round(v, 7, oracle.SR, sr_seed=12345, sr_call=10)
+    assert (out2 != out).any()                          # another call, other draws
+    assert (np.abs(out2.astype(int) - out.astype(int)) <= 1).all()
+
+
+def test_sr_update_and_conv_follow_storage_order():
+    """The update's draws are keyed by the KRSC position of each weight."""
+    d = oracle.conv_desc(2, 4, 5, 5, 3, 3, 3, 1, 1)
+    x = I.activations(1, (2, 4, 5, 5)); dy = I.errors8(2, (2, 3, 5, 5)); w = I.weights(3, (3, 4, 3, 3))
+    w2, g32, st = oracle.conv_bwd_weight(d, x, dy, w, mu=5, mode=oracle.SR, sr_seed=1, sr_call=4)
+    bp = st["bp"]
+    krsc = np.ascontiguousarray(g32.transpose(0, 2, 3, 1)).reshape(-1)
+    wk = np.ascontiguousarray(w.transpose(0, 2, 3, 1)).reshape(-1)
+    exp = [max(-127, min(127, int(wk[i]) - oracle.sr(int(krsc[i]), bp, oracle.sr_draw(1, 4, i))))
+           for i in range(krsc.size)]
+    assert np.ascontiguousarray(w2.transpose(0, 2, 3, 1)).reshape(-1).tolist() == exp
