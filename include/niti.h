@@ -282,6 +282,21 @@ niti_status niti_maxpool2_bwd(const int8_t *dy, const uint8_t *idx, int8_t *dx, 
 /* Backward ReLU on an int8 error: e[i] = 0 where a[i] <= 0, in place. */
 niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
 
+/* Dropout (the VGG-small networks of Table 5 put it before their
+ * classifier; the paper gives no integer form): element i of x (n int8
+ * values, any layout) is kept when the top byte of draw (seed, call, i) of
+ * the stochastic-rounding generator (see Rounding above) is at least
+ * drop256, i.e. with probability 1 - drop256/256; y = x where kept, 0
+ * elsewhere; keep[i] = 1 / 0 records the choice.  The kept values are
+ * rescaled through the exponent: *s_y = *s_x + exp_add when both are given
+ * (drop256 = 128 with exp_add = 1 is the 1/(1 - p) = 2 of inverted dropout,
+ * exactly).  drop256 in 0..256, exp_add in -8..8. */
+niti_status niti_dropout_fwd(const int8_t *x, int8_t *y, uint8_t *keep, int64_t n, uint64_t seed,
+                             uint32_t call, int drop256, const int8_t *s_x, int8_t *s_y, int exp_add,
+                             void *stream);
+/* Backward of niti_dropout_fwd: dx = dy where keep, 0 elsewhere. */
+niti_status niti_dropout_bwd(const int8_t *dy, const uint8_t *keep, int8_t *dx, int64_t n, void *stream);
+
 /* Size of niti_stats (128), for bindings. */
 size_t niti_stats_bytes(void);
 

@@ -97,6 +97,8 @@ def _load():
                 "orc_maxpool2_fwd": (None, [P, I64, I64, I64, I64, P, P]),
                 "orc_maxpool2_bwd": (None, [P, P, I64, I64, I64, I64, P]),
                 "orc_quantize_u8": (None, [P, I64, P]),
+                "orc_dropout_fwd": (None, [P, P, I64, U64, U32, I, P, P]),
+                "orc_dropout_bwd": (None, [P, P, I64, P]),
             }
             for name, (res, args) in sig.items():
                 f = getattr(lib, name)
@@ -430,3 +432,24 @@ def quantize_u8(px):
     q = np.empty(px.shape, np.int8)
     _load().orc_quantize_u8(pp, px.size, _ptr(q))
     return q
+
+
+def dropout_fwd(x, seed: int, call: int, drop256: int = 128, nhwc=True):
+    """Dropout of an NCHW tensor (draws keyed by NHWC storage offsets when
+    nhwc, else by flat position).  Returns (y, keep)."""
+    x, px = _c(x, np.int8)
+    idx = nhwc_index(x.shape) if (nhwc and x.ndim == 4) else None
+    idx, pidx = _idx_ptr(idx)
+    y = np.empty(x.shape, np.int8)
+    keep = np.empty(x.shape, np.uint8)
+    _load().orc_dropout_fwd(px, pidx, x.size, int(seed) & 0xFFFFFFFFFFFFFFFF, int(call), int(drop256),
+                            _ptr(y), _ptr(keep))
+    return y, keep
+
+
+def dropout_bwd(dy, keep):
+    dy, pdy = _c(dy, np.int8)
+    keep, pk = _c(keep, np.uint8)
+    dx = np.empty(dy.shape, np.int8)
+    _load().orc_dropout_bwd(pdy, pk, dy.size, _ptr(dx))
+    return dx

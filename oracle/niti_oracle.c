@@ -706,3 +706,26 @@ void orc_quantize_u8(const uint8_t *px, int64_t n, int8_t *q)
     for (i = 0; i < n; i++)
         q[i] = (int8_t)(px[i] >> 1);
 }
+
+/* Dropout before a classifier (Table 5's VGG-small networks; reading in the
+ * design notes): element i, in the tensor's storage order, is kept when the
+ * top byte of draw (seed, call, i) is at least drop256; kept values pass
+ * unchanged (the caller moves the exponent), the others become 0.  The
+ * backward pass lets the error through where the element was kept. */
+void orc_dropout_fwd(const int8_t *x, const int64_t *idx, int64_t n, uint64_t seed, uint32_t call,
+                     int drop256, int8_t *y, uint8_t *keep)
+{
+    int64_t i;
+    for (i = 0; i < n; i++) {
+        const uint64_t r = orc_sr_draw(seed, call, (uint64_t)(idx ? idx[i] : i));
+        keep[i] = (uint8_t)((int)(r >> 56) >= drop256);
+        y[i] = keep[i] ? x[i] : 0;
+    }
+}
+
+void orc_dropout_bwd(const int8_t *dy, const uint8_t *keep, int64_t n, int8_t *dx)
+{
+    int64_t i;
+    for (i = 0; i < n; i++)
+        dx[i] = keep[i] ? dy[i] : 0;
+}

@@ -704,6 +704,28 @@ __global__ void relu_mask_kernel(int8_t* e, const int8_t* a, int64_t n) {
         if (a[i] <= 0) e[i] = 0;
 }
 
+// Dropout: element i is kept when the top byte of its draw (the stochastic
+// rounding generator, keyed by seed, call and i) is at least drop256.
+__global__ void dropout_fwd_kernel(const int8_t* x, int8_t* y, uint8_t* keep, int64_t n, uint64_t seed,
+                                   uint32_t call, uint32_t drop256, const int8_t* s_x, int8_t* s_y, int exp_add) {
+    if (s_x && blockIdx.x == 0 && threadIdx.x == 0) {
+        const int s = (int)*s_x + exp_add;
+        *s_y = (int8_t)(s > 127 ? 127 : (s < -128 ? -128 : s));
+    }
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const uint32_t k = (uint32_t)(sr_draw(seed, call, (uint64_t)i) >> 56) >= drop256 ? 1u : 0u;
+        keep[i] = (uint8_t)k;
+        y[i] = k ? x[i] : (int8_t)0;
+    }
+}
+
+__global__ void dropout_bwd_kernel(const int8_t* dy, const uint8_t* keep, int8_t* dx, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        dx[i] = keep[i] ? dy[i] : (int8_t)0;
+}
+
 }  // namespace
 
 hipError_t fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
@@ -899,6 +921,20 @@ hipError_t zero_classes_run(int8_t* out, int64_t n, int64_t h, int64_t w, int64_
 hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(relu_mask_kernel, dim3(grid_for(n, 4)), dim3(kThreads), 0, s, e, a, n);
+    return hipGetLastError();
+}
+
+hipError_t dropout_fwd_run(const int8_t* x, int8_t* y, uint8_t* keep, int64_t n, uint64_t seed, uint32_t call,
+                           uint32_t drop256, const int8_t* s_x, int8_t* s_y, int exp_add, hipStream_t s) {
+    if (n <= 0 && !s_x) return hipSuccess;
+    hipLaunchKernelGGL(dropout_fwd_kernel, dim3(grid_for(n > 0 ? n : 1, 4)), dim3(kThreads), 0, s, x, y, keep, n, seed,
+                       call, drop256, s_x, s_y, exp_add);
+    return hipGetLastError();
+}
+
+hipError_t dropout_bwd_run(const int8_t* dy, const uint8_t* keep, int8_t* dx, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dropout_bwd_kernel, dim3(grid_for(n, 4)), dim3(kThreads), 0, s, dy, keep, dx, n);
     return hipGetLastError();
 }
 

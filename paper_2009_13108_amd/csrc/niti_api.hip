@@ -671,6 +671,24 @@ niti_status niti_maxpool2_bwd(const int8_t* dy, const uint8_t* idx, int8_t* dx, 
     return hip_status(maxpool_bwd_run(dy, idx, dx, n, h, w, c, as_stream(stream)));
 }
 
+niti_status niti_dropout_fwd(const int8_t* x, int8_t* y, uint8_t* keep, int64_t n, uint64_t seed, uint32_t call,
+                             int drop256, const int8_t* s_x, int8_t* s_y, int exp_add, void* stream) {
+    if (n < 0) return NITI_ERR_SHAPE;
+    if ((!x || !y || !keep) && n > 0) return NITI_ERR_NULL;
+    if ((s_x == nullptr) != (s_y == nullptr)) return NITI_ERR_NULL;
+    if (drop256 < 0 || drop256 > 256 || exp_add < -8 || exp_add > 8) return NITI_ERR_ARG;
+    if (too_big(n)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(dropout_fwd_run(x, y, keep, n, seed, call, (uint32_t)drop256, s_x, s_y, exp_add,
+                                      as_stream(stream)));
+}
+
+niti_status niti_dropout_bwd(const int8_t* dy, const uint8_t* keep, int8_t* dx, int64_t n, void* stream) {
+    if (n < 0) return NITI_ERR_SHAPE;
+    if ((!dy || !keep || !dx) && n > 0) return NITI_ERR_NULL;
+    if (too_big(n)) return NITI_ERR_UNSUPPORTED;
+    return hip_status(dropout_bwd_run(dy, keep, dx, n, as_stream(stream)));
+}
+
 niti_status niti_relu_mask(int8_t* e, const int8_t* a, int64_t n, void* stream) {
     if (n < 0) return NITI_ERR_SHAPE;
     if ((!e || !a) && n > 0) return NITI_ERR_NULL;

@@ -159,6 +159,9 @@ hipError_t maxpool_fwd_run(const int8_t* x, int8_t* y, uint8_t* idx, int64_t n, 
 hipError_t maxpool_bwd_run(const int8_t* dy, const uint8_t* idx, int8_t* dx, int64_t n, int64_t h,
                            int64_t w, int64_t c, hipStream_t s);
 hipError_t relu_mask_run(int8_t* e, const int8_t* a, int64_t n, hipStream_t s);
+hipError_t dropout_fwd_run(const int8_t* x, int8_t* y, uint8_t* keep, int64_t n, uint64_t seed, uint32_t call,
+                           uint32_t drop256, const int8_t* s_x, int8_t* s_y, int exp_add, hipStream_t s);
+hipError_t dropout_bwd_run(const int8_t* dy, const uint8_t* keep, int8_t* dx, int64_t n, hipStream_t s);
 // Zero the pixels of out (NHWC, c % 4 == 0) whose sub-pixel class
 // (y % st, x % st) has bit (y % st) * st + x % st set in mask.
 hipError_t zero_classes_run(int8_t* out, int64_t n, int64_t h, int64_t w, int64_t c, int st, uint32_t mask,

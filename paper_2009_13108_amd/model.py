@@ -6,6 +6,9 @@ A network is a list of layer specs:
   ("fc",   n_in, n_out, relu)
   ("conv", c_in, c_out, ksize, stride, pad, relu)
   ("pool",)                                  2x2 stride-2 max pooling
+  ("dropout", drop256)                       dropout with probability drop256/256;
+                                             drop256 = 128 doubles the kept values
+                                             through the exponent (inverted dropout)
 Activations are NHWC int8 with one int8 exponent per tensor; a fully-
 connected layer after convolutions reads the NHWC tensor flattened in
 (h, w, c) order.  One training step (Algorithm 1):
@@ -17,6 +20,12 @@ connected layer after convolutions reads the NHWC tensor flattened in
            layer below is fused into that call), then the weight gradient is
            formed, shifted to mu bits and subtracted from the weights
            (Section 3.3).  The first layer's input error is not needed.
+Rounding: `mode` for activations and errors, `grad_mode` for the weight
+gradients (the paper's experiments round a and e to nearest and g with
+pseudo stochastic rounding, Section 4.3); `mu` may change from step to step
+(the schedule 5 -> 4 -> 3 of Section 4.3).  Stochastic rounding draws are
+keyed by each stats block's seed (sr_seed + block index) and call count;
+dropout draws by (drop_seed, step index, element).
 """
 from __future__ import annotations
 
@@ -31,7 +40,8 @@ def _i8(v):
 
 
 class IntNet:
-    def __init__(self, specs, in_shape, batch, weights, w_exps, mu=5, mode=niti.PSR):
+    def __init__(self, specs, in_shape, batch, weights, w_exps, mu=5, mode=niti.PSR, grad_mode=None, sr_seed=0,
+                 drop_seed=0):
         """in_shape = (h, w, c) of the NHWC input (c a multiple of 4 for convs);
         weights: list of int8 numpy arrays (KRSC for conv, [out][in] for fc),
         one per weighted layer; w_exps: their static exponents."""
@@ -40,6 +50,9 @@ class IntNet:
         self.batch = batch
         self.mu = mu
         self.mode = mode
+        self.grad_mode = mode if grad_mode is None else grad_mode
+        self.drop_seed = drop_seed
+        self.t = 0
         self.layers = []
         h, w, c = in_shape
         wi = 0
@@ -61,6 +74,8 @@ class IntNet:
             elif sp[0] == "pool":
                 L.update(kind="pool")
                 h, w = h // 2, w // 2
+            elif sp[0] == "dropout":
+                L.update(kind="dropout", drop256=sp[1])
             else:
                 raise ValueError(sp)
             L["out_shape"] = (h, w, c)
@@ -75,6 +90,8 @@ class IntNet:
         assert wi == len(weights)
         self.stats = niti.new_stats(nstats + 1)
         self.loss_stats = nstats
+        for i in range(nstats + 1):
+            niti.set_sr_seed(self.stats, sr_seed + i, index=i)
         # buffers
         for L in self.layers:
             oh, ow, oc = L["out_shape"]
@@ -83,6 +100,8 @@ class IntNet:
             L["e_in"] = torch.empty((batch,) + tuple(L["in_shape"]), dtype=torch.int8, device="cuda")
             if L["kind"] == "pool":
                 L["idx"] = torch.empty_like(L["y"], dtype=torch.uint8)
+            if L["kind"] == "dropout":
+                L["keep"] = torch.empty_like(L["y"], dtype=torch.uint8)
         ws = 0
         for L in self.layers:
             if L["kind"] in ("conv", "fc"):
@@ -106,15 +125,18 @@ class IntNet:
                 niti.gemm_fwd(a.view(self.batch, L["nin"]), L["w"], L["y"].view(self.batch, L["nout"]),
                               self.stats, s_a, L["s_w"], L["s_y"], 7, L["relu"], self.mode,
                               stats_index=L["stats"])
-            else:
+            elif k == "pool":
                 niti.maxpool2_fwd(a, L["y"], L["idx"])
                 L["s_y"] = s_a
+            else:
+                niti.dropout_fwd(a, L["y"], L["keep"], self.drop_seed, self.t, L["drop256"], s_a, L["s_y"],
+                                 1 if L["drop256"] == 128 else 0)
             L["x"] = a
             a, s_a = L["y"], L["s_y"]
         return a, s_a
 
     # -------------------------------------------------------------- backward
-    def backward(self, err):
+    def backward(self, err, mu):
         e = err.view(self.layers[-1]["y"].shape)
         for i in range(len(self.layers) - 1, -1, -1):
             L = self.layers[i]
@@ -125,8 +147,11 @@ class IntNet:
             mask = None
             if below is not None and below["kind"] in ("conv", "fc") and below["relu"]:
                 mask = L["x"]
-            if k == "pool":
-                niti.maxpool2_bwd(e, L["idx"], L["e_in"])
+            if k in ("pool", "dropout"):
+                if k == "pool":
+                    niti.maxpool2_bwd(e, L["idx"], L["e_in"])
+                else:
+                    niti.dropout_bwd(e, L["keep"], L["e_in"])
                 if below is not None and below["kind"] in ("conv", "fc") and below["relu"]:
                     niti.relu_mask(L["e_in"], below["y"])
                 e = L["e_in"]
@@ -144,25 +169,62 @@ class IntNet:
             if need_e_in:
                 niti.conv_bwd_data(d, e_v, w_v, ein_v, self.stats, self.ws, relu_src=m_v, mode=self.mode,
                                    stats_index=L["stats"] + 1)
-            niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws, mu=self.mu, mode=self.mode,
+            niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws, mu=mu, mode=self.grad_mode,
                                  stats_index=L["stats"] + 2)
             e = L["e_in"]
 
-    def step(self, x, s_x, labels):
-        """One training step; returns (logits, s_logits) of the forward pass."""
+    def step(self, x, s_x, labels, mu=None):
+        """One training step; returns (logits, s_logits) of the forward pass.
+        mu: this step's update width (default: the net's)."""
         logits, s_l = self.forward(x, s_x)
         n_cls = logits.shape[-1]
         niti.int_ce_loss_grad(logits.view(self.batch, n_cls), s_l, labels, self.err, self.stats, self.ws,
                               mode=self.mode, stats_index=self.loss_stats)
-        self.backward(self.err)
+        self.backward(self.err, self.mu if mu is None else mu)
+        self.t += 1
         return logits, s_l
 
     def weights(self):
         return [L["w"] for L in self.layers if L["kind"] in ("conv", "fc")]
 
 
+def mu_schedule(epoch, steps=((0, 5), (100, 4), (150, 3))):
+    """m_u of an epoch under the schedule of Section 4.3 (Tables 3 and 4):
+    5 bits, 4 from epoch 100, 3 from epoch 150."""
+    mu = steps[0][1]
+    for start, m in steps:
+        if epoch >= start:
+            mu = m
+    return mu
+
+
 # ------------------------------------------------------------------ workloads
 MLP_784 = [("fc", 784, 256, True), ("fc", 256, 128, True), ("fc", 128, 10, False)]
+
+# The paper's own networks (Section 4, Tables 5 and 6), on inputs with the
+# datasets' shapes.  The kernels need channel counts that are multiples of 4,
+# so an image's channels are padded with zeros (MNIST 1 -> 4, CIFAR10 3 -> 4)
+# and LeNet-5's six first-layer filters with two filters held at zero (their
+# outputs, errors and gradients stay zero, so the network is unchanged).
+LENET5 = [("conv", 4, 8, 5, 1, 2, True), ("pool",), ("conv", 8, 16, 5, 1, 0, True), ("pool",),
+          ("fc", 400, 120, True), ("fc", 120, 84, True), ("fc", 84, 10, False)]
+LENET5_REAL = {"image_channels": 1, "zero_filters": {0: (6, 8)}}
+
+
+def vgg_small(depth):
+    """VGG-small-7/8/9 of Table 5 on 32x32 inputs: 3x3 convolutions
+    128-128(-128), pool, 256-256(-256), pool, 512-512, pool, dropout, FC 10."""
+    assert depth in (7, 8, 9)
+    c1 = [128, 128] + ([128] if depth >= 8 else [])
+    c2 = [256, 256] + ([256] if depth >= 9 else [])
+    specs, cin = [], 4
+    for block in (c1, c2, [512, 512]):
+        for cout in block:
+            specs.append(("conv", cin, cout, 3, 1, 1, True))
+            cin = cout
+        specs.append(("pool",))
+    specs += [("dropout", 128), ("fc", 512 * 4 * 4, 10, False)]
+    return specs
 
 VGG_32 = [("conv", 4, 64, 3, 1, 1, True), ("conv", 64, 64, 3, 1, 1, True), ("pool",),
           ("conv", 64, 128, 3, 1, 1, True), ("conv", 128, 128, 3, 1, 1, True), ("pool",),
@@ -188,13 +250,17 @@ RESNET18_FC = (512, 1000)
 
 
 # ------------------------------------------------------------------ synthetic set-up
-def synthetic_weights(specs, in_channels, cfg, image_channels=None, first_id=10):
+def synthetic_weights(specs, in_channels, cfg, image_channels=None, first_id=10, zero_filters=None):
     """Seeded U[-127,127] weights in the library's layouts for a layer list:
     KRSC for convolutions (channels past image_channels of the first layer
     zero), [out][in] for fully-connected layers with the input read in
     (h, w, c) order; plus the static exponents (He-uniform style, from the
-    real fan-in).  Returns (weights as numpy arrays, exponents)."""
+    real fan-in).  zero_filters maps a convolution's index among the weighted
+    layers to a range [lo, hi) of its output filters held at zero, together
+    with the same input channels of the convolution after it.  Returns
+    (weights as numpy arrays, exponents)."""
     from . import inputs as I
+    zero_filters = zero_filters or {}
     ws, exps = [], []
     wi = 0
     for sp in specs:
@@ -205,6 +271,13 @@ def synthetic_weights(specs, in_channels, cfg, image_channels=None, first_id=10)
             if wi == 0 and image_channels is not None and image_channels < cin:
                 w[..., image_channels:] = 0
                 real = image_channels
+            if wi in zero_filters:
+                lo, hi = zero_filters[wi]
+                w[lo:hi] = 0
+            if wi - 1 in zero_filters:
+                lo, hi = zero_filters[wi - 1]
+                w[..., lo:hi] = 0
+                real = cin - (hi - lo)
             ws.append(w)
             exps.append(I.weight_exponent(real * k * k))
             wi += 1

@@ -85,7 +85,7 @@ EXPORTS = [
     "niti_conv_bwd_data_packed", "niti_conv_bwd_weight", "niti_conv_bwd_weight_noalloc",
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
-    "niti_relu_mask", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read", "niti_timing_record",
+    "niti_relu_mask", "niti_dropout_fwd", "niti_dropout_bwd", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read", "niti_timing_record",
 ]
 
 TIMING_IGEMM = 0
@@ -120,6 +120,8 @@ def lib():
                 "niti_maxpool2_fwd": [P, P, P, I64, I64, I64, I64, P],
                 "niti_maxpool2_bwd": [P, P, P, I64, I64, I64, I64, P],
                 "niti_relu_mask": [P, P, I64, P],
+                "niti_dropout_fwd": [P, P, P, I64, ctypes.c_uint64, ctypes.c_uint32, I, P, P, I, P],
+                "niti_dropout_bwd": [P, P, P, I64, P],
                 "niti_timing_enable": [I],
                 "niti_timing_read": [I, P, P],
                 "niti_timing_record": [I64, P, P, P],
@@ -467,3 +469,24 @@ def relu_mask(e, a, stream=None):
     if e.numel() != a.numel():
         raise ValueError("relu_mask: sizes differ")
     _run("niti_relu_mask", _ptr(e), _ptr(a), e.numel(), _stream(stream))
+
+
+def dropout_fwd(x, y, keep, seed: int, call: int, drop256: int = 128, s_x=None, s_y=None, exp_add: int = 0,
+                stream=None):
+    """y = x where the draw keeps the element (probability 1 - drop256/256),
+    else 0; *s_y = *s_x + exp_add when the exponents are given."""
+    torch = _torch()
+    _dev(x, torch.int8, "x"); _dev(y, torch.int8, "y"); _dev(keep, torch.uint8, "keep")
+    _dev(s_x, torch.int8, "s_x"); _dev(s_y, torch.int8, "s_y")
+    if not (x.numel() == y.numel() == keep.numel()):
+        raise ValueError("dropout_fwd: sizes differ")
+    _run("niti_dropout_fwd", _ptr(x), _ptr(y), _ptr(keep), x.numel(), int(seed) & 0xFFFFFFFFFFFFFFFF, int(call),
+         int(drop256), _ptr(s_x), _ptr(s_y), int(exp_add), _stream(stream))
+
+
+def dropout_bwd(dy, keep, dx, stream=None):
+    torch = _torch()
+    _dev(dy, torch.int8, "dy"); _dev(keep, torch.uint8, "keep"); _dev(dx, torch.int8, "dx")
+    if not (dy.numel() == dx.numel() == keep.numel()):
+        raise ValueError("dropout_bwd: sizes differ")
+    _run("niti_dropout_bwd", _ptr(dy), _ptr(keep), _ptr(dx), dy.numel(), _stream(stream))

@@ -154,7 +154,10 @@ def make_c3(batch=256):
             specs.append(("conv", cin) + tuple(sp[2:]))
             wi += 1
         elif sp[0] == "fc":
-            w_orc.append(I.weights(I.base_seed(3, 10 + wi), (sp[2], sp[1])))
+            # drawn as [out][(c, h, w)], stored as [out][(h, w, c)]: the order the
+            # oracle network flattens its input in
+            w = I.weights(I.base_seed(3, 10 + wi), (sp[2], sp[1]))
+            w_orc.append(np.ascontiguousarray(w.reshape(sp[2], 256, 4, 4).transpose(0, 2, 3, 1).reshape(sp[2], -1)))
             exps.append(I.weight_exponent(sp[1]))
             specs.append(sp)
             wi += 1
@@ -165,13 +168,11 @@ def make_c3(batch=256):
     logits, s = net.step(oracle.quantize_u8(px), -7, labels)
     rec = {"batch": batch, "steps": 1, "logits_sha256": sha(logits), "s_logits": int(s),
            "weights_sha256": []}
-    hw, c = 4, 256
     for li, w in enumerate(net.w):
         if w.ndim == 4:      # conv: KCRS -> KRSC, channels padded to 4 for the image layer
             rec["weights_sha256"].append(sha(nhwc(pad_c(w, 4 if li == 0 else w.shape[1]))))
-        else:                # fc: [out][(c,h,w)] -> [out][(h,w,c)]
-            rec["weights_sha256"].append(
-                sha(w.reshape(w.shape[0], c, hw, hw).transpose(0, 2, 3, 1).reshape(w.shape[0], -1)))
+        else:                # fc: [out][(h,w,c)], the library's order
+            rec["weights_sha256"].append(sha(w))
     print(rec, "%.1fs" % (time.time() - t0), flush=True)
     return rec
 

@@ -20,8 +20,8 @@ import alg1_bigint as R
 
 FC_NET = [("fc", 6, 5, True), ("fc", 5, 4, False)]
 CONV_NET = [("conv", 2, 3, 3, 1, 1, True), ("pool",), ("fc", 12, 4, False)]
-DEEP_NET = [("conv", 1, 2, 3, 2, 1, True), ("conv", 2, 3, 3, 1, 1, True), ("pool",), ("fc", 12, 3, True),
-            ("fc", 3, 2, False)]
+DEEP_NET = [("conv", 1, 2, 3, 2, 1, True), ("conv", 2, 3, 3, 1, 1, True), ("pool",), ("fc", 12, 6, True),
+            ("fc", 6, 2, False)]
 
 CASES = [
     # name, specs, input (c, h, w), batch, weight exponents, mu, mode, pixel range
@@ -33,7 +33,7 @@ CASES = [
     ("conv_pool_fc_taylor", CONV_NET, (2, 4, 4), 2, (-9, -11), 4, oracle.PSR, 127),
     ("conv_pool_fc_rtn", CONV_NET, (2, 4, 4), 3, (-6, -8), 1, oracle.RTN, 127),
     ("deep_strided", DEEP_NET, (1, 8, 8), 2, (-7, -7, -7, -7), 5, oracle.PSR, 127),
-    ("deep_small_pixels", DEEP_NET, (1, 8, 8), 2, (-5, -6, -7, -8), 5, oracle.PSR, 3),
+    ("deep_small_pixels", DEEP_NET, (1, 8, 8), 2, (-5, -6, -7, -8), 5, oracle.PSR, 9),
 ]
 
 
@@ -94,3 +94,87 @@ def test_reference_rounding_matches_worked_examples():
     ex = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "psr_examples.json")))
     for e in ex["cases"]:
         assert R.psr(e["x"], e["bp"]) == e["out"], e
+
+
+DROP_NET = [("conv", 2, 4, 3, 1, 1, True), ("pool",), ("dropout", 128), ("fc", 16, 4, False)]
+DROP_NET2 = [("conv", 2, 4, 3, 1, 1, True), ("conv", 4, 4, 3, 1, 1, True), ("pool",), ("dropout", 64),
+             ("fc", 16, 6, True), ("dropout", 128), ("fc", 6, 3, False)]
+
+EXT_CASES = [
+    # name, specs, input (c, h, w), batch, weight exponents, mu per step, mode, grad mode, sr seed, drop seed
+    ("rtn_ae_psr_g_schedule", CONV_NET, (2, 4, 4), 2, (-7, -7), (5, 4, 3), oracle.RTN, oracle.PSR, 0, 0),
+    ("rtn_ae_sr_g", FC_NET, (6, 1, 1), 3, (-7, -7), (5, 5, 4), oracle.RTN, oracle.SR, 101, 0),
+    ("sr_everywhere", CONV_NET, (2, 4, 4), 2, (-9, -11), (5, 4, 4), oracle.SR, oracle.SR, 7, 0),
+    ("sr_taylor", FC_NET, (6, 1, 1), 2, (-12, -12), (3, 3, 3), oracle.SR, oracle.SR, 2 ** 63 + 5, 0),
+    ("dropout", DROP_NET, (2, 4, 4), 2, (-7, -7), (5, 5, 5), oracle.PSR, oracle.PSR, 0, 13),
+    ("dropout_deep_sr", DROP_NET2, (2, 4, 4), 3, (-6, -7, -8, -7), (5, 4, 3), oracle.RTN, oracle.SR, 5, 99),
+]
+
+
+@pytest.mark.parametrize("case", EXT_CASES, ids=[c[0] for c in EXT_CASES])
+def test_oracle_step_options_match_bigint_algorithm1(case):
+    """The same pin for dropout layers, gradients rounded in another mode
+    than activations and errors, stochastic rounding keyed per statistics
+    block and step, and an update width that changes from step to step."""
+    name, specs, in_shape, batch, wexp, mus, mode, gmode, sr_seed, drop_seed = case
+    seed = 3500 + 19 * EXT_CASES.index(case)
+    ws, x, ncls = _init(specs, in_shape, batch, seed, 127)
+    net = OracleNet(specs, in_shape, batch, ws, wexp, mode=mode, grad_mode=gmode, sr_seed=sr_seed,
+                    drop_seed=drop_seed)
+    ref_w = [w.tolist() for w in ws]
+    rmode = {oracle.PSR: R.PSR, oracle.RTN: R.RTN, oracle.SR: R.SR}
+    for step, mu in enumerate(mus):
+        labels = I.labels(seed + 60 + step, batch, ncls)
+        lo, so = net.step(x, -7, labels, mu=mu)
+        lr, sr = R.train_step(specs, ref_w, list(wexp), x.tolist(), -7, [int(v) for v in labels], mu=mu,
+                              mode=rmode[mode], grad_mode=rmode[gmode], t=step, sr_seed=sr_seed,
+                              drop_seed=drop_seed)
+        assert so == sr, (step, so, sr)
+        assert np.array_equal(np.asarray(lo).reshape(batch, -1), np.array(lr).reshape(batch, -1)), step
+        for li, (wo, wr) in enumerate(zip(net.w, ref_w)):
+            assert np.array_equal(wo, np.array(wr, dtype=np.int8)), (step, li)
+    assert any(not np.array_equal(a, b) for a, b in zip(net.w, ws))
+
+
+def test_dropout_rate_and_exponent():
+    """Dropout keeps an element with probability 1 - drop256/256 and, at
+    rate 1/2, doubles the kept values through the exponent."""
+    x = np.full((4, 8, 16, 16), 9, np.int8)
+    for drop in (0, 64, 128, 192, 256):
+        y, keep = oracle.dropout_fwd(x, 77, 3, drop)
+        frac = keep.mean()
+        assert abs(frac - (1 - drop / 256)) < 0.03, (drop, frac)
+        assert ((y == 9) == (keep == 1)).all() and ((y == 0) == (keep == 0)).all()
+        assert (oracle.dropout_bwd(np.full(x.shape, -5, np.int8), keep) == np.where(keep == 1, -5, 0)).all()
+    net = OracleNet(DROP_NET, (2, 4, 4), 2, _init(DROP_NET, (2, 4, 4), 2, 7, 127)[0], (-7, -7), drop_seed=1)
+    net.step(_init(DROP_NET, (2, 4, 4), 2, 7, 127)[1], -7, np.array([0, 1], np.int32))
+    s_pool, s_drop = net.history[-1]["s"][1], net.history[-1]["s"][2]
+    assert s_drop == s_pool + 1
+
+
+def test_padded_lenet_filters_stay_zero_and_match_unpadded():
+    """LeNet-5's six first-layer filters are run as eight with two held at
+    zero (and the matching input channels of the next layer): after steps
+    of training the padded network's real weights equal those of the
+    six-filter network and the padding is still zero."""
+    from paper_2009_13108_amd import model as M
+    real = [("conv", 1, 6, 5, 1, 2, True), ("pool",), ("conv", 6, 16, 5, 1, 0, True), ("pool",),
+            ("fc", 400, 120, True), ("fc", 120, 84, True), ("fc", 84, 10, False)]
+    pad = [("conv", 1, 8, 5, 1, 2, True)] + M.LENET5[1:]
+    w_real = [I.weights(40 + i, s) for i, s in enumerate([(6, 1, 5, 5), (16, 6, 5, 5), (120, 400), (84, 120),
+                                                         (10, 84)])]
+    w_pad = [np.zeros((8, 1, 5, 5), np.int8), np.zeros((16, 8, 5, 5), np.int8)] + [w.copy() for w in w_real[2:]]
+    w_pad[0][:6] = w_real[0]
+    w_pad[1][:, :6] = w_real[1]
+    exps = (-6, -8, -9, -7, -7)
+    x = (I.activations(50, (4, 1, 28, 28)) // 2).astype(np.int8)
+    a = OracleNet(real, (1, 28, 28), 4, w_real, exps)
+    b = OracleNet(pad, (1, 28, 28), 4, w_pad, exps)
+    for step in range(2):
+        lab = I.labels(60 + step, 4, 10)
+        la, sa = a.step(x, -7, lab)
+        lb, sb = b.step(x, -7, lab)
+        assert sa == sb and (la == lb).all()
+    assert (b.w[0][:6] == a.w[0]).all() and not b.w[0][6:].any()
+    assert (b.w[1][:, :6] == a.w[1]).all() and not b.w[1][:, 6:].any()
+    assert all((p == q).all() for p, q in zip(a.w[2:], b.w[2:]))

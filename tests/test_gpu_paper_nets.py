@@ -1,0 +1,83 @@
+"""The paper's own networks (Section 4, Tables 5 and 6) trained step by step
+on the GPU against the oracle's composition, byte for byte: LeNet-5 on
+28x28x1 inputs and VGG-small-7/8/9 (with dropout before the classifier) on
+32x32x3 inputs, synthetic images and labels of the datasets' shapes.  Cases
+cover the paper's default rounding (a, e: nearest; g: pseudo stochastic),
+the m_u schedule 5 -> 4 -> 3, pseudo stochastic rounding everywhere and
+stochastic rounding for the gradients.  Image channels are padded with zeros
+to 4 on both sides (and LeNet-5's six first filters to eight, two held at
+zero), so that the stochastic draws, keyed by storage offset, agree."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle.model import OracleNet
+from paper_2009_13108_amd import inputs as I
+from paper_2009_13108_amd import model as M
+from paper_2009_13108_amd import niti
+from helpers import dev, host, kcrs, nchw, nhwc, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _orc_specs(specs):
+    return [("conv",) + tuple(sp[1:]) if sp[0] == "conv" else sp for sp in specs]
+
+
+def _setup(specs, hw, img_c, batch, cfg):
+    """Seeded pixels, labels and weights of a network in both layouts."""
+    px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hw, hw))
+    labels = I.labels(I.base_seed(cfg, 2), batch, 10)
+    zf = M.LENET5_REAL["zero_filters"] if specs is M.LENET5 else None
+    w_gpu, exps = M.synthetic_weights(specs, 4, cfg, image_channels=img_c, zero_filters=zf)
+    w_orc = [kcrs(w) if w.ndim == 4 else w.copy() for w in w_gpu]
+    x_orc = np.zeros((batch, 4, hw, hw), np.int8)
+    x_orc[:, :img_c] = oracle.quantize_u8(px)
+    return px, labels, w_gpu, w_orc, exps, x_orc
+
+
+CASES = [
+    # name, specs, image size, image channels, batch, steps (mu per step), mode, grad mode
+    ("lenet5_psr", M.LENET5, 28, 1, 16, (3, 3), oracle.PSR, oracle.PSR),
+    ("lenet5_paper_rounding", M.LENET5, 28, 1, 16, (3, 3, 3), oracle.RTN, oracle.PSR),
+    ("lenet5_sr_g", M.LENET5, 28, 1, 8, (3, 3), oracle.RTN, oracle.SR),
+    ("vgg_small7_psr", M.vgg_small(7), 32, 3, 4, (5, 5), oracle.PSR, oracle.PSR),
+    ("vgg_small7_schedule", M.vgg_small(7), 32, 3, 4, (5, 4, 3), oracle.RTN, oracle.PSR),
+    ("vgg_small7_sr", M.vgg_small(7), 32, 3, 2, (5, 4), oracle.SR, oracle.SR),
+    ("vgg_small8", M.vgg_small(8), 32, 3, 2, (5,), oracle.RTN, oracle.PSR),
+    ("vgg_small9", M.vgg_small(9), 32, 3, 2, (5,), oracle.RTN, oracle.PSR),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_paper_network_training_steps(case):
+    import torch
+    name, specs, hw, img_c, batch, mus, mode, gmode = case
+    say("paper net", name, batch, mus)
+    cfg = 20 + CASES.index(case)
+    px, labels, w_gpu, w_orc, exps, x_orc = _setup(specs, hw, img_c, batch, cfg)
+    seed, dseed = 1000 + cfg, 2000 + cfg
+    onet = OracleNet(_orc_specs(specs), (4, hw, hw), batch, w_orc, exps, mode=mode, grad_mode=gmode, sr_seed=seed,
+                     drop_seed=dseed)
+    gnet = M.IntNet(specs, (hw, hw, 4), batch, w_gpu, exps, mode=mode, grad_mode=gmode, sr_seed=seed,
+                    drop_seed=dseed)
+    x_g = torch.empty((batch, hw, hw, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(dev(px), x_g)
+    assert (nchw(host(x_g)) == x_orc).all()
+    lab = dev(labels)
+    s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+    w0 = [w.copy() for w in w_gpu]
+    for step, mu in enumerate(mus):
+        lo, so = onet.step(x_orc, -7, labels, mu=mu)
+        lg, sg = gnet.step(x_g, s0, lab, mu=mu)
+        torch.cuda.synchronize()
+        assert (host(lg).reshape(batch, -1) == lo).all(), "logits step %d" % step
+        assert int(host(sg)[0]) == so, "exponent step %d" % step
+        for li, (wg, wo) in enumerate(zip(gnet.weights(), onet.w)):
+            got = host(wg)
+            assert ((kcrs(got) if got.ndim == 4 else got) == wo).all(), "weights layer %d step %d" % (li, step)
+    moved = [not (host(a) == b).all() for a, b in zip(gnet.weights(), w0)]
+    assert any(moved)
+    if specs is M.LENET5:
+        got = [host(w) for w in gnet.weights()]
+        assert not got[0][6:].any() and not got[1][..., 6:].any()    # the padding filters stay zero

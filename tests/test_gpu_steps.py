@@ -110,10 +110,10 @@ def _vgg_setup(batch, cfg=3):
         elif sp[0] == "pool":
             hw //= 2
         else:
-            w = I.weights(I.base_seed(cfg, 10 + wi), (sp[2], sp[1]))  # [out][(c,h,w)]
-            w_orc.append(w)
-            w_gpu.append(np.ascontiguousarray(
-                w.reshape(sp[2], c_prev, hw, hw).transpose(0, 2, 3, 1).reshape(sp[2], -1)))
+            w = I.weights(I.base_seed(cfg, 10 + wi), (sp[2], sp[1]))  # drawn as [out][(c,h,w)]
+            w_hwc = np.ascontiguousarray(w.reshape(sp[2], c_prev, hw, hw).transpose(0, 2, 3, 1).reshape(sp[2], -1))
+            w_orc.append(w_hwc)         # both sides read the flattened input in (h, w, c) order
+            w_gpu.append(w_hwc.copy())
             exps.append(I.weight_exponent(sp[1]))
             wi += 1
     return px, labels, w_orc, w_gpu, exps
@@ -123,10 +123,6 @@ def _vgg_orc_specs():
     specs = list(M.VGG_32)
     specs[0] = ("conv", 3) + specs[0][2:]
     return specs
-
-
-def _gpu_fc_to_orc(w, c, hw):
-    return w.reshape(w.shape[0], hw, hw, c).transpose(0, 3, 1, 2).reshape(w.shape[0], -1)
 
 
 @pytest.mark.parametrize("batch,steps", [(8, 2), (3, 1)])
@@ -151,7 +147,7 @@ def test_config3_vgg_training_steps(batch, steps):
         for li in range(6):
             assert (kcrs(gw[li])[:, :w_orc[li].shape[1]] == onet.w[li]).all(), "conv %d step %d" % (li, step)
         assert (kcrs(gw[0])[:, 3] == 0).all()
-        assert (_gpu_fc_to_orc(gw[6], 256, 4) == onet.w[6]).all(), "fc step %d" % step
+        assert (gw[6] == onet.w[6]).all(), "fc step %d" % step
 
 
 def test_graph_replay_matches_eager():
