@@ -572,6 +572,105 @@ def small_configs(reps=50):
     return res
 
 
+def paper_nets(reps=10, batch=256):
+    """The paper's own networks (Section 4, Tables 5) as whole training
+    steps at batch 256 on synthetic inputs of the datasets' shapes (input
+    quantisation, forward, integer loss, backward and update; dropout before
+    VGG-small's classifier), each step's calls marshalled once and replayed."""
+    import torch
+    from paper_2009_13108_amd import inputs as I
+    from paper_2009_13108_amd import model as M
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    res = {}
+    nets = [("lenet5", M.LENET5, 28, 1, M.LENET5_REAL["zero_filters"])]
+    nets += [("vgg_small%d" % dd, M.vgg_small(dd), 32, 3, None) for dd in (7, 8, 9)]
+    for i, (name, specs, hw, img_c, zf) in enumerate(nets):
+        cfg = 40 + i
+        ws_, exps = M.synthetic_weights(specs, 4, cfg, image_channels=img_c, zero_filters=zf)
+        net = M.IntNet(specs, (hw, hw, 4), batch, ws_, exps, drop_seed=cfg)
+        px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hw, hw), device="cuda")
+        lab = I.labels(I.base_seed(cfg, 2), batch, 10, device="cuda")
+        xq = torch.empty((batch, hw, hw, 4), dtype=torch.int8, device="cuda")
+        s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+        with niti.recording() as calls:
+            niti.quantize_u8(px, xq)
+            net.step(xq, s0, lab)
+        ms = _replay_time(calls, reps)
+        ops = 2 * M.contraction_macs(specs, (hw, hw, 4), batch, img_c)
+        res[name] = {"batch": batch, "input": "%dx%dx%d" % (hw, hw, img_c), "us_per_step": round(ms * 1e3, 2),
+                     "tops": round(ops / (ms * 1e-3) / 1e12, 1), "ops_per_step": ops}
+        del net, calls
+    return res
+
+
+def alexnet_layers(reps=5, batch=128):
+    """AlexNet's contraction shapes (Table 6's network) at batch 128: per
+    layer the forward (exponent + rounding + ReLU fused), the
+    back-propagation (rounding and ReLU mask fused; not formed for the first
+    layer) and the weight gradient with its update."""
+    import torch
+    from paper_2009_13108_amd import inputs as I
+    from paper_2009_13108_amd import model as M
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    out = []
+    shapes = [(n, ci, co, k, st, pd, hw) for (n, ci, co, k, st, pd, hw) in M.ALEXNET_LAYERS]
+    shapes += [(n, fi, fo, 1, 1, 0, 1) for (n, fi, fo) in M.ALEXNET_FC]
+    for li, (name, cin, cout, k, st, pd, hw) in enumerate(shapes):
+        d = niti.ConvDesc.make(batch, hw, hw, cin, cout, k, k, st, pd)
+        x = I.activations(I.base_seed(8, 100 + li), d.x_shape(), device="cuda")
+        w = I.weights(I.base_seed(8, 200 + li), d.w_shape(), device="cuda")
+        c_real = cin
+        if li == 0:
+            x[..., 3:] = 0
+            w[..., 3:] = 0
+            c_real = 3
+        dy = I.errors8(I.base_seed(8, 300 + li), d.y_shape(), device="cuda")
+        y = torch.empty(d.y_shape(), dtype=torch.int8, device="cuda")
+        dx = torch.empty(d.x_shape(), dtype=torch.int8, device="cuda")
+        stats = niti.new_stats(3)
+        ws = niti.new_workspace(max(niti.workspace_bytes(op, d) for op in (1, 2, 3)))
+        passes = {"fwd": lambda: niti.conv_fwd(d, x, w, y, stats, relu=True, ws=ws, stats_index=0),
+                  "bwd_data": lambda: niti.conv_bwd_data(d, dy, w, dx, stats, ws, relu_src=x, stats_index=1),
+                  "bwd_weight+update": lambda: niti.conv_bwd_weight(d, x, dy, w, stats, ws, mu=5, stats_index=2)}
+        if li == 0:
+            del passes["bwd_data"]
+        macs = conv_macs(batch, c_real, hw, hw, cout, k, k, st, pd)
+        for pss, fn in passes.items():
+            with niti.recording() as calls:
+                fn()
+            ms = _replay_time(calls, reps)
+            tops = 2 * macs / (ms * 1e-3) / 1e12
+            out.append({"layer": name, "pass": pss, "us": round(ms * 1e3, 2), "tops": round(tops, 1),
+                        "frac": round(tops / PEAK_INT8_TOPS, 4)})
+        del x, w, dy, y, dx, ws
+    return out
+
+
+def mfma_loop_rate(iters=4096, per_cu=4, reps=5):
+    """The int8 MFMA loop (register operands, no memory traffic) over
+    256 x per_cu workgroups: the rate matrix work sustains on this device."""
+    import torch
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    wg = 256 * per_cu
+    out = torch.empty(wg * 256, dtype=torch.int32, device="cuda")
+    niti.mfma_loop(16, wg, out)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        niti.mfma_loop(iters, wg, out)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = sorted(times)[len(times) // 2]
+    ops = wg * 4 * iters * 8 * 65536
+    tops = ops / (ms * 1e-3) / 1e12
+    return {"workgroups": wg, "iters": iters, "us": round(ms * 1e3, 1), "tops": round(tops, 1),
+            "frac": round(tops / PEAK_INT8_TOPS, 4)}
+
+
 # RTX 3090 int8 times (ms) the paper's Table 7 reports for these shapes: context only.
 TABLE7_PAPER_3090_MS = {"a": {224: 3.928, 112: 1.006, 56: 0.289, 28: 0.089, 14: 0.038},
                         "e": {224: 4.731, 112: 1.269, 56: 0.453, 28: 0.185, 14: 0.117},
@@ -731,21 +830,46 @@ def summarize_kernel_trace(path):
 def summarize_counters(path):
     """Per-kernel averages of a rocprofv3 --pmc counter CSV (e.g. FETCH_SIZE
     or WRITE_SIZE in KiB per dispatch), labelled as above, plus the plain
-    copy kernel used for calibration."""
+    copy kernel used for calibration.  When the run collected
+    GRBM_GUI_ACTIVE with SQ_VALU_MFMA_BUSY_CYCLES (and optionally
+    SQ_INSTS_VALU_MFMA_MOPS_I8), also per kernel: the shader clock
+    (GRBM_GUI_ACTIVE is summed over the 8 XCDs, so cycles = value / 8, over
+    the dispatch's duration), the matrix cores' busy fraction (busy cycles
+    over 1024 SIMDs x cycles) and the int8 rate (MOPS_I8 counts units of
+    512 operations)."""
     import collections
     import csv
 
     per = collections.defaultdict(lambda: collections.defaultdict(float))
-    disp = collections.defaultdict(set)
+    disp = collections.defaultdict(dict)
     for r in csv.DictReader(open(path)):
         name = r["Kernel_Name"]
         lab = kernel_label(name) if "niti::" in name else name[:60]
         per[r["Counter_Name"]][lab] += float(r["Counter_Value"])
-        disp[lab].add(r["Dispatch_Id"])
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 if "End_Timestamp" in r else 0.0
+        disp[lab][r["Dispatch_Id"]] = dur
     for cname, vals in per.items():
         for lab, v in sorted(vals.items(), key=lambda kv: -kv[1]):
             n = len(disp[lab])
             print("%s %-60s launches %6d per launch %14.1f" % (cname, lab, n, v / n))
+    grbm, busy = per.get("GRBM_GUI_ACTIVE"), per.get("SQ_VALU_MFMA_BUSY_CYCLES")
+    if not grbm or not busy:
+        return
+    mops = per.get("SQ_INSTS_VALU_MFMA_MOPS_I8", {})
+    print()
+    print("%-48s %7s %9s %6s %7s %8s" % ("kernel", "calls", "avg_us", "GHz", "mfma%", "int8TOPS"))
+    rows = []
+    for lab in grbm:
+        n = len(disp[lab])
+        us = sum(disp[lab].values()) / n
+        cyc = grbm[lab] / 8.0 / n
+        if cyc <= 0 or us <= 0:
+            continue
+        util = busy.get(lab, 0.0) / n / (cyc * 1024.0)
+        tops = mops.get(lab, 0.0) * 512.0 / n / (us * 1e-6) / 1e12
+        rows.append((us * n, lab, n, us, cyc / us / 1e3, 100.0 * util, tops))
+    for _, lab, n, us, ghz, util, tops in sorted(rows, reverse=True):
+        print("%-48s %7d %9.2f %6.2f %7.1f %8.1f" % (lab[:48], n, us, ghz, util, tops))
 
 
 def copy_calibration(nbytes):
@@ -770,8 +894,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=64)
     ap.add_argument("--no-configs", action="store_true",
-                    help="skip configs 1-3, the config-5 GEMM sweep and the Table 7 shapes")
-    ap.add_argument("--only", choices=("c5", "small", "table7"),
+                    help="skip configs 1-3, the config-5 GEMM sweep, the Table 7 shapes, the paper networks and the AlexNet layers")
+    ap.add_argument("--only", choices=("c5", "small", "table7", "paper_nets", "alexnet", "mfma_loop"),
                     help="run only the config-5 sweep, configs 1-3 or the Table 7 shapes and print their JSON "
                          "(for profiling one workload)")
     ap.add_argument("--c5-sizes", default="4096,8192,16384", help="sizes of the --only c5 sweep")
@@ -806,6 +930,12 @@ def main():
             res = c5_sweep(sizes=tuple(int(v) for v in args.c5_sizes.split(",")))
         elif args.only == "small":
             res = small_configs()
+        elif args.only == "paper_nets":
+            res = paper_nets()
+        elif args.only == "alexnet":
+            res = alexnet_layers()
+        elif args.only == "mfma_loop":
+            res = mfma_loop_rate()
         else:
             res = table7()
         print(json.dumps({"only": args.only, "result": res}), flush=True)
@@ -859,6 +989,10 @@ def main():
     value = job.ops_per_step / (ms * 1e-3) / 1e12
     fam = ser["families"]
 
+    # the matrix cores' sustained int8 rate with no memory traffic (context
+    # for the roofline fraction, which stays against the published peak)
+    loop = mfma_loop_rate()
+
     extra = {}
     if not args.no_configs:
         print("[bench] configs 1-3", file=sys.stderr, flush=True)
@@ -867,6 +1001,10 @@ def main():
         extra["c5"] = c5_sweep()
         print("[bench] paper Table 7 shapes", file=sys.stderr, flush=True)
         extra["table7_context"] = table7()
+        print("[bench] paper networks", file=sys.stderr, flush=True)
+        extra["paper_nets"] = paper_nets()
+        print("[bench] AlexNet layer shapes", file=sys.stderr, flush=True)
+        extra["alexnet_layers"] = alexnet_layers()
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -918,6 +1056,7 @@ def main():
                      "family_ms_per_step": {f: round(v[1] / args.steps, 4) for f, v in fam.items()}},
         "passes": passes,
         "c4_layers": c4_layer_table(ser),
+        "mfma_loop": loop,
         "cpu_baseline": cpu,
     }
     for k in ("c1", "c2", "c3"):
@@ -928,8 +1067,9 @@ def main():
         big = [r for r in c5 if r["M"] == r["N"] == r["K"]]
         out["c5_square_frac"] = {"%s_%d" % (r["dist"], r["M"]): r["frac"] for r in big}
         out["c5_best_frac"] = max(r["frac"] for r in c5)
-    if "table7_context" in extra:
-        out["table7_context"] = extra["table7_context"]
+    for k in ("table7_context", "paper_nets", "alexnet_layers"):
+        if k in extra:
+            out[k] = extra[k]
     print(json.dumps(out), flush=True)
 
 

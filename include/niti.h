@@ -116,7 +116,12 @@ typedef struct niti_stats {
 
 /* Convolution geometry.  Input x is NHWC [n][h][w][c]; filter is KRSC
  * [k][r][s][c]; output is NHWC [n][p][q][k] with
- * p = (h + 2 pad_h - r) / stride_h + 1 and q = (w + 2 pad_w - s) / stride_w + 1. */
+ * p = (h + 2 pad_h - r) / stride_h + 1 and q = (w + 2 pad_w - s) / stride_w + 1.
+ * The kernels take stride_h == stride_w, at most 8 for the forward pass and
+ * the weight gradient and at most 2 for the back-propagation (a strided first
+ * layer, such as AlexNet's 11 x 11 stride-4 one, forms no input error in
+ * Algorithm 1); other strides return NITI_ERR_UNSUPPORTED, and
+ * niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, ...) is then 0. */
 typedef struct niti_conv_desc {
     int64_t n, h, w, c;
     int64_t k, r, s;
@@ -332,6 +337,16 @@ enum {
 niti_status niti_timing_enable(int on);
 niti_status niti_timing_read(int family, double *ms, int64_t *calls);
 niti_status niti_timing_record(int64_t i, int *family, const char **name, double *ms);
+
+/* ---- Matrix-core rate check (a measurement aid; no part of the method) ----
+ * Runs `workgroups` workgroups of four waves; each wave issues iters x 8
+ * int8 MFMAs (32x32x32: 65536 integer operations each) on register operands
+ * in eight independent accumulator chains, then writes one int32 per lane
+ * to out[workgroup * 256 + lane] (device, caller-owned, at least
+ * workgroups * 256 elements).  Its rate is what int8 matrix work sustains
+ * on this device with no memory traffic.  NITI_ERR_SHAPE for iters < 0 or
+ * workgroups outside 1..2^20. */
+niti_status niti_mfma_loop(int64_t iters, int64_t workgroups, int32_t *out, void *stream);
 
 #ifdef __cplusplus
 }

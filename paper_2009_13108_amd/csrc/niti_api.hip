@@ -49,7 +49,7 @@ niti_status check_conv(const niti_conv_desc* d, int64_t* P, int64_t* Q) {
     *P = p / d->stride_h + 1;
     *Q = q / d->stride_w + 1;
     if (d->c % 4 != 0) return NITI_ERR_UNSUPPORTED;
-    if (d->stride_h != d->stride_w || d->stride_h > 2) return NITI_ERR_UNSUPPORTED;
+    if (d->stride_h != d->stride_w || d->stride_h > kMaxConvStride) return NITI_ERR_UNSUPPORTED;
     if (too_big(d->n * d->h * d->w * d->c) || too_big(d->n * *P * *Q * d->k) ||
         too_big(d->k * d->r * d->s * d->c) || too_big(d->k * d->r * d->s * d->c * 4))
         return NITI_ERR_UNSUPPORTED;
@@ -181,6 +181,7 @@ size_t niti_workspace_bytes(int op, const niti_conv_desc* d, int64_t M, int64_t 
             return w.on ? (size_t)(w.xpad_bytes + w.wr_bytes) : 0;
         }
         case NITI_OP_CONV_BWD_DATA:
+            if (d->stride_h > kMaxDgradStride) return 0;
             return (size_t)round_up(d->k * d->r * d->s * d->c, 256);
         case NITI_OP_CONV_BWD_WEIGHT: {
             const int64_t nw = d->k * d->r * d->s * d->c;
@@ -447,6 +448,7 @@ niti_status check_dgrad(const niti_conv_desc* d, const int8_t* dy, const void* p
     if (!valid_mode(mode)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, P, Q);
     if (s != NITI_OK) return s;
+    if (d->stride_h > kMaxDgradStride) return NITI_ERR_UNSUPPORTED;
     if (packed_bytes < niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0)) return NITI_ERR_WORKSPACE;
     return NITI_OK;
 }
@@ -463,6 +465,7 @@ niti_status niti_conv_bwd_data(const niti_conv_desc* d, const int8_t* dy, const 
     if (!valid_mode(mode)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
+    if (d->stride_h > kMaxDgradStride) return NITI_ERR_UNSUPPORTED;
     const size_t need = niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0);
     if (!ws || ws_bytes < need) return NITI_ERR_WORKSPACE;
     DgradPlan pl;
@@ -479,6 +482,7 @@ niti_status niti_conv_pack_bwd_data(const niti_conv_desc* d, const int8_t* w, vo
     if (mis16(w) || mis16(packed)) return NITI_ERR_ARG;
     niti_status s = check_conv(d, &P, &Q);
     if (s != NITI_OK) return s;
+    if (d->stride_h > kMaxDgradStride) return NITI_ERR_UNSUPPORTED;
     if (packed_bytes < niti_workspace_bytes(NITI_OP_CONV_BWD_DATA, d, 0, 0, 0)) return NITI_ERR_WORKSPACE;
     DgradPlan pl;
     plan_dgrad(d, P, Q, nullptr, (const int8_t*)packed, nullptr, nullptr, pl);

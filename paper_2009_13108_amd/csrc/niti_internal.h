@@ -7,6 +7,8 @@
 namespace niti {
 
 constexpr int kMaxProblems = 4;   // sub-pixel classes of a stride-2 back-propagation
+constexpr int kMaxDgradStride = 2;  // back-propagation: stride^2 classes <= kMaxProblems
+constexpr int kMaxConvStride = 8;   // forward and weight gradient
 constexpr int kFixupGrid = 256;   // workgroups of the fix-up launch (one per compute unit)
 
 // One implicit-GEMM problem (see igemm.hip for the index form).

@@ -1,6 +1,6 @@
 // Kernel timing hooks: HIP event pairs recorded on a call's stream around
-// its launches, summed per family or read one by one on request.  Host code
-// only.
+// its launches, summed per family or read one by one on request; and the
+// int8 MFMA loop that measures the matrix cores' sustained rate.
 #include <stdarg.h>
 #include <stdio.h>
 
@@ -111,6 +111,47 @@ niti_status niti_timing_record(int64_t i, int* family, const char** name, double
     if (hipEventElapsedTime(&t, g_pool[i].a, g_pool[i].b) != hipSuccess) return NITI_ERR_HIP;
     *ms = t;
     return NITI_OK;
+}
+
+}  // extern "C"
+
+namespace niti {
+namespace {
+
+// Eight independent 32x32x32 int8 MFMA chains per wave on register operands,
+// `iters` rounds; the accumulators are summed into one word per lane so the
+// work is kept.  Four waves per workgroup, one per SIMD.
+__global__ __launch_bounds__(256) void mfma_loop_kernel(int64_t iters, int32_t* out, int64_t n_out) {
+    const int t = (int)threadIdx.x;
+    const v4i a = {t, 3 * t + 1, 5 * t + 2, 7 * t + 3};
+    const v4i b = {11 * t + 4, 13 * t + 5, 17 * t + 6, 19 * t + 7};
+    v16i acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) acc[j] = v16i{};
+    for (int64_t i = 0; i < iters; i++) {
+#pragma unroll
+        for (int j = 0; j < 8; j++) acc[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[j], 0, 0, 0);
+    }
+    int32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+#pragma unroll
+        for (int e = 0; e < 16; e++) s += acc[j][e];
+    const int64_t o = (int64_t)blockIdx.x * 256 + t;
+    if (o < n_out) out[o] = s;
+}
+
+}  // namespace
+}  // namespace niti
+
+extern "C" {
+
+niti_status niti_mfma_loop(int64_t iters, int64_t workgroups, int32_t* out, void* stream) {
+    if (!out) return NITI_ERR_NULL;
+    if (iters < 0 || workgroups < 1 || workgroups > (1 << 20)) return NITI_ERR_SHAPE;
+    hipLaunchKernelGGL(niti::mfma_loop_kernel, dim3((unsigned)workgroups), dim3(256), 0, (hipStream_t)stream, iters,
+                       out, workgroups * 256);
+    return hipGetLastError() == hipSuccess ? NITI_OK : NITI_ERR_HIP;
 }
 
 }  // extern "C"

@@ -248,6 +248,20 @@ RESNET18_LAYERS = [
 ]
 RESNET18_FC = (512, 1000)
 
+# AlexNet on 224x224 ImageNet-shaped inputs (the network of the paper's
+# Table 6, 62.38M parameters: no channel groups): the contraction layers as
+# (name, c_in, c_out, ksize, stride, pad, input size).  Its 3x3 stride-2
+# overlapping max pools sit between them (55 -> 27 -> 13 -> 6); the image's
+# three channels are padded to 4.
+ALEXNET_LAYERS = [
+    ("conv1_11x11s4", 4, 96, 11, 4, 2, 224),
+    ("conv2_5x5", 96, 256, 5, 1, 2, 27),
+    ("conv3_3x3", 256, 384, 3, 1, 1, 13),
+    ("conv4_3x3", 384, 384, 3, 1, 1, 13),
+    ("conv5_3x3", 384, 256, 3, 1, 1, 13),
+]
+ALEXNET_FC = [("fc6", 256 * 6 * 6, 4096), ("fc7", 4096, 4096), ("fc8", 4096, 1000)]
+
 
 # ------------------------------------------------------------------ synthetic set-up
 def synthetic_weights(specs, in_channels, cfg, image_channels=None, first_id=10, zero_filters=None):

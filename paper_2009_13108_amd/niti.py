@@ -86,6 +86,7 @@ EXPORTS = [
     "niti_round_psr", "niti_int_ce_loss_grad", "niti_sgd_update", "niti_workspace_bytes",
     "niti_status_str", "niti_quantize_u8", "niti_maxpool2_fwd", "niti_maxpool2_bwd",
     "niti_relu_mask", "niti_dropout_fwd", "niti_dropout_bwd", "niti_stats_bytes", "niti_timing_enable", "niti_timing_read", "niti_timing_record",
+    "niti_mfma_loop",
 ]
 
 TIMING_IGEMM = 0
@@ -125,6 +126,7 @@ def lib():
                 "niti_timing_enable": [I],
                 "niti_timing_read": [I, P, P],
                 "niti_timing_record": [I64, P, P, P],
+                "niti_mfma_loop": [I64, I64, P, P],
             }
             for name, args in sig.items():
                 f = getattr(L, name)
@@ -156,6 +158,17 @@ def timing_read(family: int):
     n = ctypes.c_int64(0)
     _check(lib().niti_timing_read(int(family), ctypes.byref(ms), ctypes.byref(n)), "niti_timing_read")
     return ms.value, n.value
+
+
+def mfma_loop(iters, workgroups, out, stream=None):
+    """Matrix-core rate check: workgroups x 4 waves x iters x 8 int8 MFMAs
+    of 65536 operations; out is an int32 device tensor of at least
+    workgroups * 256 elements."""
+    torch = _torch()
+    _dev(out, torch.int32, "out")
+    if out.numel() < workgroups * 256:
+        raise ValueError("mfma_loop: out too small")
+    _run("niti_mfma_loop", int(iters), int(workgroups), _ptr(out), _stream(stream))
 
 
 def timing_records():

@@ -70,8 +70,15 @@ def test_conv_rejects_on_host():
     L = niti.lib()
     d = niti.ConvDesc.make(2, 8, 8, 3, 16, 3, 3, 1, 1)           # c % 4 != 0
     assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -3
-    d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 3, 1)           # stride 3
+    d = niti.ConvDesc.make(2, 32, 32, 4, 16, 3, 3, 9, 1)         # stride 9
     assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -3
+    assert L.niti_conv_bwd_weight(ctypes.byref(d), FAKE, FAKE, FAKE, None, 5, 0, FAKE, FAKE, 1 << 20, None) == -3
+    d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 3, 1)           # stride 3: no back-propagation
+    assert L.niti_workspace_bytes(niti.OP_CONV_BWD_DATA, ctypes.byref(d), 0, 0, 0) == 0
+    assert L.niti_conv_bwd_data(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, 1 << 20, None) == -3
+    assert L.niti_conv_pack_bwd_data(ctypes.byref(d), FAKE, FAKE, 1 << 20, None) == -3
+    assert L.niti_conv_bwd_data_packed(ctypes.byref(d), FAKE, FAKE, FAKE, None, 0, FAKE, 1 << 20, None) == -3
+    assert L.niti_workspace_bytes(niti.OP_CONV_FWD, ctypes.byref(d), 0, 0, 0) > 0   # few channels: window copy
     d = niti.ConvDesc.make(2, 2, 2, 4, 16, 5, 5, 1, 0)           # filter larger than padded input
     assert L.niti_conv_fwd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, 0, 0, FAKE, None, 0, None) == -2
     d = niti.ConvDesc.make(2, 8, 8, 4, 16, 3, 3, 1, 1)

@@ -242,6 +242,41 @@ def test_conv_bwd_weight_parity(case, mu):
     assert (kcrs(host(w2)) == exp_w).all()
 
 
+STRIDE_CASES = [
+    # n, c, h, w, k, r, s, stride, pad, relu: strides above 2 (forward and
+    # weight gradient only), few channels (window copy) and 64 channels
+    (2, 4, 31, 29, 32, 11, 11, 4, 2, True),
+    (2, 8, 17, 17, 16, 5, 5, 3, 1, False),
+    (2, 64, 15, 13, 64, 3, 3, 3, 1, True),
+    (1, 128, 16, 16, 96, 3, 3, 4, 0, False),
+    (3, 64, 9, 9, 40, 1, 1, 8, 0, True),
+]
+
+
+@pytest.mark.parametrize("case", STRIDE_CASES)
+def test_conv_large_stride_parity(case):
+    import torch
+    say("conv large stride", case)
+    d, gd, x, wt, dy = _conv_inputs(case, 11 * case[2] + case[7])
+    relu = case[-1]
+    y_o, _, st_f = oracle.conv_fwd(d, x, wt, relu=relu)
+    w_o, g_o, st_w = oracle.conv_bwd_weight(d, x, dy, wt, mu=5)
+    y = torch.empty(gd.y_shape(), dtype=torch.int8, device="cuda")
+    stats = niti.new_stats(2)
+    ws = niti.new_workspace(max(16, niti.workspace_bytes(niti.OP_CONV_FWD, gd),
+                                niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gd)))
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_DATA, gd) == 0
+    niti.conv_fwd(gd, dev(nhwc(x)), dev(krsc(wt)), y, stats, relu=relu, ws=ws, stats_index=0)
+    w_dev = dev(krsc(wt))
+    g32 = torch.empty(gd.w_shape(), dtype=torch.int32, device="cuda")
+    niti.conv_bwd_weight(gd, dev(nhwc(x)), dev(nhwc(dy)), w_dev, stats, ws, g32_out=g32, mu=5, stats_index=1)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)
+    assert (nchw(host(y)) == y_o).all() and same_stats(g[0], st_f)
+    assert (kcrs(host(g32)) == g_o).all()
+    assert (kcrs(host(w_dev)) == w_o).all() and same_stats(g[1], st_w)
+
+
 @pytest.mark.parametrize("n", [0, 1, 5, 1000, 65537])
 def test_round_psr_parity(n):
     import torch

@@ -81,3 +81,57 @@ def test_paper_network_training_steps(case):
     if specs is M.LENET5:
         got = [host(w) for w in gnet.weights()]
         assert not got[0][6:].any() and not got[1][..., 6:].any()    # the padding filters stay zero
+
+
+ALEX = [(n, ci, co, k, st, pd, hw, 2) for (n, ci, co, k, st, pd, hw) in M.ALEXNET_LAYERS]
+ALEX += [(n, fi, fo, 1, 1, 0, 1, 4) for (n, fi, fo) in M.ALEXNET_FC]
+
+
+@pytest.mark.parametrize("layer", ALEX, ids=[a[0] for a in ALEX])
+def test_alexnet_layer_shapes(layer):
+    """AlexNet's contraction shapes (Table 6's network), each layer's three
+    contractions with their fused epilogues, element by element and with the
+    statistics, at a small batch; weights and errors with the first layer's
+    padding channel held at zero."""
+    import torch
+    from helpers import krsc, same_stats
+    name, cin, cout, k, st, pd, hw, n = layer
+    say("alexnet", name, n)
+    seed = 300 + 10 * ALEX.index(layer)
+    d = oracle.conv_desc(n, cin, hw, hw, cout, k, k, st, pd)
+    P, Q = oracle.conv_out_hw(d)
+    x = I.activations(seed + 1, (n, cin, hw, hw))
+    wt = I.weights(seed + 2, (cout, cin, k, k))
+    dy = I.errors8(seed + 3, (n, cout, P, Q))
+    if cin == 4:
+        x[:, 3:] = 0
+        wt[:, 3:] = 0
+    gd = niti.ConvDesc.make(n, hw, hw, cin, cout, k, k, st, pd)
+    ws = niti.new_workspace(max(niti.workspace_bytes(op, gd) for op in (1, 2, 3)))
+    stats = niti.new_stats(3)
+    xs, wd, dyd = dev(nhwc(x)), dev(krsc(wt)), dev(nhwc(dy))
+    # forward
+    y_o, _, st_f = oracle.conv_fwd(d, x, wt, relu=True)
+    y = torch.empty(gd.y_shape(), dtype=torch.int8, device="cuda")
+    niti.conv_fwd(gd, xs, wd, y, stats, relu=True, ws=ws, stats_index=0)
+    # back-propagation, masked by the ReLU of the layer below (not formed
+    # for the stride-4 first layer: the library rejects it)
+    dx = torch.empty(gd.x_shape(), dtype=torch.int8, device="cuda")
+    if st > 2:
+        with pytest.raises(niti.NitiError) as ei:
+            niti.conv_bwd_data(gd, dyd, wd, dx, stats, ws, relu_src=xs, stats_index=1)
+        assert ei.value.status == -3
+    else:
+        dx_o, _, st_d = oracle.conv_bwd_data(d, dy, wt, relu_src=x)
+        niti.conv_bwd_data(gd, dyd, wd, dx, stats, ws, relu_src=xs, stats_index=1)
+    # weight gradient and update
+    w_o, g_o, st_w = oracle.conv_bwd_weight(d, x, dy, wt, mu=5)
+    g32 = torch.empty(gd.w_shape(), dtype=torch.int32, device="cuda")
+    niti.conv_bwd_weight(gd, xs, dyd, wd, stats, ws, g32_out=g32, mu=5, stats_index=2)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)
+    assert (nchw(host(y)) == y_o).all() and same_stats(g[0], st_f)
+    if st <= 2:
+        assert (nchw(host(dx)) == dx_o).all() and same_stats(g[1], st_d)
+    assert (kcrs(host(g32)) == g_o).all()
+    assert (kcrs(host(wd)) == w_o).all() and same_stats(g[2], st_w)
