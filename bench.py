@@ -423,10 +423,11 @@ def measure_serial(job, steps):
             passes["loss"][2] += job.batch * job.fc_desc.k * (1 + 16 + 16 + 1) + 4 * job.batch
             call_ms = c["ms"]
         else:
-            k = kern.setdefault(c["kernel"], [0, 0.0, 0])
+            k = kern.setdefault(c["kernel"], [0, 0.0, 0, 0])
             k[0] += 1
             k[1] += c["kernel_ms"]
             k[2] += ops
+            k[3] += nbytes
             f = fam["wgrad" if pss == "wgrad" else "igemm"]
             f[0] += 1
             f[1] += c["ms"]
@@ -646,6 +647,28 @@ def alexnet_layers(reps=5, batch=128):
     return out
 
 
+def launch_overhead_us(reps=50):
+    """Average time between a HIP event pair around one empty launch (the
+    int8 MFMA loop with no iterations, one workgroup) on the current stream,
+    queued behind other work: what an event-timed kernel duration holds
+    besides the kernel itself."""
+    import torch
+    niti = __import__("paper_2009_13108_amd.niti", fromlist=["niti"])
+    out = torch.empty(1024 * 256, dtype=torch.int32, device="cuda")
+    niti.mfma_loop(0, 1, out)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    # a few milliseconds of matrix work first, so that the pairs below are
+    # queued before the GPU reaches them and time the GPU, not the host
+    niti.mfma_loop(8192, 1024, out)
+    for a, b in ev:
+        a.record()
+        niti.mfma_loop(0, 1, out)
+        b.record()
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in ev) * 1e3 / reps
+
+
 def mfma_loop_rate(iters=4096, per_cu=4, reps=5):
     """The int8 MFMA loop (register operands, no memory traffic) over
     256 x per_cu workgroups: the rate matrix work sustains on this device."""
@@ -812,19 +835,28 @@ def kernel_label(profiler_name):
 def summarize_kernel_trace(path):
     """Per-kernel durations from a rocprofv3 kernel-trace CSV
     (--kernel-trace --output-format csv), labelled as the library labels its
-    timing records."""
+    timing records: all launches, and the launches on the default stream
+    (stream 0: the serial pass whose per-kernel times the bench line's
+    roofline uses; the timed steps run on two other streams, where kernels
+    overlap)."""
     import collections
     import csv
 
     per = collections.OrderedDict()
+    ser = collections.defaultdict(list)
     for r in csv.DictReader(open(path)):
         if "niti::" not in r["Kernel_Name"]:
             continue
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        per.setdefault(kernel_label(r["Kernel_Name"]), []).append(dur)
-    print("%-44s %7s %11s %9s" % ("kernel", "calls", "total_us", "avg_us"))
+        lab = kernel_label(r["Kernel_Name"])
+        per.setdefault(lab, []).append(dur)
+        if r.get("Stream_Id", "0") == "0":
+            ser[lab].append(dur)
+    print("%-44s %7s %11s %9s %11s %11s" % ("kernel", "calls", "total_us", "avg_us", "serial_n", "serial_avg"))
     for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
-        print("%-44s %7d %11.1f %9.2f" % (name[:44], len(v), sum(v), sum(v) / len(v)))
+        sv = ser.get(name, [])
+        print("%-44s %7d %11.1f %9.2f %11d %11s" % (name[:44], len(v), sum(v), sum(v) / len(v), len(sv),
+                                                     "%.2f" % (sum(sv) / len(sv)) if sv else "-"))
 
 
 def summarize_counters(path):
@@ -872,17 +904,29 @@ def summarize_counters(path):
         print("%-48s %7d %9.2f %6.2f %7.1f %8.1f" % (lab[:48], n, us, ghz, util, tops))
 
 
-def copy_calibration(nbytes):
+def copy_calibration(nbytes, pattern="contiguous"):
     """A plain device copy of nbytes (torch's copy kernel), five times: the
-    reference for scaling FETCH_SIZE / WRITE_SIZE to bytes."""
+    reference for scaling FETCH_SIZE / WRITE_SIZE to bytes.  pattern:
+      contiguous  read nbytes, write nbytes;
+      strided128  read the first 128 bytes of every 256-byte row of a
+                  2 * nbytes buffer (whole 128-byte lines, every other one),
+                  write them contiguously: nbytes each way;
+      strided64   read the first 64 bytes of every 128-byte row (half lines),
+                  write them contiguously: nbytes of data each way."""
     import torch
-    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
-    b = torch.empty_like(a)
+    if pattern == "contiguous":
+        a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+        src = a
+    else:
+        w = 128 if pattern == "strided128" else 64
+        a = torch.empty(2 * nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+        src = a.view(nbytes // w, 2 * w)[:, :w]
+    b = torch.empty(src.shape, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     for _ in range(5):
-        b.copy_(a)
+        b.copy_(src)
     torch.cuda.synchronize()
-    print("copied %d bytes x5" % nbytes, flush=True)
+    print("copied %d bytes x5 (%s)" % (nbytes, pattern), flush=True)
 
 
 def main():
@@ -907,6 +951,8 @@ def main():
                     help="summarize a rocprofv3 --pmc counter CSV per kernel family and exit (no GPU)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run only a plain device copy of this many bytes (counter calibration)")
+    ap.add_argument("--copy-pattern", choices=("contiguous", "strided128", "strided64"), default="contiguous",
+                    help="access pattern of the --copy-bytes copy")
     args = ap.parse_args()
     if args.kernel_trace:
         summarize_kernel_trace(args.kernel_trace)
@@ -915,7 +961,7 @@ def main():
         summarize_counters(args.counters)
         return
     if args.copy_bytes:
-        copy_calibration(args.copy_bytes)
+        copy_calibration(args.copy_bytes, args.copy_pattern)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path; "
@@ -984,7 +1030,7 @@ def main():
     ser = measure_serial(job, args.steps)
     kern = ser["kernels"]
     top = max(kern, key=lambda k: kern[k][1])
-    n_top, ms_top, ops_top = kern[top]
+    n_top, ms_top, ops_top, bytes_top = kern[top]
     achieved = ops_top / (ms_top * 1e-3) / 1e12
     value = job.ops_per_step / (ms * 1e-3) / 1e12
     fam = ser["families"]
@@ -992,6 +1038,7 @@ def main():
     # the matrix cores' sustained int8 rate with no memory traffic (context
     # for the roofline fraction, which stays against the published peak)
     loop = mfma_loop_rate()
+    overhead = launch_overhead_us()
 
     extra = {}
     if not args.no_configs:
@@ -1048,7 +1095,10 @@ def main():
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "launches_per_step": n_top // args.steps,
                      "avg_us": round(ms_top * 1e3 / n_top, 2),
+                     "event_launch_overhead_us": round(overhead, 2),
+                     "avg_us_less_launch_overhead": round(ms_top * 1e3 / n_top - overhead, 2),
                      "algorithmic_ops_per_launch": ops_top // n_top,
+                     "algorithmic_bytes_per_launch": bytes_top // n_top,
                      "kernels": {k: {"launches_per_step": v[0] // args.steps, "avg_us": round(v[1] * 1e3 / v[0], 2),
                                      "tops": round(v[2] / (v[1] * 1e-3) / 1e12, 1)}
                                  for k, v in sorted(kern.items(), key=lambda kv: -kv[1][1])},

@@ -133,6 +133,13 @@ CONV_CASES = [
     (1, 4, 1, 1, 8, 1, 1, 2, 1, False),
     # classifier head as a 1x1 convolution: 512 features, 1000 classes
     (128, 512, 1, 1, 1000, 1, 1, 1, 0, True),
+    # stride 1, 64 or 128 channels: input rows staged per band of output rows
+    # (ragged last band, two or three 64-channel output tiles)
+    (2, 64, 20, 60, 64, 3, 3, 1, 1, True),
+    (2, 128, 30, 20, 128, 3, 3, 1, 1, False),
+    (1, 64, 9, 7, 192, 3, 3, 1, 1, True),
+    (3, 128, 6, 9, 64, 3, 3, 1, 0, False),
+    (1, 64, 11, 13, 64, 5, 5, 1, 2, True),
 ]
 
 
