@@ -293,9 +293,10 @@ niti_status niti_relu_mask(int8_t *e, const int8_t *a, int64_t n, void *stream);
  * the stochastic-rounding generator (see Rounding above) is at least
  * drop256, i.e. with probability 1 - drop256/256; y = x where kept, 0
  * elsewhere; keep[i] = 1 / 0 records the choice.  The kept values are
- * rescaled through the exponent: *s_y = *s_x + exp_add when both are given
- * (drop256 = 128 with exp_add = 1 is the 1/(1 - p) = 2 of inverted dropout,
- * exactly).  drop256 in 0..256, exp_add in -8..8. */
+ * rescaled through the exponent: *s_y = *s_x + exp_add, held to
+ * [-128, 127], when both are given (drop256 = 128 with exp_add = 1 is the
+ * 1/(1 - p) = 2 of inverted dropout, exactly).  drop256 in 0..256, exp_add in
+ * -8..8 (NITI_ERR_ARG otherwise); s_x and s_y both given or both NULL. */
 niti_status niti_dropout_fwd(const int8_t *x, int8_t *y, uint8_t *keep, int64_t n, uint64_t seed,
                              uint32_t call, int drop256, const int8_t *s_x, int8_t *s_y, int exp_add,
                              void *stream);

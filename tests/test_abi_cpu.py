@@ -104,6 +104,20 @@ def test_other_calls_reject_on_host():
     assert L.niti_maxpool2_fwd(FAKE, FAKE, FAKE, 1, 3, 4, 4, None) == -2
     assert L.niti_quantize_u8(FAKE, FAKE, 1, 3, 4, 4, 2, None) == -2
     assert L.niti_relu_mask(FAKE, FAKE, -4, None) == -2
+    # dropout: size, missing buffers, one exponent pointer without the other, rate and exponent step ranges
+    assert L.niti_dropout_fwd(FAKE, FAKE, FAKE, -1, 0, 0, 128, None, None, 1, None) == -2
+    assert L.niti_dropout_fwd(None, FAKE, FAKE, 16, 0, 0, 128, None, None, 1, None) == -1
+    assert L.niti_dropout_fwd(FAKE, FAKE, FAKE, 16, 0, 0, 128, FAKE, None, 1, None) == -1
+    assert L.niti_dropout_fwd(FAKE, FAKE, FAKE, 16, 0, 0, 257, None, None, 1, None) == -6
+    assert L.niti_dropout_fwd(FAKE, FAKE, FAKE, 16, 0, 0, -1, None, None, 1, None) == -6
+    assert L.niti_dropout_fwd(FAKE, FAKE, FAKE, 16, 0, 0, 128, FAKE, FAKE, 9, None) == -6
+    assert L.niti_dropout_bwd(FAKE, FAKE, FAKE, -1, None) == -2
+    assert L.niti_dropout_bwd(FAKE, None, FAKE, 16, None) == -1
+    # the matrix-core rate check
+    assert L.niti_mfma_loop(16, 4, None, None) == -1
+    assert L.niti_mfma_loop(-1, 4, FAKE, None) == -2
+    assert L.niti_mfma_loop(16, 0, FAKE, None) == -2
+    assert L.niti_mfma_loop(16, (1 << 20) + 1, FAKE, None) == -2
 
 
 def test_conv_fwd_workspace_rules():
