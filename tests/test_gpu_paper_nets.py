@@ -135,3 +135,46 @@ def test_alexnet_layer_shapes(layer):
         assert (nchw(host(dx)) == dx_o).all() and same_stats(g[1], st_d)
     assert (kcrs(host(g32)) == g_o).all()
     assert (kcrs(host(wd)) == w_o).all() and same_stats(g[2], st_w)
+
+
+FIT_CASES = [
+    # name, specs, image size, image channels, m_u, steps, training accuracy required after them
+    ("lenet5", M.LENET5, 28, 1, 3, 200, 0.95),
+    ("vgg_small7", M.vgg_small(7), 32, 3, 5, 150, 0.75),
+]
+
+
+@pytest.mark.parametrize("case", FIT_CASES, ids=[c[0] for c in FIT_CASES])
+def test_integer_training_fits_a_fixed_batch(case):
+    """The method learns: the library alone (integer forward, loss,
+    back-propagation and update; nearest rounding for activations and
+    errors, pseudo stochastic for gradients, as in the paper's experiments;
+    dropout on in VGG-small) trained on one fixed batch of 256 synthetic
+    images with random labels drives the training accuracy (argmax of the
+    int8 logits) from chance to near memorisation.  Every result is an
+    integer, so the run is deterministic."""
+    import torch
+    name, specs, hw, img_c, mu, steps, need = case
+    say("fit", name, steps)
+    batch = 256
+    zf = M.LENET5_REAL["zero_filters"] if specs is M.LENET5 else None
+    ws, exps = M.synthetic_weights(specs, 4, 60, image_channels=img_c, zero_filters=zf)
+    net = M.IntNet(specs, (hw, hw, 4), batch, ws, exps, mode=niti.RTN, grad_mode=niti.PSR, drop_seed=3)
+    px = I.pixels(I.base_seed(61, 1), (batch, img_c, hw, hw), device="cuda")
+    lab = I.labels(I.base_seed(61, 2), batch, 10, device="cuda")
+    x = torch.empty((batch, hw, hw, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(px, x)
+    s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+
+    def accuracy(lg):
+        return (lg.view(batch, -1).float().argmax(1) == lab.long()).float().mean().item()
+
+    lg, _ = net.step(x, s0, lab, mu=mu)
+    torch.cuda.synchronize()
+    first = accuracy(lg)
+    for _ in range(steps - 1):
+        lg, _ = net.step(x, s0, lab, mu=mu)
+    torch.cuda.synchronize()
+    last = accuracy(lg)
+    say("fit", name, "accuracy", first, "->", last)
+    assert first < 0.2 and last >= need, (first, last)
