@@ -9,6 +9,7 @@ GPU tests can compare whole full-size outputs without running the oracle.
     python tests/golden/make_fullsize.py c5      # GEMM sweep, 27 shapes x 2 ranges
     python tests/golden/make_fullsize.py c4      # ResNet-18 layer set, batch 128
     python tests/golden/make_fullsize.py c3      # VGG-style CNN, batch 256, one step
+    python tests/golden/make_fullsize.py nets    # LeNet-5 and VGG-small-7, batch 256, a few steps
 
 Writes tests/golden/fullsize_<config>.json.
 """
@@ -177,9 +178,72 @@ def make_c3(batch=256):
     return rec
 
 
+# ------------------------------------------------- the paper's networks
+def net_weights(specs, cfg, image_channels, zero_filters):
+    """The benchmark's seeded weights of a layer list in the oracle's layouts
+    (KCRS, [out][in] with the input in (h, w, c) order) and their static
+    exponents: the first layer's channels past the image's, and the filters
+    in zero_filters (with the same input channels of the next convolution),
+    held at zero; exponents from the real fan-in."""
+    ws, exps = [], []
+    wi = 0
+    for sp in specs:
+        if sp[0] == "conv":
+            _, cin, cout, k = sp[:4]
+            w = I.weights(I.base_seed(cfg, 10 + wi), (cout, k, k, cin))
+            real = cin
+            if wi == 0 and image_channels < cin:
+                w[..., image_channels:] = 0
+                real = image_channels
+            if wi in zero_filters:
+                lo, hi = zero_filters[wi]
+                w[lo:hi] = 0
+            if wi - 1 in zero_filters:
+                lo, hi = zero_filters[wi - 1]
+                w[..., lo:hi] = 0
+                real = cin - (hi - lo)
+            ws.append(nchw(w))
+            exps.append(I.weight_exponent(real * k * k))
+            wi += 1
+        elif sp[0] == "fc":
+            ws.append(I.weights(I.base_seed(cfg, 10 + wi), (sp[2], sp[1])))
+            exps.append(I.weight_exponent(sp[1]))
+            wi += 1
+    return ws, exps
+
+
+def make_nets(batch=256):
+    """LeNet-5 (28x28x1) and VGG-small-7 (32x32x3, dropout) as the benchmark
+    builds them: seeds 40 and 41, pseudo stochastic rounding everywhere,
+    m_u = 5, dropout seed = the seed; image channels padded with zeros to 4.
+    Per step the logits digest and exponent; after the last step every
+    layer's weights (KRSC / [out][in])."""
+    from paper_2009_13108_amd import model as M
+    nets = [("lenet5", M.LENET5, 28, 1, {0: (6, 8)}, 40, 3), ("vgg_small7", M.vgg_small(7), 32, 3, {}, 41, 2)]
+    out = []
+    for name, specs, hw, img_c, zf, cfg, steps in nets:
+        t0 = time.time()
+        w, exps = net_weights(specs, cfg, img_c, zf)
+        px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hw, hw))
+        labels = I.labels(I.base_seed(cfg, 2), batch, 10)
+        x = np.zeros((batch, 4, hw, hw), np.int8)
+        x[:, :img_c] = oracle.quantize_u8(px)
+        ospecs = [("conv",) + tuple(sp[1:]) if sp[0] == "conv" else sp for sp in specs]
+        net = OracleNet(ospecs, (4, hw, hw), batch, w, exps, mu=5, mode=oracle.PSR, grad_mode=oracle.PSR,
+                        sr_seed=0, drop_seed=cfg)
+        rec = {"net": name, "batch": batch, "seed": cfg, "steps": []}
+        for _ in range(steps):
+            logits, s = net.step(x, -7, labels)
+            rec["steps"].append({"logits_sha256": sha(logits), "s_logits": int(s)})
+        rec["weights_sha256"] = [sha(nhwc(v)) if v.ndim == 4 else sha(v) for v in net.w]
+        out.append(rec)
+        print(rec, "%.1fs" % (time.time() - t0), flush=True)
+    return out
+
+
 def main():
     which = sys.argv[1]
-    fn = {"c5": make_c5, "c4": make_c4, "c3": make_c3}[which]
+    fn = {"c5": make_c5, "c4": make_c4, "c3": make_c3, "nets": make_nets}[which]
     res = fn()
     path = os.path.join(HERE, "fullsize_%s.json" % which)
     with open(path, "w") as f:

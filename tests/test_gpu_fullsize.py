@@ -198,3 +198,36 @@ def test_vgg_full_batch_step():
     assert int(s.cpu()[0]) == rec["s_logits"]
     for li, w in enumerate(net.weights()):
         assert sha(w) == rec["weights_sha256"][li], "layer %d" % li
+
+
+NETS = [("lenet5", M.LENET5, 28, 1, M.LENET5_REAL["zero_filters"]), ("vgg_small7", M.vgg_small(7), 32, 3, None)]
+
+
+@pytest.mark.parametrize("net", NETS, ids=[n[0] for n in NETS])
+def test_paper_network_full_batch_steps(net):
+    """LeNet-5 and VGG-small-7 (Section 4, Table 5) trained at batch 256
+    exactly as bench.py times them (same seeds and rounding; dropout on in
+    VGG-small): every step's logits and exponent, and every layer's weights
+    after the last step, against the oracle's digests."""
+    import torch
+    name, specs, hw, img_c, zf = net
+    recs = [r for r in _load("fullsize_nets.json") if r["net"] == name]
+    if not recs:
+        pytest.skip("no digest for %s" % name)
+    rec = recs[0]
+    batch, cfg = rec["batch"], rec["seed"]
+    say("paper net full batch", name, batch, len(rec["steps"]))
+    ws, exps = M.synthetic_weights(specs, 4, cfg, image_channels=img_c, zero_filters=zf)
+    gnet = M.IntNet(specs, (hw, hw, 4), batch, ws, exps, drop_seed=cfg)
+    px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hw, hw), device="cuda")
+    lab = I.labels(I.base_seed(cfg, 2), batch, 10, device="cuda")
+    x = torch.empty((batch, hw, hw, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(px, x)
+    s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+    for i, want in enumerate(rec["steps"]):
+        lg, s = gnet.step(x, s0, lab)
+        torch.cuda.synchronize()
+        assert sha(lg.reshape(batch, -1)) == want["logits_sha256"], "logits step %d" % i
+        assert int(s.cpu()[0]) == want["s_logits"], "exponent step %d" % i
+    for li, w in enumerate(gnet.weights()):
+        assert sha(w) == rec["weights_sha256"][li], "weights layer %d" % li

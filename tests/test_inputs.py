@@ -20,3 +20,23 @@ def test_distribution_is_flat():
     a = I.weights(7, (1 << 20,)).astype(np.int64)
     h = np.bincount(a + 127, minlength=255)
     assert h.min() > 0.9 * h.mean() and h.max() < 1.1 * h.mean()
+
+
+def test_golden_net_weights_match_the_library_draw():
+    """The full-batch network digests were written from weights drawn by the
+    digest script itself (oracle layouts); the GPU test rebuilds them with
+    the library's synthetic_weights (its layouts).  Both must be the same
+    tensors, zeroed filters and exponents included."""
+    import importlib.util
+    import os
+    from paper_2009_13108_amd import model as M
+    path = os.path.join(os.path.dirname(__file__), "golden", "make_fullsize.py")
+    spec = importlib.util.spec_from_file_location("make_fullsize", path)
+    mk = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mk)
+    for specs, img_c, zf, cfg in [(M.LENET5, 1, M.LENET5_REAL["zero_filters"], 40), (M.vgg_small(7), 3, {}, 41)]:
+        wo, eo = mk.net_weights(specs, cfg, img_c, zf)
+        wl, el = M.synthetic_weights(specs, 4, cfg, image_channels=img_c, zero_filters=zf)
+        assert eo == el
+        for a, b in zip(wo, wl):
+            assert (mk.nhwc(a) == b).all() if a.ndim == 4 else (a == b).all()
