@@ -9,7 +9,8 @@ GPU tests can compare whole full-size outputs without running the oracle.
     python tests/golden/make_fullsize.py c5      # GEMM sweep, 27 shapes x 2 ranges
     python tests/golden/make_fullsize.py c4      # ResNet-18 layer set, batch 128
     python tests/golden/make_fullsize.py c3      # VGG-style CNN, batch 256, one step
-    python tests/golden/make_fullsize.py nets    # LeNet-5 and VGG-small-7, batch 256, a few steps
+    python tests/golden/make_fullsize.py nets    # LeNet-5, VGG-small-7/8/9, batch 256, 1-3 steps
+    python tests/golden/make_fullsize.py nets vgg_small8,vgg_small9   # only those (others kept)
 
 Writes tests/golden/fullsize_<config>.json.
 """
@@ -212,16 +213,19 @@ def net_weights(specs, cfg, image_channels, zero_filters):
     return ws, exps
 
 
-def make_nets(batch=256):
-    """LeNet-5 (28x28x1) and VGG-small-7 (32x32x3, dropout) as the benchmark
-    builds them: seeds 40 and 41, pseudo stochastic rounding everywhere,
+def make_nets(only=None, batch=256):
+    """LeNet-5 (28x28x1) and VGG-small-7/8/9 (32x32x3, dropout) as the
+    benchmark builds them: seeds 40 to 43, pseudo stochastic rounding everywhere,
     m_u = 5, dropout seed = the seed; image channels padded with zeros to 4.
     Per step the logits digest and exponent; after the last step every
     layer's weights (KRSC / [out][in])."""
     from paper_2009_13108_amd import model as M
-    nets = [("lenet5", M.LENET5, 28, 1, {0: (6, 8)}, 40, 3), ("vgg_small7", M.vgg_small(7), 32, 3, {}, 41, 2)]
+    nets = [("lenet5", M.LENET5, 28, 1, {0: (6, 8)}, 40, 3), ("vgg_small7", M.vgg_small(7), 32, 3, {}, 41, 2),
+            ("vgg_small8", M.vgg_small(8), 32, 3, {}, 42, 1), ("vgg_small9", M.vgg_small(9), 32, 3, {}, 43, 1)]
     out = []
     for name, specs, hw, img_c, zf, cfg, steps in nets:
+        if only and name not in only:
+            continue
         t0 = time.time()
         w, exps = net_weights(specs, cfg, img_c, zf)
         px = I.pixels(I.base_seed(cfg, 1), (batch, img_c, hw, hw))
@@ -244,8 +248,17 @@ def make_nets(batch=256):
 def main():
     which = sys.argv[1]
     fn = {"c5": make_c5, "c4": make_c4, "c3": make_c3, "nets": make_nets}[which]
-    res = fn()
     path = os.path.join(HERE, "fullsize_%s.json" % which)
+    if which == "nets" and len(sys.argv) > 2:
+        # only the named networks; the others' cases already in the file are kept
+        only = sys.argv[2].split(",")
+        res = fn(only)
+        if os.path.exists(path):
+            with open(path) as f:
+                kept = [c for c in json.load(f)["cases"] if c["net"] not in only]
+            res = kept + res
+    else:
+        res = fn()
     with open(path, "w") as f:
         json.dump({"source": "oracle (tests/golden/make_fullsize.py %s)" % which, "cases": res}, f, indent=1)
     print("wrote", path)

@@ -200,12 +200,13 @@ def test_vgg_full_batch_step():
         assert sha(w) == rec["weights_sha256"][li], "layer %d" % li
 
 
-NETS = [("lenet5", M.LENET5, 28, 1, M.LENET5_REAL["zero_filters"]), ("vgg_small7", M.vgg_small(7), 32, 3, None)]
+NETS = [("lenet5", M.LENET5, 28, 1, M.LENET5_REAL["zero_filters"])]
+NETS += [("vgg_small%d" % d, M.vgg_small(d), 32, 3, None) for d in (7, 8, 9)]
 
 
 @pytest.mark.parametrize("net", NETS, ids=[n[0] for n in NETS])
 def test_paper_network_full_batch_steps(net):
-    """LeNet-5 and VGG-small-7 (Section 4, Table 5) trained at batch 256
+    """LeNet-5 and VGG-small-7/8/9 (Section 4, Table 5) trained at batch 256
     exactly as bench.py times them (same seeds and rounding; dropout on in
     VGG-small): every step's logits and exponent, and every layer's weights
     after the last step, against the oracle's digests."""

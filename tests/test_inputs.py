@@ -34,7 +34,9 @@ def test_golden_net_weights_match_the_library_draw():
     spec = importlib.util.spec_from_file_location("make_fullsize", path)
     mk = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(mk)
-    for specs, img_c, zf, cfg in [(M.LENET5, 1, M.LENET5_REAL["zero_filters"], 40), (M.vgg_small(7), 3, {}, 41)]:
+    cases = [(M.LENET5, 1, M.LENET5_REAL["zero_filters"], 40)]
+    cases += [(M.vgg_small(d), 3, {}, 34 + d) for d in (7, 8, 9)]
+    for specs, img_c, zf, cfg in cases:
         wo, eo = mk.net_weights(specs, cfg, img_c, zf)
         wl, el = M.synthetic_weights(specs, 4, cfg, image_channels=img_c, zero_filters=zf)
         assert eo == el
