@@ -71,7 +71,9 @@ typedef enum niti_status {
     NITI_OK = 0,
     NITI_ERR_NULL = -1,        /* a required pointer is NULL               */
     NITI_ERR_SHAPE = -2,       /* a size is negative, zero where it must not be, or inconsistent */
-    NITI_ERR_UNSUPPORTED = -3, /* valid but outside what the kernels cover */
+    NITI_ERR_UNSUPPORTED = -3, /* valid but outside what the kernels cover, among them any
+                                  operand, result or workspace part of 2^31 bytes or more
+                                  (the kernels address with 32-bit offsets)            */
     NITI_ERR_WORKSPACE = -4,   /* workspace missing or smaller than needed */
     NITI_ERR_HIP = -5,         /* the HIP runtime reported an error        */
     NITI_ERR_ARG = -6          /* an enum or scalar argument is out of range */

@@ -64,6 +64,9 @@ def test_gemm_rejects_on_host():
     assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, FAKE, None, None, 7, 0, 0, S, None) == -1
     assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 4, 4, 4, None, None, None, 7, 0, 0, None, None) == -1
     assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 1 << 20, 1 << 20, 4, None, None, None, 7, 0, 0, S, None) == -3
+    # an operand of exactly 2^31 bytes (A: 2^27 x 16) is past the 32-bit offsets
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 1 << 27, 16, 16, None, None, None, 7, 0, 0, S, None) == -3
+    assert L.niti_gemm_fwd(FAKE, FAKE, FAKE, 16, 1 << 27, 16, None, None, None, 7, 0, 0, S, None) == -3
 
 
 def test_conv_rejects_on_host():
