@@ -355,8 +355,12 @@ WgradPlan wgrad_tap_plan(int64_t K, int64_t C, int64_t npix) {
     pl.tbk = 64;
     const int64_t tiles = (K / 64) * (C / CW);
     const int64_t steps = (npix + PIX - 1) / PIX;
-    // about one workgroup per CU, at least two stages each
-    int64_t splits = (256 + tiles - 1) / tiles;
+    // About 192 workgroups, at least two stages each.  A workgroup holds
+    // most of its CU's LDS and registers, so a grid of one per CU would shut
+    // out a kernel running beside it on another stream (the back-propagation
+    // of a training step); leaving a quarter of the CUs free measured ~2%
+    // faster steps than 256, 160, 224 or a floor of 192 / tiles.
+    int64_t splits = (192 + tiles - 1) / tiles;
     const int64_t max_splits = steps / 2 > 1 ? steps / 2 : 1;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
