@@ -47,7 +47,7 @@ def test_two_stream_prepared_steps_equal_serial_steps():
     par.prepare()                       # step 1 (recorded)
     for _ in range(STEPS - 1):
         par.step_prepared()
-    par.sA.wait_event(par.ev_upd)
+    par.ev_upd.wait(par.sA)
     for _ in range(STEPS):
         ser.step_serial()
     a, b = _state(par), _state(ser)
