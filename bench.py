@@ -258,6 +258,7 @@ class ResNetStep:
         # the final a_tail of them take their weight gradient on A.
         bwd = [(L, c) for L in reversed(self.layers) if L["bwd_data"] for c in reversed(range(L["count"]))]
         on_a = set((id(L), c) for L, c in bwd[len(bwd) - self.a_tail:]) if self.a_tail > 0 else set()
+        pos = {(id(L), c): i for i, (L, c) in enumerate(bwd)}
 
         def pack_filters(tail):
             for L in self.layers:
@@ -313,6 +314,11 @@ class ResNetStep:
         seg(B, lambda: niti.conv_bwd_weight(fd, self.feat.view(Bsz, 1, 1, fin), self.err.view(Bsz, 1, 1, fout),
                                             self.wfc.view(fout, 1, 1, fin), self.stats, self.ws_b, mu=self.mu,
                                             stats_index=s + 3))
+        # B waits, before layer l's weight gradient, for the event after the
+        # A call that produced dy(l) (the back-propagation of layer l + 1, or
+        # the head): the back-propagation of layer l itself reads the packed
+        # copy of w(l), not w(l), so the update need not wait for it.
+        waited = ev
         for L in reversed(self.layers):
             d = L["desc"]
             for c in reversed(range(L["count"])):
@@ -325,18 +331,22 @@ class ResNetStep:
                     seg(A, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu,
                                                         stats_index=s0 + 2))
                     continue
+                if (id(L), c) not in on_a:
+                    if waited != ev:
+                        wait(B, self.ev_bwd[ev])
+                        waited = ev
+                    seg(B, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws_b, mu=self.mu,
+                                                        stats_index=s0 + 2))
                 pk = L["packed"][c]
                 seg(A, lambda: niti.conv_bwd_data_packed(d, L["dy"], pk, L["dx"], self.stats,
                                                          relu_src=L["x"], stats_index=s0 + 1))
+                nb = pos[(id(L), c)] + 1
+                if nb < len(bwd) and (id(bwd[nb][0]), bwd[nb][1]) not in on_a:
+                    ev += 1                         # dy of the next layer, for its weight gradient on B
+                    rec(self.ev_bwd[ev], A)
                 if (id(L), c) in on_a:
                     seg(A, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws, mu=self.mu,
                                                         stats_index=s0 + 2))
-                    continue
-                ev += 1
-                rec(self.ev_bwd[ev], A)
-                wait(B, self.ev_bwd[ev])
-                seg(B, lambda: niti.conv_bwd_weight(d, L["x"], L["dy"], w, self.stats, self.ws_b, mu=self.mu,
-                                                    stats_index=s0 + 2))
         rec(self.ev_upd, B)
         if on_a:
             rec(self.ev_tail, A)
