@@ -122,6 +122,16 @@ class ResNetStep:
             if name.startswith("stem"):
                 x[..., 3:] = 0          # 3 image channels, zero-padded to 4
                 c_real = 3
+                # The input batch is stored with its zero border (as a data
+                # loader can write it), so that the image layer's descriptor
+                # has no padding and the library reads the image in place;
+                # the outputs and the work are those of the padded 224 x 224
+                # convolution.
+                hb = hw + 2 * pd
+                xb = torch.zeros((batch, hb, hb, cin), dtype=torch.int8, device=dev)
+                xb[:, pd:pd + hw, pd:pd + hw] = x
+                x = xb
+                d = niti.ConvDesc.make(batch, hb, hb, cin, cout, k, k, st, 0)
             dy = I.errors8(I.base_seed(seed_cfg, 200 + li), d.y_shape(), device=dev)
             ws_ = []
             for cpy in range(count):

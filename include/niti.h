@@ -157,7 +157,11 @@ niti_status niti_gemm_fwd(const int8_t *A, const int8_t *B, int8_t *C,
  * with target 7.  Needs c % 4 == 0 (pad image channels with zeros).
  * Workspace: niti_workspace_bytes(NITI_OP_CONV_FWD, d, ...), zero for most
  * layers; layers with few channels (s*c <= 64) use it for a zero-padded
- * copy of x. */
+ * copy of x and for their filter rows widened to whole load windows.  Such
+ * a layer reads x in place, without the copy, when the descriptor has no
+ * padding and every filter window of an output row lies inside the input
+ * row (for example an image stored with its zero border); the weight
+ * gradient does the same. */
 niti_status niti_conv_fwd(const niti_conv_desc *d, const int8_t *x, const int8_t *w,
                           int8_t *y, const int8_t *s_x, const int8_t *s_w, int8_t *s_y,
                           int relu, niti_round_mode mode, niti_stats *stats,

@@ -58,10 +58,13 @@ niti_status check_conv(const niti_conv_desc* d, int64_t* P, int64_t* Q) {
 
 // Layers with few channels (S*C <= 64, C % 64 != 0) read a zero-padded copy
 // of their input in filter-row windows of lw bytes (igemm_dma.hip, wgrad_dma.hip).
+// An input without padding whose rows already reach the last window (an
+// image stored with its zero border) is read in place: no copy.
 struct WinPlan {
     bool on;
+    bool in_place;
     int64_t hp, wp, lw, ktot;
-    int64_t xpad_bytes, wr_bytes;  // workspace pieces, 256-byte rounded
+    int64_t xpad_bytes, wr_bytes;  // workspace pieces, 256-byte rounded (xpad_bytes 0 in place)
 };
 
 WinPlan win_plan(const niti_conv_desc* d, int64_t P, int64_t Q) {
@@ -77,7 +80,8 @@ WinPlan win_plan(const niti_conv_desc* d, int64_t P, int64_t Q) {
     const int64_t xb = d->n * w.hp * w.wp * d->c;
     if (too_big(xb) || too_big(d->k * w.ktot)) return w;
     (void)P;
-    w.xpad_bytes = round_up(xb, 256);
+    w.in_place = d->pad_h == 0 && d->pad_w == 0 && w.hp == d->h && w.wp == d->w;
+    w.xpad_bytes = w.in_place ? 0 : round_up(xb, 256);
     w.wr_bytes = round_up(d->k * w.ktot, 256);
     w.on = true;
     return w;
@@ -290,10 +294,11 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
 
     const WinPlan wp = win_plan(d, P, Q);
     if (wp.on && mode != NITI_ROUND_SR) {
-        // zero-padded input and window-extended filter rows in the workspace
-        int8_t* xpad = (int8_t*)ws;
-        int8_t* wr = xpad + wp.xpad_bytes;
-        p.act = xpad;
+        // zero-padded input (unless read in place) and window-extended filter
+        // rows in the workspace
+        int8_t* xpad = wp.in_place ? nullptr : (int8_t*)ws;
+        int8_t* wr = (int8_t*)ws + wp.xpad_bytes;
+        p.act = wp.in_place ? x : xpad;
         p.wgt = wr;
         p.H = (int32_t)wp.hp;
         p.W = (int32_t)wp.wp;
@@ -306,8 +311,8 @@ niti_status niti_conv_fwd(const niti_conv_desc* d, const int8_t* x, const int8_t
         p.wgt_bytes = d->k * wp.ktot;
         p.win = 1;
         if (igemm_dma_eligible(b)) {
-            hipError_t e = pad_repack_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, w, wr,
-                                          d->k, d->r, d->s * d->c, wp.lw, wp.ktot, strm);
+            hipError_t e = pad_repack_run(x, xpad, wp.in_place ? 0 : d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h,
+                                          d->pad_w, w, wr, d->k, d->r, d->s * d->c, wp.lw, wp.ktot, strm);
             if (e != hipSuccess) return NITI_ERR_HIP;
             return hip_status(igemm_run(b, ctl, strm));
         }
@@ -530,7 +535,7 @@ niti_status niti_conv_bwd_weight(const niti_conv_desc* d, const int8_t* x, const
     int32_t* g32 = g32_out ? g32_out : (int32_t*)ws;
     int32_t* part = plan.splits > 1 ? (int32_t*)((char*)ws + g_bytes) : g32;
     hipError_t e;
-    if (win) {
+    if (win && !wp.in_place) {
         int8_t* xpad = (int8_t*)ws + g_bytes + p_bytes;
         e = pad_image_run(x, xpad, d->n, d->h, d->w, d->c, wp.hp, wp.wp, d->pad_h, d->pad_w, strm);
         if (e != hipSuccess) return NITI_ERR_HIP;

@@ -120,6 +120,10 @@ CONV_CASES = [
     (2, 8, 10, 10, 32, 3, 3, 2, 1, False),
     (3, 4, 13, 12, 48, 5, 5, 2, 2, True),
     (2, 16, 7, 7, 32, 2, 2, 1, 0, False),
+    # no padding and rows that reach the last window: read in place (an image
+    # stored with its zero border); one column short: copied
+    (2, 4, 38, 38, 64, 7, 7, 2, 0, True),
+    (2, 4, 37, 37, 64, 7, 7, 2, 0, False),
     # strided 3x3 back-propagation over 64 error channels (odd sizes: sub-pixel
     # classes of unequal size)
     (2, 32, 9, 11, 64, 3, 3, 2, 1, True),
@@ -258,6 +262,44 @@ STRIDE_CASES = [
     (1, 128, 16, 16, 96, 3, 3, 4, 0, False),
     (3, 64, 9, 9, 40, 1, 1, 8, 0, True),
 ]
+
+
+def test_conv_bordered_image_read_in_place():
+    """A few-channel image stored with its zero border (no padding in the
+    descriptor, rows reaching the last filter window) is read in place; the
+    forward pass and the weight gradient then equal those of the unbordered
+    image with the padding in the descriptor, byte for byte, statistics
+    included (the 7x7 stride-2 image layer: 32x32 inside a 3-pixel border)."""
+    import torch
+    n, c, hw, k, r, st, pd = 2, 4, 32, 64, 7, 2, 3
+    x = I.activations(901, (n, hw, hw, c))
+    x[..., 3:] = 0
+    xb = np.zeros((n, hw + 2 * pd, hw + 2 * pd, c), np.int8)
+    xb[:, pd:pd + hw, pd:pd + hw] = x
+    wt = I.weights(902, (k, r, r, c))
+    wt[..., 3:] = 0
+    gp = niti.ConvDesc.make(n, hw, hw, c, k, r, r, st, pd)
+    gb = niti.ConvDesc.make(n, hw + 2 * pd, hw + 2 * pd, c, k, r, r, st, 0)
+    assert gp.y_shape() == gb.y_shape()
+    assert niti.workspace_bytes(niti.OP_CONV_FWD, gb) < niti.workspace_bytes(niti.OP_CONV_FWD, gp)
+    assert niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gb) < niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, gp)
+    dy = dev(I.errors8(903, gp.y_shape()))
+    res = []
+    for gd, xi in ((gp, x), (gb, xb)):
+        stats = niti.new_stats(2)
+        ws = niti.new_workspace(max(niti.workspace_bytes(op, gd) for op in (niti.OP_CONV_FWD, niti.OP_CONV_BWD_WEIGHT)))
+        xd, wd = dev(xi), dev(wt)
+        y = torch.empty(gd.y_shape(), dtype=torch.int8, device="cuda")
+        g32 = torch.empty(gd.w_shape(), dtype=torch.int32, device="cuda")
+        niti.conv_fwd(gd, xd, wd, y, stats, relu=True, ws=ws, stats_index=0)
+        niti.conv_bwd_weight(gd, xd, dy, wd, stats, ws, g32_out=g32, mu=5, stats_index=1)
+        torch.cuda.synchronize()
+        res.append((host(y), host(g32), host(wd), niti.read_stats(stats)))
+    (y0, g0, w0, s0), (y1, g1, w1, s1) = res
+    assert (y0 == y1).all() and (g0 == g1).all() and (w0 == w1).all()
+    for i in (0, 1):
+        assert all(int(s0[i][f]) == int(s1[i][f]) for f in ("max_abs", "b", "bp", "flags")), i
+    assert y0.any() and g0.any()
 
 
 @pytest.mark.parametrize("case", STRIDE_CASES)
