@@ -41,10 +41,15 @@ def _i8(v):
 
 class IntNet:
     def __init__(self, specs, in_shape, batch, weights, w_exps, mu=5, mode=niti.PSR, grad_mode=None, sr_seed=0,
-                 drop_seed=0):
+                 drop_seed=0, streams=2):
         """in_shape = (h, w, c) of the NHWC input (c a multiple of 4 for convs);
         weights: list of int8 numpy arrays (KRSC for conv, [out][in] for fc),
-        one per weighted layer; w_exps: their static exponents."""
+        one per weighted layer; w_exps: their static exponents.  streams=2:
+        the weight gradients and updates run on a second stream beside the
+        back-propagation (each after the back-propagation that reads the same
+        weights), and the caller's stream waits for them at the end of the
+        step; streams=1: every call on the caller's stream, in the order of
+        Algorithm 1.  Results are the same either way."""
         import torch
         self.specs = list(specs)
         self.batch = batch
@@ -112,6 +117,13 @@ class IntNet:
         ws = max(ws, niti.workspace_bytes(niti.OP_INT_CE_LOSS, None, batch, n_cls))
         self.ws = niti.new_workspace(ws)
         self.err = torch.empty((batch, n_cls), dtype=torch.int8, device="cuda")
+        assert streams in (1, 2)
+        self.two = streams == 2
+        if self.two:
+            self.sB = torch.cuda.Stream()
+            self.ws_b = niti.new_workspace(ws)
+            self.ev_upd = torch.cuda.Event()
+            self.ev_bwd = [torch.cuda.Event() for _ in range(wi)]
 
     # -------------------------------------------------------------- forward
     def forward(self, x, s_x):
@@ -137,7 +149,10 @@ class IntNet:
 
     # -------------------------------------------------------------- backward
     def backward(self, err, mu):
+        import torch
         e = err.view(self.layers[-1]["y"].shape)
+        cur = torch.cuda.current_stream()
+        nw = sum(1 for L in self.layers if L["kind"] in ("conv", "fc"))
         for i in range(len(self.layers) - 1, -1, -1):
             L = self.layers[i]
             k = L["kind"]
@@ -169,9 +184,21 @@ class IntNet:
             if need_e_in:
                 niti.conv_bwd_data(d, e_v, w_v, ein_v, self.stats, self.ws, relu_src=m_v, mode=self.mode,
                                    stats_index=L["stats"] + 1)
-            niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws, mu=mu, mode=self.grad_mode,
-                                 stats_index=L["stats"] + 2)
+            if self.two:
+                # after the back-propagation that reads w (issued above on this
+                # stream) and everything that produced this layer's error
+                nw -= 1
+                niti.stream_record(self.ev_bwd[nw], cur)
+                niti.stream_wait(self.sB, self.ev_bwd[nw])
+                with torch.cuda.stream(self.sB):
+                    niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws_b, mu=mu, mode=self.grad_mode,
+                                         stats_index=L["stats"] + 2)
+            else:
+                niti.conv_bwd_weight(d, x_v, e_v, w_v, self.stats, self.ws, mu=mu, mode=self.grad_mode,
+                                     stats_index=L["stats"] + 2)
             e = L["e_in"]
+        if self.two:
+            niti.stream_record(self.ev_upd, self.sB)
 
     def step(self, x, s_x, labels, mu=None):
         """One training step; returns (logits, s_logits) of the forward pass.
@@ -181,6 +208,9 @@ class IntNet:
         niti.int_ce_loss_grad(logits.view(self.batch, n_cls), s_l, labels, self.err, self.stats, self.ws,
                               mode=self.mode, stats_index=self.loss_stats)
         self.backward(self.err, self.mu if mu is None else mu)
+        if self.two:
+            import torch
+            niti.stream_wait(torch.cuda.current_stream(), self.ev_upd)   # the updates, before anything after
         self.t += 1
         return logits, s_l
 

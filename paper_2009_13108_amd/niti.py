@@ -252,6 +252,30 @@ class recording:
         return False
 
 
+def _kept(fn):
+    """A recorded non-library operation: runs fn and reports success."""
+    def run():
+        fn()
+        return 0
+    return run
+
+
+def stream_record(event, stream):
+    """Record a torch event on a stream (ordering work across streams); kept
+    in an active recording, so that replay() issues it again in place."""
+    event.record(stream)
+    if _recorder is not None:
+        _recorder.append((_kept(lambda: event.record(stream)), (), "event record"))
+
+
+def stream_wait(stream, event):
+    """Make a stream wait for an event's last record; kept in an active
+    recording like stream_record."""
+    stream.wait_event(event)
+    if _recorder is not None:
+        _recorder.append((_kept(lambda: stream.wait_event(event)), (), "event wait"))
+
+
 def replay(calls):
     """Reissue recorded calls (see recording); raises on the first error."""
     for f, args, name in calls:

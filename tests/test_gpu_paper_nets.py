@@ -83,6 +83,30 @@ def test_paper_network_training_steps(case):
         assert not got[0][6:].any() and not got[1][..., 6:].any()    # the padding filters stay zero
 
 
+@pytest.mark.parametrize("name", ["lenet5", "vgg_small7"])
+def test_two_streams_equal_one_stream(name):
+    """The step with the weight gradients on a second stream leaves exactly
+    the logits, exponents and weights of the single-stream step (every
+    call in Algorithm 1's order), step after step."""
+    import torch
+    specs, hw, img_c, batch = (M.LENET5, 28, 1, 16) if name == "lenet5" else (M.vgg_small(7), 32, 3, 8)
+    say("streams", name, batch)
+    px, labels, w_gpu, _, exps, _ = _setup(specs, hw, img_c, batch, 70)
+    nets = [M.IntNet(specs, (hw, hw, 4), batch, [w.copy() for w in w_gpu], exps, drop_seed=5, streams=k)
+            for k in (1, 2)]
+    x = torch.empty((batch, hw, hw, 4), dtype=torch.int8, device="cuda")
+    niti.quantize_u8(dev(px), x)
+    lab = dev(labels)
+    s0 = torch.tensor([-7], dtype=torch.int8, device="cuda")
+    for step in range(3):
+        out = [net.step(x, s0, lab) for net in nets]
+        torch.cuda.synchronize()
+        assert (host(out[0][0]) == host(out[1][0])).all(), "logits step %d" % step
+        assert int(host(out[0][1])[0]) == int(host(out[1][1])[0])
+        for a, b in zip(nets[0].weights(), nets[1].weights()):
+            assert (host(a) == host(b)).all(), "weights step %d" % step
+
+
 ALEX = [(n, ci, co, k, st, pd, hw, 2) for (n, ci, co, k, st, pd, hw) in M.ALEXNET_LAYERS]
 ALEX += [(n, fi, fo, 1, 1, 0, 1, 4) for (n, fi, fo) in M.ALEXNET_FC]
 

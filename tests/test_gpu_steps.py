@@ -159,8 +159,8 @@ def test_graph_replay_matches_eager():
     batch = 8
     say("graph replay vgg", batch)
     px, labels, w_orc, w_gpu, exps = _vgg_setup(batch)
-    eager = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps)
-    graphed = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps)
+    eager = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps, streams=1)
+    graphed = M.IntNet(M.VGG_32, (32, 32, 4), batch, [w.copy() for w in w_gpu], exps, streams=1)
     x = torch.empty((batch, 32, 32, 4), dtype=torch.int8, device="cuda")
     niti.quantize_u8(dev(px), x)
     lab = dev(labels)
