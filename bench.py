@@ -41,55 +41,9 @@ PEAK_INT8_TOPS = 5000.0       # MI355X dense int8 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
-class StreamEvent:
-    """An event that orders two streams of this device: created without
-    timing and without the system-scope fence (hipEventDisableSystemFence),
-    so recording it releases at device scope only, which is all another
-    stream of the same device needs (the host waits with a device
-    synchronisation).  Calls go to the HIP runtime torch already loaded."""
-    _hip = None
-
-    @classmethod
-    def hip(cls):
-        if cls._hip is None:
-            import ctypes
-            path = None
-            with open("/proc/self/maps") as f:
-                for line in f:
-                    if "libamdhip64" in line:
-                        path = line.split()[-1]
-                        break
-            if path is None:
-                raise RuntimeError("the HIP runtime is not loaded")
-            lib = ctypes.CDLL(path)
-            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
-            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-            lib.hipStreamWaitEvent.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint]
-            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
-            cls._hip = lib
-        return cls._hip
-
-    def __init__(self):
-        import ctypes
-        self.h = ctypes.c_void_p()
-        rc = self.hip().hipEventCreateWithFlags(ctypes.byref(self.h), 0x2 | 0x20000000)
-        if rc != 0:
-            raise RuntimeError("hipEventCreateWithFlags failed (%d)" % rc)
-
-    def record(self, stream):
-        rc = self.hip().hipEventRecord(self.h, stream.cuda_stream)
-        if rc != 0:
-            raise RuntimeError("hipEventRecord failed (%d)" % rc)
-
-    def wait(self, stream):
-        """Make stream wait for the last record of this event."""
-        rc = self.hip().hipStreamWaitEvent(stream.cuda_stream, self.h, 0)
-        if rc != 0:
-            raise RuntimeError("hipStreamWaitEvent failed (%d)" % rc)
-
-    def __del__(self):
-        if self._hip is not None and self.h:
-            self._hip.hipEventDestroy(self.h)
+def _stream_event():
+    from paper_2009_13108_amd.stream_event import StreamEvent
+    return StreamEvent()
 
 
 def conv_macs(n, c, h, w, k, r, s, st, pd):
@@ -181,11 +135,11 @@ class ResNetStep:
         # image layer's filter is updated on A).
         self.sA = torch.cuda.Stream()
         self.sB = torch.cuda.Stream()
-        self.ev_bwd = [StreamEvent() for _ in range(sum(L["count"] for L in self.layers) + 1)]
-        self.ev_fwd = [StreamEvent() for _ in range(8)]
-        self.ev_upd = StreamEvent()
-        self.ev_pack = StreamEvent()
-        self.ev_tail = StreamEvent()
+        self.ev_bwd = [_stream_event() for _ in range(sum(L["count"] for L in self.layers) + 1)]
+        self.ev_fwd = [_stream_event() for _ in range(8)]
+        self.ev_upd = _stream_event()
+        self.ev_pack = _stream_event()
+        self.ev_tail = _stream_event()
         self.ev_upd.record(self.sB)
         self.ev_tail.record(self.sA)
         # The weight gradients of the last a_tail layers before the image

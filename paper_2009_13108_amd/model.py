@@ -122,8 +122,9 @@ class IntNet:
         if self.two:
             self.sB = torch.cuda.Stream()
             self.ws_b = niti.new_workspace(ws)
-            self.ev_upd = torch.cuda.Event()
-            self.ev_bwd = [torch.cuda.Event() for _ in range(wi)]
+            from .stream_event import StreamEvent
+            self.ev_upd = StreamEvent()
+            self.ev_bwd = [StreamEvent() for _ in range(wi)]
 
     # -------------------------------------------------------------- forward
     def forward(self, x, s_x):

@@ -261,8 +261,9 @@ def _kept(fn):
 
 
 def stream_record(event, stream):
-    """Record a torch event on a stream (ordering work across streams); kept
-    in an active recording, so that replay() issues it again in place."""
+    """Record an event (torch.cuda.Event or stream_event.StreamEvent) on a
+    stream, to order work across streams; kept in an active recording, so
+    that replay() issues it again in place."""
     event.record(stream)
     if _recorder is not None:
         _recorder.append((_kept(lambda: event.record(stream)), (), "event record"))
@@ -271,9 +272,9 @@ def stream_record(event, stream):
 def stream_wait(stream, event):
     """Make a stream wait for an event's last record; kept in an active
     recording like stream_record."""
-    stream.wait_event(event)
+    event.wait(stream)
     if _recorder is not None:
-        _recorder.append((_kept(lambda: stream.wait_event(event)), (), "event wait"))
+        _recorder.append((_kept(lambda: event.wait(stream)), (), "event wait"))
 
 
 def replay(calls):
