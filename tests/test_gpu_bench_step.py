@@ -2,7 +2,8 @@
 stream, calls marshalled once and replayed) leaves exactly the state that
 the same calls issued one after another on one stream leave: every weight,
 every output buffer the serial step also writes, and every statistics
-block, after several steps."""
+block, after several steps, at a small batch and at the benchmark's batch of 128
+(its exact launch configuration: tiles, splits, grids)."""
 import numpy as np
 import pytest
 
@@ -11,8 +12,7 @@ from helpers import FLAG_HINT_MISS, host, say
 
 pytestmark = pytest.mark.gpu
 
-STEPS = 3
-BATCH = 8
+CASES = [(8, 3), (128, 2)]   # batch, steps
 
 
 def _state(job):
@@ -35,9 +35,11 @@ def _stats(job):
     return [(s["max_abs"], s["b"], s["bp"], s["flags"] & ~FLAG_HINT_MISS, s["s_out"], s["calls"]) for s in st]
 
 
-def test_two_stream_prepared_steps_equal_serial_steps():
+@pytest.mark.parametrize("case", CASES, ids=["batch%d" % c[0] for c in CASES])
+def test_two_stream_prepared_steps_equal_serial_steps(case):
     import torch
     import bench
+    BATCH, STEPS = case
     say("bench step: two streams vs serial, batch", BATCH, "steps", STEPS)
     par = bench.ResNetStep(batch=BATCH)
     ser = bench.ResNetStep(batch=BATCH)
