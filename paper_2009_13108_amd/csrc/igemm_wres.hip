@@ -87,15 +87,17 @@ __device__ __forceinline__ uint4 wr_round_fragment(const v16i& acc, const RoundK
 }
 
 // Write 16 rounded channels (nv <= 16 valid) at out + off, with the
-// backward ReLU mask (a byte is kept where the mask byte is positive).
-__device__ __forceinline__ void wr_store16(const IgemmProblem& P, int64_t off, uint4 v, int nv) {
+// backward ReLU mask (a byte is kept where the mask byte is positive);
+// have_m: mpre holds the 16 mask bytes at off, loaded earlier.
+__device__ __forceinline__ void wr_store16(const IgemmProblem& P, int64_t off, uint4 v, int nv,
+                                           bool have_m = false, uint4 mpre = make_uint4(0, 0, 0, 0)) {
     int8_t* dst = P.out + off;
     const bool full = nv == 16 && (((uintptr_t)dst) & 15) == 0;
     if (P.mask) {
         const int8_t* ms = P.mask + off;
         uint32_t mw[4];
         if (full) {
-            const uint4 mv = *(const uint4*)ms;
+            const uint4 mv = have_m ? mpre : *(const uint4*)ms;
             mw[0] = mv.x; mw[1] = mv.y; mw[2] = mv.z; mw[3] = mv.w;
         } else {
             for (int q = 0; q < 4; q++) mw[q] = 0;
@@ -280,6 +282,33 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
         for (int a = 0; a < NF; a++)
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[a][e] = 0;
+        // output offset of pixel t*32 + lane%32 (channels a*32 + 16*hi ..
+        // + 15), and, for a back-propagation, the ReLU mask bytes there,
+        // loaded now so that they arrive during the task's MFMAs
+        const int m = t * 32 + (lane & 31);
+        int64_t ooff = -1;
+        if (m < P.M) {
+            if (dense) {
+                ooff = (int64_t)m * P.ldo;
+            } else {
+                const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
+                const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
+                const uint32_t i0 = fdiv(rem, P.div_ow);
+                const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
+                const int oh = (int)i0 * P.os + P.oa;
+                const int ow = (int)j0 * P.os + P.ob;
+                ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
+            }
+        }
+        uint4 mpre[NF];
+        bool mok[NF];
+#pragma unroll
+        for (int a = 0; a < NF; a++) {
+            const int n0 = a * 32 + 16 * hi;
+            mok[a] = do_store && P.mask && ooff >= 0 && n0 + 16 <= P.Nout &&
+                     (((uintptr_t)(P.mask + ooff + n0)) & 15) == 0 && (((uintptr_t)(P.out + ooff + n0)) & 15) == 0;
+            mpre[a] = mok[a] ? *(const uint4*)(P.mask + ooff + n0) : make_uint4(0, 0, 0, 0);
+        }
         for (int g = 0; g < groups; g++) {
             // the loads issued in this group are for the next task's first steps
             if (g == groups - 1) next_task_cursor(t + tl.step);
@@ -306,22 +335,7 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
             }
         }
         if (t + tl.step >= tl.end && snap_st && threadIdx.x == 0) snap = load_acc(snap_st, snap_slot);
-        // epilogue: pixel t*32 + lane%32, channels a*32 + 16*hi .. + 15
-        const int m = t * 32 + (lane & 31);
-        int64_t ooff = -1;
-        if (m < P.M) {
-            if (dense) {
-                ooff = (int64_t)m * P.ldo;
-            } else {
-                const uint32_t img = fdiv((uint32_t)m, P.div_ohw);
-                const uint32_t rem = (uint32_t)m - img * (uint32_t)(P.OHc * P.OWc);
-                const uint32_t i0 = fdiv(rem, P.div_ow);
-                const uint32_t j0 = rem - i0 * (uint32_t)P.OWc;
-                const int oh = (int)i0 * P.os + P.oa;
-                const int ow = (int)j0 * P.os + P.ob;
-                ooff = (((int64_t)img * P.OH + oh) * P.OW + ow) * P.ldo;
-            }
-        }
+        // epilogue
         uint32_t mx = 0;
 #pragma unroll
         for (int a = 0; a < NF; a++) {
@@ -333,7 +347,8 @@ __device__ __forceinline__ void wres_tasks(const IgemmProblem& P, const TaskList
                 default: v = wr_round_fragment<true, true, false>(acc[a], rk, mx); break;
             }
             const int n0 = a * 32 + 16 * hi;
-            if (do_store && ooff >= 0 && n0 < P.Nout) wr_store16(P, ooff + n0, v, min(16, P.Nout - n0));
+            if (do_store && ooff >= 0 && n0 < P.Nout)
+                wr_store16(P, ooff + n0, v, min(16, P.Nout - n0), mok[a], mpre[a]);
         }
         if (do_max) tmax = mx > tmax ? mx : tmax;
     }
