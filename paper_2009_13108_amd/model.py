@@ -39,6 +39,20 @@ def _i8(v):
     return torch.tensor([int(v)], dtype=torch.int8, device="cuda")
 
 
+_SIDE = None
+
+
+def side_stream():
+    """The second stream of IntNet steps, one per process: streams beyond the
+    device's few hardware queues share queues and then order each other's
+    work, so the networks of a process share this one."""
+    global _SIDE
+    if _SIDE is None:
+        import torch
+        _SIDE = torch.cuda.Stream()
+    return _SIDE
+
+
 class IntNet:
     def __init__(self, specs, in_shape, batch, weights, w_exps, mu=5, mode=niti.PSR, grad_mode=None, sr_seed=0,
                  drop_seed=0, streams=2):
@@ -120,7 +134,7 @@ class IntNet:
         assert streams in (1, 2)
         self.two = streams == 2
         if self.two:
-            self.sB = torch.cuda.Stream()
+            self.sB = side_stream()
             self.ws_b = niti.new_workspace(ws)
             from .stream_event import StreamEvent
             self.ev_upd = StreamEvent()
