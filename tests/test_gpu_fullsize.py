@@ -118,6 +118,46 @@ def test_resnet18_layer_fullsize(rec):
         assert _stats_ok(g[2], rec["bwd_weight"]) and sha(w) == rec["bwd_weight"]["sha256_w"], ("update", rep)
 
 
+def test_resnet18_bordered_image_layer_fullsize():
+    """The image layer as bench.py runs it: the batch stored with its 3-pixel
+    zero border (230 x 230) and a descriptor without padding, read in place.
+    The forward output and the weight gradient and update must be the
+    oracle's digests of the padded 224 x 224 layer."""
+    import torch
+    recs = [c for c in _c4_layer_cases() if c["layer"].startswith("stem")]
+    if not recs:
+        pytest.skip("fullsize_c4.json not generated")
+    rec = recs[0]
+    li = rec["li"]
+    name, cin, cout, k, st, pd, hw, count = M.RESNET18_LAYERS[li]
+    say("c4 bordered image layer", name)
+    B = 128
+    dp = niti.ConvDesc.make(B, hw, hw, cin, cout, k, k, st, pd)
+    x = I.activations(I.base_seed(4, 100 + li), dp.x_shape(), device="cuda")
+    dy = I.errors8(I.base_seed(4, 200 + li), dp.y_shape(), device="cuda")
+    w = I.weights(I.base_seed(4, 1000 + 10 * li), dp.w_shape(), device="cuda")
+    x[..., 3:] = 0
+    w[..., 3:] = 0
+    hb = hw + 2 * pd
+    xb = torch.zeros((B, hb, hb, cin), dtype=torch.int8, device="cuda")
+    xb[:, pd:pd + hw, pd:pd + hw] = x
+    del x
+    d = niti.ConvDesc.make(B, hb, hb, cin, cout, k, k, st, 0)
+    assert d.y_shape() == dp.y_shape()
+    stats = niti.new_stats(3)
+    y = torch.empty(d.y_shape(), dtype=torch.int8, device="cuda")
+    g32 = torch.empty(d.w_shape(), dtype=torch.int32, device="cuda")
+    ws = niti.new_workspace(max(niti.workspace_bytes(niti.OP_CONV_FWD, d),
+                                niti.workspace_bytes(niti.OP_CONV_BWD_WEIGHT, d)))
+    niti.conv_fwd(d, xb, w, y, stats, relu=True, stats_index=0, ws=ws)
+    niti.conv_bwd_weight(d, xb, dy, w, stats, ws, g32_out=g32, mu=5, stats_index=2)
+    torch.cuda.synchronize()
+    g = niti.read_stats(stats)
+    assert _stats_ok(g[0], rec["fwd"]) and sha(y) == rec["fwd"]["sha256"]
+    assert sha(g32) == rec["bwd_weight"]["sha256_g32"]
+    assert _stats_ok(g[2], rec["bwd_weight"]) and sha(w) == rec["bwd_weight"]["sha256_w"]
+
+
 def test_resnet18_head_and_loss_fullsize():
     import torch
     cases = [c for c in _load("fullsize_c4.json") if c["layer"] == "fc"]
